@@ -1,0 +1,193 @@
+"""CPU checker for the COLD scoring path -- test infrastructure only.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It wraps ``cold_oracle.c`` (plain
+double-precision C, see that file for the steps and the paper passages they
+follow) with ctypes, takes plain numpy arrays, and shares no code with the
+HIP library.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcold_oracle.so")
+SRC_PATH = os.path.join(_HERE, "cold_oracle.c")
+
+DTYPES = {"f32": 0, "bf16": 1, "f16": 2}
+
+
+def build(force: bool = True) -> str:
+    """Compile the checker with gcc (-O2, no fast-math, OpenMP)."""
+    if force or not os.path.exists(LIB_PATH):
+        tmp = LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                               "-Wall", "-Wextra", "-o", tmp, SRC_PATH, "-lm"])
+        os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("n_requests", ctypes.c_int64), ("n_rows", ctypes.c_int64),
+        ("n_user", ctypes.c_int32), ("n_seq", ctypes.c_int32),
+        ("n_ad", ctypes.c_int32), ("n_cross", ctypes.c_int32),
+        ("emb_dim", ctypes.c_int32), ("se_hidden", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("hashed", ctypes.c_int32),
+        ("linear_log", ctypes.c_int32), ("topk_k", ctypes.c_int32),
+        ("n_layers", ctypes.c_int32),
+        ("widths", ctypes.c_void_p), ("table_rows", ctypes.c_void_p),
+        ("tables", ctypes.c_void_p),
+        ("se_w1", ctypes.c_void_p), ("se_b1", ctypes.c_void_p),
+        ("se_w2", ctypes.c_void_p), ("se_b2", ctypes.c_void_p),
+        ("mlp_w", ctypes.c_void_p), ("mlp_b", ctypes.c_void_p),
+        ("req_off", ctypes.c_void_p), ("user_ids", ctypes.c_void_p),
+        ("ad_ids", ctypes.c_void_p), ("cross_ids", ctypes.c_void_p),
+        ("seq_off", ctypes.c_void_p), ("seq_ids", ctypes.c_void_p),
+        ("n_seq_ids", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        L.orc_score.restype = ctypes.c_int
+        L.orc_score.argtypes = [ctypes.POINTER(_Problem), ctypes.c_void_p, ctypes.c_int64,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_int]
+        L.orc_linear_log.restype = ctypes.c_double
+        L.orc_linear_log.argtypes = [ctypes.c_double]
+        L.orc_mix64.restype = ctypes.c_uint64
+        L.orc_mix64.argtypes = [ctypes.c_uint64]
+        L.orc_hash_row.restype = ctypes.c_uint64
+        L.orc_hash_row.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint64]
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+_ERRORS = {-1: "bad argument", -2: "id out of range", -3: "out of memory"}
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def linear_log(x: float) -> float:
+    return lib().orc_linear_log(float(x))
+
+
+def mix64(z: int) -> int:
+    return int(lib().orc_mix64(z & 0xFFFFFFFFFFFFFFFF))
+
+
+def hash_row(raw: int, g: int, rows: int) -> int:
+    return int(lib().orc_hash_row(raw & 0xFFFFFFFFFFFFFFFF, g, rows))
+
+
+def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
+          want_rows=False, want_s=False, want_x=False, n_threads=None) -> dict:
+    """Score rows of a batch.
+
+    dims: n_user, n_seq, n_ad, n_cross, emb_dim, se_hidden, dtype ('f32' |
+      'bf16' | 'f16'), hashed, linear_log, topk_k, widths.
+    tables: list of M arrays [rows][d] in stored form (float32, float16, or
+      uint16 bf16 bit patterns).
+    params: se_w1 [H][M], se_b1, se_w2 [M][H], se_b2 (float32); mlp_w list of
+      [out][in] arrays in stored form; mlp_b list of float32 [out].
+    batch: req_off, user_ids, ad_ids, cross_ids, seq_off, seq_ids.
+    sample: row indices to score (default: every row).
+
+    Returns a dict with 'scores' and, on request, 'rows', 's', 'x', and (when
+    topk_k > 0) 'importance' and 'mask' per request.
+    """
+    L = lib()
+    m = dims["n_user"] + dims["n_seq"] + dims["n_ad"] + dims["n_cross"]
+    d = dims["emb_dim"]
+    hashed = bool(dims["hashed"])
+    id_dt = np.uint64 if hashed else np.int32
+    keep = []
+
+    def arr(a, dt):
+        a = np.ascontiguousarray(a, dtype=dt)
+        keep.append(a)
+        return a
+
+    widths = arr(dims["widths"], np.int32)
+    n_layers = len(widths) - 1
+    req_off = arr(batch["req_off"], np.int32)
+    q = len(req_off) - 1
+    r = int(req_off[-1])
+    tabs = [np.ascontiguousarray(t) for t in tables]
+    keep.extend(tabs)
+    assert len(tabs) == m
+    for t in tabs:
+        assert t.ndim == 2 and t.shape[1] == d
+    table_rows = arr([t.shape[0] for t in tabs], np.int64)
+    table_ptrs = arr([t.ctypes.data for t in tabs], np.uint64)
+    mlp_w = [np.ascontiguousarray(w) for w in params["mlp_w"]]
+    mlp_b = [np.ascontiguousarray(b, dtype=np.float32) for b in params["mlp_b"]]
+    keep.extend(mlp_w)
+    keep.extend(mlp_b)
+    w_ptrs = arr([w.ctypes.data for w in mlp_w], np.uint64)
+    b_ptrs = arr([b.ctypes.data for b in mlp_b], np.uint64)
+    se_w1 = arr(params["se_w1"], np.float32)
+    se_b1 = arr(params["se_b1"], np.float32)
+    se_w2 = arr(params["se_w2"], np.float32)
+    se_b2 = arr(params["se_b2"], np.float32)
+    user_ids = arr(np.asarray(batch["user_ids"]).reshape(dims["n_user"], q), id_dt)
+    ad_ids = arr(np.asarray(batch["ad_ids"]).reshape(dims["n_ad"], r), id_dt)
+    cross_ids = arr(np.asarray(batch["cross_ids"]).reshape(dims["n_cross"], r), id_dt)
+    seq_off = arr(batch.get("seq_off", np.zeros(1, np.int32)), np.int32)
+    seq_ids = arr(batch.get("seq_ids", np.zeros(0, id_dt)), id_dt)
+    if seq_ids.size == 0:
+        seq_ids = arr(np.zeros(1, id_dt), id_dt)
+        n_seq_ids = 0
+    else:
+        n_seq_ids = seq_ids.size
+    prob = _Problem(
+        n_requests=q, n_rows=r, n_user=dims["n_user"], n_seq=dims["n_seq"],
+        n_ad=dims["n_ad"], n_cross=dims["n_cross"], emb_dim=d,
+        se_hidden=dims["se_hidden"], dtype=DTYPES[dims["dtype"]], hashed=int(hashed),
+        linear_log=int(bool(dims["linear_log"])), topk_k=int(dims.get("topk_k", 0)),
+        n_layers=n_layers, widths=_ptr(widths), table_rows=_ptr(table_rows),
+        tables=_ptr(table_ptrs), se_w1=_ptr(se_w1), se_b1=_ptr(se_b1), se_w2=_ptr(se_w2),
+        se_b2=_ptr(se_b2), mlp_w=_ptr(w_ptrs), mlp_b=_ptr(b_ptrs), req_off=_ptr(req_off),
+        user_ids=_ptr(user_ids), ad_ids=_ptr(ad_ids), cross_ids=_ptr(cross_ids),
+        seq_off=_ptr(seq_off), seq_ids=_ptr(seq_ids), n_seq_ids=n_seq_ids)
+    sample = arr(np.arange(r) if sample is None else sample, np.int64)
+    n = sample.size
+    out = {"scores": np.zeros(n, np.float64)}
+    if want_rows:
+        out["rows"] = np.zeros((n, m), np.int64)
+    if want_s:
+        out["s"] = np.zeros((n, m), np.float64)
+    if want_x:
+        out["x"] = np.zeros((n, m * d), np.float64)
+    topk = int(dims.get("topk_k", 0)) > 0
+    if topk:
+        out["importance"] = np.zeros((q, m), np.float64)
+        out["mask"] = np.zeros((q, m), np.uint8)
+    if n_threads is None:
+        n_threads = len(os.sched_getaffinity(0))
+    st = L.orc_score(ctypes.byref(prob), _ptr(sample), n, _ptr(out["scores"]),
+                     _ptr(out.get("rows")), _ptr(out.get("s")), _ptr(out.get("x")),
+                     _ptr(out.get("importance")), _ptr(out.get("mask")), int(n_threads))
+    if st != 0:
+        raise OracleError(_ERRORS.get(st, f"status {st}"))
+    out["n_threads"] = n_threads
+    return out
