@@ -1,0 +1,173 @@
+/*
+ * cold.h -- C ABI of libcold.so, the MI355X (gfx950) scoring path of COLD,
+ * the pre-ranking system of Wang et al., "COLD: Towards the Next Generation
+ * of Pre-Ranking System" (DLP-KDD 2020).
+ *
+ * One call scores every candidate ad of a batch of requests with one deep
+ * CTR model (Section 2, Section 3.1): per (user, ad) row it gathers the user,
+ * ad and user x ad cross feature-group embeddings, sum-pools multi-valued
+ * groups (Section 3.3, low precision), weights every group by its SE
+ * importance (Section 3.2, Eq. 2), optionally keeps only the top-k groups
+ * (Section 3.2, feature group selection), optionally applies linear_log to
+ * the network input (Section 3.3, Eq. 3), and runs the fully connected
+ * network D_in x ... x n_out down to a CTR (Section 4.1).
+ *
+ * Memory: every pointer marked "device" is device memory owned by the
+ * caller; the library never allocates device memory.  Pointers marked "host"
+ * are read during the call only.  Streams are hipStream_t values passed as
+ * void* (NULL = the null stream).  Work is enqueued asynchronously on that
+ * stream unless stated otherwise.
+ *
+ * Errors: every entry point returns COLD_OK (0) or a negative status; no
+ * exception crosses the ABI.  Host-side checks run before anything is
+ * enqueued, so a rejected call has no device side effect.
+ * cold_last_error() gives the message of the model's last failure.
+ *
+ * Threading: a cold_model may be used by concurrent cold_score calls on
+ * different streams with distinct workspaces; cold_load_weights must not
+ * race with cold_score on the same model.
+ */
+#ifndef COLD_H
+#define COLD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+#define COLD_OK 0
+#define COLD_ERR_INVALID_ARG (-1)    /* null pointer, negative size, bad flag */
+#define COLD_ERR_SHAPE (-2)          /* inconsistent dimensions */
+#define COLD_ERR_DTYPE (-3)          /* unsupported dtype / id kind / dim */
+#define COLD_ERR_NOT_LOADED (-4)     /* cold_score before cold_load_weights */
+#define COLD_ERR_WORKSPACE (-5)      /* workspace or arena too small */
+#define COLD_ERR_HIP (-6)            /* a HIP runtime call failed */
+#define COLD_ERR_ID_RANGE (-7)       /* validate mode: an id or offset was out of range */
+
+/* storage and compute type of embedding tables and MLP weights */
+#define COLD_F32 0
+#define COLD_BF16 1
+#define COLD_F16 2
+
+/* id columns: int32 row ids used as-is (must be < table rows), or raw
+ * uint64 ids hashed into the table: row = mix64(raw ^ salt_g) mod rows, with
+ * mix64 the SplitMix64 output function and salt_g = (g+1) * 0x9e3779b97f4a7c15
+ * for feature group g.  (The paper does not describe id hashing.) */
+#define COLD_IDS_DIRECT_I32 0
+#define COLD_IDS_HASHED_U64 1
+
+/* cold_score flags */
+#define COLD_SCORE_VALIDATE 1        /* synchronise and report out-of-range ids */
+
+/* Model description (host memory, copied by cold_create_model).
+ * Feature groups are one per field, concatenated in the order user
+ * (single-valued), user behaviour sequence (sum-pooled), ad, cross; group g
+ * uses table g.  M = n_user + n_seq + n_ad + n_cross, D_in = M * emb_dim.
+ * The SE block has H = max(1, M / se_reduction) hidden units.
+ * widths[0] = D_in; widths[1..n_layers-1] are ReLU hidden layers;
+ * widths[n_layers] is 1 (CTR = sigmoid) or 2 (softmax, CTR = class 1).
+ * Supported: emb_dim * sizeof(dtype) a multiple of 16 bytes, M <= 1024,
+ * hidden widths multiples of 8 (bf16/f16), last hidden width <= 1024. */
+typedef struct cold_model_desc {
+  int32_t n_user, n_seq, n_ad, n_cross;
+  int32_t emb_dim;
+  int32_t id_kind;          /* COLD_IDS_* */
+  int32_t dtype;            /* COLD_F32 | COLD_BF16 | COLD_F16 */
+  int32_t se_reduction;     /* >= 1 */
+  int32_t n_layers;         /* >= 1 */
+  const int32_t *widths;    /* host [n_layers + 1] */
+  const int64_t *table_rows;/* host [M], rows of each table, 1 .. 2^31-1 */
+  int32_t linear_log;       /* 0/1: apply Eq. 3 to the network input */
+  int32_t topk_k;           /* 0: off; else keep the k most important groups per request */
+} cold_model_desc;
+
+typedef struct cold_model cold_model;
+
+/* Parameters (cold_load_weights).  Tables are used in place (not copied) and
+ * must stay alive while the model scores; the rest is copied into the arena.
+ *   tables[g]   device [table_rows[g]][emb_dim], dtype, 16-byte aligned
+ *   se_w1       device fp32 [H][M]      se_b1 device fp32 [H]
+ *   se_w2       device fp32 [M][H]      se_b2 device fp32 [M]
+ *   mlp_w[l]    device [widths[l+1]][widths[l]] (out x in), dtype
+ *   mlp_b[l]    device fp32 [widths[l+1]]                                  */
+typedef struct cold_weights {
+  const void *const *tables;    /* host array [M] of device pointers */
+  const float *se_w1, *se_b1, *se_w2, *se_b2;
+  const void *const *mlp_w;     /* host array [n_layers] of device pointers */
+  const float *const *mlp_b;    /* host array [n_layers] of device pointers */
+} cold_weights;
+
+/* One batch of requests in the column (field-major) layout of Section 3.3.
+ * Q = n_requests, R = n_rows; rows of request q are req_off[q] .. req_off[q+1]-1.
+ * Id element type is int32 (COLD_IDS_DIRECT_I32) or uint64 (HASHED_U64).
+ *   req_off    device int32 [Q + 1], non-decreasing, req_off[0] = 0, req_off[Q] = R
+ *   user_ids   device [n_user][Q]
+ *   ad_ids     device [n_ad][R]
+ *   cross_ids  device [n_cross][R]
+ *   seq_off    device int32 [n_seq * Q + 1]; ids of sequence field f of request q
+ *              are seq_ids[seq_off[f*Q + q] .. seq_off[f*Q + q + 1] - 1]
+ *   seq_ids    device [n_seq_ids]
+ * Empty requests and empty sequences (pooled to zero) are allowed. */
+typedef struct cold_batch {
+  int64_t n_requests;
+  int64_t n_rows;
+  int64_t n_seq_ids;
+  const int32_t *req_off;
+  const void *user_ids;
+  const void *ad_ids;
+  const void *cross_ids;
+  const int32_t *seq_off;
+  const void *seq_ids;
+} cold_batch;
+
+/* Validate a model description and create the host-side model.  CPU only.
+ * *out receives a library-owned handle (free with cold_destroy_model). */
+int cold_create_model(const cold_model_desc *desc, cold_model **out);
+
+/* Free the host-side model (never device memory).  NULL is a no-op. */
+void cold_destroy_model(cold_model *model);
+
+/* Bytes of device memory the caller must provide as the weight arena. */
+size_t cold_weight_arena_bytes(const cold_model *model);
+
+/* Bytes of device workspace cold_score needs for up to max_rows rows and
+ * max_requests requests (0 if the model is NULL or a size is negative). */
+size_t cold_workspace_bytes(const cold_model *model, int64_t max_rows, int64_t max_requests);
+
+/* Register the tables and copy SE and MLP parameters into `arena` (device,
+ * 256-byte aligned, >= cold_weight_arena_bytes).  Callable repeatedly (an
+ * online model update); ordered on `stream`, and returns after the copies
+ * have completed.  The arena must stay alive while the model scores. */
+int cold_load_weights(cold_model *model, const cold_weights *w, void *arena,
+                      size_t arena_bytes, void *stream);
+
+/* Score every row of batch b (Sections 3.1-3.3; Section 4.1 network).
+ *   workspace   device, 256-byte aligned, ws_bytes >= cold_workspace_bytes(R, Q)
+ *   scores      device fp32 [R]: CTR of each row
+ *   importance  device fp32 [R][M] or NULL: SE weights s of each row (Eq. 2),
+ *               before any top-k mask
+ *   group_mask  device uint8 [Q][M] or NULL: kept groups per request (topk_k > 0)
+ *   rows_out    device int32 [M][R] or NULL: table row each single-valued group
+ *               of each row resolved to (-1 for sequence groups)
+ *   flags       0 or COLD_SCORE_VALIDATE (then the call synchronises the stream
+ *               and returns COLD_ERR_ID_RANGE if any id or offset was out of range;
+ *               without it such ids read a zero embedding)
+ * Asynchronous on `stream` unless validating.  Q = 0 or R = 0 is a no-op. */
+int cold_score(cold_model *model, const cold_batch *b, void *workspace, size_t ws_bytes,
+               float *scores, float *importance, uint8_t *group_mask, int32_t *rows_out,
+               int32_t flags, void *stream);
+
+/* Static text of a status code. */
+const char *cold_status_string(int status);
+
+/* Message of the last failed call on this model ("" if none; a static
+ * message if model is NULL). */
+const char *cold_last_error(const cold_model *model);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* COLD_H */

@@ -1,0 +1,344 @@
+// api.hip -- the C ABI of libcold.so (declared in include/cold.h): model
+// description checks, weight arena and workspace layout, and the launch
+// sequence of one scoring call.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "cold.h"
+#include "cold_internal.h"
+
+using namespace cold;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct ArenaLayout {
+  size_t tables, rows, magic, w1, b1, w2, b2;
+  std::vector<size_t> w, b;
+  size_t total;
+};
+
+struct WorkLayout {
+  size_t err, U, urow, X, actA, actB, sbuf, partial, mask, total;
+};
+
+}  // namespace
+
+struct cold_model {
+  cold_model_desc desc;
+  std::vector<int32_t> widths;
+  std::vector<int64_t> table_rows;
+  int M, D_in, H, d, dtype, es, nus, hashed;
+  int max_hidden;
+  ArenaLayout arena;
+  unsigned char *arena_ptr = nullptr;
+  bool loaded = false;
+  std::vector<uint64_t> host_tables;  // staging for the arena's pointer table
+  std::vector<uint64_t> host_magic;
+  mutable std::mutex mu;
+  std::string last_error;
+};
+
+namespace {
+
+int fail(cold_model *m, int status, const char *fmt, ...) __attribute__((format(printf, 3, 4)));
+int fail(cold_model *m, int status, const char *fmt, ...) {
+  if (m) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->last_error = buf;
+  }
+  return status;
+}
+
+int hip_fail(cold_model *m, hipError_t e, const char *what) {
+  return fail(m, COLD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+ArenaLayout arena_layout(const cold_model &m) {
+  ArenaLayout a;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  a.tables = take(sizeof(uint64_t) * m.M);
+  a.rows = take(sizeof(int64_t) * m.M);
+  a.magic = take(sizeof(uint64_t) * m.M);
+  a.w1 = take(sizeof(float) * m.H * m.M);
+  a.b1 = take(sizeof(float) * m.H);
+  a.w2 = take(sizeof(float) * m.M * m.H);
+  a.b2 = take(sizeof(float) * m.M);
+  const int L = m.desc.n_layers;
+  for (int l = 0; l < L; ++l) {
+    a.w.push_back(take((size_t)m.es * m.widths[l] * m.widths[l + 1]));
+    a.b.push_back(take(sizeof(float) * m.widths[l + 1]));
+  }
+  a.total = off;
+  return a;
+}
+
+WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
+  WorkLayout w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  const bool topk = m.desc.topk_k > 0;
+  w.err = take(sizeof(int32_t));
+  w.U = take(sizeof(float) * (size_t)Q * m.nus * m.d);
+  w.urow = take(sizeof(int32_t) * (size_t)Q * (m.desc.n_user > 0 ? m.desc.n_user : 1));
+  w.X = take((size_t)m.es * R * m.D_in);
+  w.actA = take((size_t)m.es * R * m.max_hidden);
+  w.actB = take((size_t)m.es * R * m.max_hidden);
+  w.sbuf = take(topk ? sizeof(float) * (size_t)R * m.M : 0);
+  w.partial = take(topk ? sizeof(float) * (size_t)Q * kMaskParts * m.M : 0);
+  w.mask = take(topk ? (size_t)Q * m.M : 0);
+  w.total = off;
+  return w;
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *cold_status_string(int status) {
+  switch (status) {
+    case COLD_OK: return "ok";
+    case COLD_ERR_INVALID_ARG: return "invalid argument";
+    case COLD_ERR_SHAPE: return "shape mismatch";
+    case COLD_ERR_DTYPE: return "unsupported dtype or dimension";
+    case COLD_ERR_NOT_LOADED: return "weights not loaded";
+    case COLD_ERR_WORKSPACE: return "workspace or arena too small";
+    case COLD_ERR_HIP: return "HIP runtime error";
+    case COLD_ERR_ID_RANGE: return "id or offset out of range";
+    default: return "unknown status";
+  }
+}
+
+const char *cold_last_error(const cold_model *m) {
+  if (!m) return "null model";
+  std::lock_guard<std::mutex> lk(m->mu);
+  return m->last_error.c_str();
+}
+
+int cold_create_model(const cold_model_desc *desc, cold_model **out) {
+  if (!desc || !out) return COLD_ERR_INVALID_ARG;
+  *out = nullptr;
+  const cold_model_desc &D = *desc;
+  if (D.n_user < 0 || D.n_seq < 0 || D.n_ad < 0 || D.n_cross < 0 || D.emb_dim <= 0 ||
+      D.se_reduction < 1 || D.n_layers < 1 || !D.widths || !D.table_rows || D.topk_k < 0 ||
+      (D.linear_log != 0 && D.linear_log != 1))
+    return COLD_ERR_INVALID_ARG;
+  if (D.dtype != COLD_F32 && D.dtype != COLD_BF16 && D.dtype != COLD_F16) return COLD_ERR_DTYPE;
+  if (D.id_kind != COLD_IDS_DIRECT_I32 && D.id_kind != COLD_IDS_HASHED_U64) return COLD_ERR_DTYPE;
+  const int M = D.n_user + D.n_seq + D.n_ad + D.n_cross;
+  if (M <= 0 || M > 1024) return COLD_ERR_SHAPE;
+  const int es = D.dtype == COLD_F32 ? 4 : 2;
+  const int epc = 16 / es;
+  if ((D.emb_dim * es) % 16 != 0 || !is_pow2(D.emb_dim / epc) || D.emb_dim / epc > 64)
+    return COLD_ERR_DTYPE;
+  const int cpr = M * (D.emb_dim / epc);
+  if (cpr > kGatherThreads * kGatherChunksPerThread) return COLD_ERR_SHAPE;
+  if (D.widths[0] != M * D.emb_dim) return COLD_ERR_SHAPE;
+  const int n_out = D.widths[D.n_layers];
+  if (n_out != 1 && n_out != 2) return COLD_ERR_SHAPE;
+  int max_hidden = 0;
+  for (int l = 1; l < D.n_layers; ++l) {
+    if (D.widths[l] <= 0) return COLD_ERR_SHAPE;
+    if (D.dtype != COLD_F32 && D.widths[l] % 8 != 0) return COLD_ERR_DTYPE;
+    max_hidden = D.widths[l] > max_hidden ? D.widths[l] : max_hidden;
+  }
+  const int last_in = D.widths[D.n_layers - 1];
+  if ((size_t)n_out * last_in * sizeof(float) > 64 * 1024) return COLD_ERR_SHAPE;
+  for (int g = 0; g < M; ++g)
+    if (D.table_rows[g] < 1 || D.table_rows[g] > 0x7FFFFFFF) return COLD_ERR_SHAPE;
+
+  cold_model *m = new (std::nothrow) cold_model();
+  if (!m) return COLD_ERR_INVALID_ARG;
+  m->desc = D;
+  m->widths.assign(D.widths, D.widths + D.n_layers + 1);
+  m->table_rows.assign(D.table_rows, D.table_rows + M);
+  m->desc.widths = m->widths.data();
+  m->desc.table_rows = m->table_rows.data();
+  m->M = M;
+  m->d = D.emb_dim;
+  m->D_in = M * D.emb_dim;
+  m->H = M / D.se_reduction > 0 ? M / D.se_reduction : 1;
+  m->dtype = D.dtype;
+  m->es = es;
+  m->nus = D.n_user + D.n_seq;
+  m->hashed = D.id_kind == COLD_IDS_HASHED_U64;
+  m->max_hidden = max_hidden;
+  m->arena = arena_layout(*m);
+  m->host_tables.assign(M, 0);
+  m->host_magic.resize(M);
+  for (int g = 0; g < M; ++g) m->host_magic[g] = ~0ull / (uint64_t)m->table_rows[g];
+  *out = m;
+  return COLD_OK;
+}
+
+void cold_destroy_model(cold_model *m) { delete m; }
+
+size_t cold_weight_arena_bytes(const cold_model *m) { return m ? m->arena.total : 0; }
+
+size_t cold_workspace_bytes(const cold_model *m, int64_t max_rows, int64_t max_requests) {
+  if (!m || max_rows < 0 || max_requests < 0) return 0;
+  return work_layout(*m, max_rows, max_requests).total;
+}
+
+int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t arena_bytes,
+                      void *stream) {
+  if (!m) return COLD_ERR_INVALID_ARG;
+  if (!w || !arena || !w->tables || !w->se_w1 || !w->se_b1 || !w->se_w2 || !w->se_b2 || !w->mlp_w ||
+      !w->mlp_b)
+    return fail(m, COLD_ERR_INVALID_ARG, "cold_load_weights: null pointer");
+  if (reinterpret_cast<uintptr_t>(arena) % kAlign)
+    return fail(m, COLD_ERR_INVALID_ARG, "arena must be %zu-byte aligned", kAlign);
+  if (arena_bytes < m->arena.total)
+    return fail(m, COLD_ERR_WORKSPACE, "arena has %zu bytes, needs %zu", arena_bytes, m->arena.total);
+  for (int g = 0; g < m->M; ++g) {
+    if (!w->tables[g] || reinterpret_cast<uintptr_t>(w->tables[g]) % 16)
+      return fail(m, COLD_ERR_INVALID_ARG, "table %d is null or not 16-byte aligned", g);
+    m->host_tables[g] = reinterpret_cast<uint64_t>(w->tables[g]);
+  }
+  const int L = m->desc.n_layers;
+  for (int l = 0; l < L; ++l)
+    if (!w->mlp_w[l] || !w->mlp_b[l]) return fail(m, COLD_ERR_INVALID_ARG, "layer %d weights null", l);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char *A = static_cast<unsigned char *>(arena);
+  const ArenaLayout &al = m->arena;
+  struct Copy { size_t off; const void *src; size_t bytes; hipMemcpyKind kind; };
+  std::vector<Copy> copies = {
+      {al.tables, m->host_tables.data(), sizeof(uint64_t) * m->M, hipMemcpyHostToDevice},
+      {al.rows, m->table_rows.data(), sizeof(int64_t) * m->M, hipMemcpyHostToDevice},
+      {al.magic, m->host_magic.data(), sizeof(uint64_t) * m->M, hipMemcpyHostToDevice},
+      {al.w1, w->se_w1, sizeof(float) * m->H * m->M, hipMemcpyDeviceToDevice},
+      {al.b1, w->se_b1, sizeof(float) * m->H, hipMemcpyDeviceToDevice},
+      {al.w2, w->se_w2, sizeof(float) * m->M * m->H, hipMemcpyDeviceToDevice},
+      {al.b2, w->se_b2, sizeof(float) * m->M, hipMemcpyDeviceToDevice}};
+  for (int l = 0; l < L; ++l) {
+    copies.push_back({al.w[l], w->mlp_w[l], (size_t)m->es * m->widths[l] * m->widths[l + 1],
+                      hipMemcpyDeviceToDevice});
+    copies.push_back({al.b[l], w->mlp_b[l], sizeof(float) * m->widths[l + 1], hipMemcpyDeviceToDevice});
+  }
+  for (const Copy &c : copies) {
+    hipError_t e = hipMemcpyAsync(A + c.off, c.src, c.bytes, c.kind, s);
+    if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: copy");
+  }
+  hipError_t e = hipStreamSynchronize(s);  // host staging must outlive the copies
+  if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: synchronize");
+  m->arena_ptr = A;
+  m->loaded = true;
+  return COLD_OK;
+}
+
+int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_bytes, float *scores,
+               float *importance, uint8_t *group_mask, int32_t *rows_out, int32_t flags,
+               void *stream) {
+  if (!m) return COLD_ERR_INVALID_ARG;
+  if (!b) return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null batch");
+  if (flags & ~COLD_SCORE_VALIDATE) return fail(m, COLD_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (!m->loaded) return fail(m, COLD_ERR_NOT_LOADED, "cold_score before cold_load_weights");
+  const int64_t Q = b->n_requests, R = b->n_rows;
+  if (Q < 0 || R < 0 || b->n_seq_ids < 0) return fail(m, COLD_ERR_INVALID_ARG, "negative size");
+  if (Q == 0 && R > 0) return fail(m, COLD_ERR_SHAPE, "rows without requests");
+  if (R > 0x7FFFFFFFll * 16 || Q > 0x7FFFFFFF) return fail(m, COLD_ERR_SHAPE, "batch too large");
+  if (Q == 0 || R == 0) return COLD_OK;
+  const cold_model_desc &D = m->desc;
+  if (!b->req_off || !scores || !workspace ||
+      (D.n_user > 0 && !b->user_ids) || (D.n_ad > 0 && !b->ad_ids) ||
+      (D.n_cross > 0 && !b->cross_ids) || (D.n_seq > 0 && !b->seq_off) ||
+      (D.n_seq > 0 && b->n_seq_ids > 0 && !b->seq_ids))
+    return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null pointer");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(m, COLD_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
+  const WorkLayout wl = work_layout(*m, R, Q);
+  if (ws_bytes < wl.total)
+    return fail(m, COLD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, wl.total);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char *W = static_cast<unsigned char *>(workspace);
+  unsigned char *A = m->arena_ptr;
+  const ArenaLayout &al = m->arena;
+  const bool topk = D.topk_k > 0;
+
+  GatherArgs g{};
+  g.M = m->M; g.n_user = D.n_user; g.n_seq = D.n_seq; g.n_ad = D.n_ad; g.n_cross = D.n_cross;
+  g.d = m->d; g.H = m->H;
+  const int cpr = m->M * (m->d * m->es / 16);
+  g.rows_per_tile = (kGatherThreads * kGatherChunksPerThread) / cpr;
+  g.R = R; g.Q = Q; g.n_seq_ids = b->n_seq_ids;
+  g.req_off = b->req_off; g.user_ids = b->user_ids; g.ad_ids = b->ad_ids; g.cross_ids = b->cross_ids;
+  g.seq_off = b->seq_off; g.seq_ids = b->seq_ids;
+  g.tables = reinterpret_cast<const void *const *>(A + al.tables);
+  g.table_rows = reinterpret_cast<const int64_t *>(A + al.rows);
+  g.table_magic = reinterpret_cast<const uint64_t *>(A + al.magic);
+  g.w1 = reinterpret_cast<const float *>(A + al.w1);
+  g.b1 = reinterpret_cast<const float *>(A + al.b1);
+  g.w2 = reinterpret_cast<const float *>(A + al.w2);
+  g.b2 = reinterpret_cast<const float *>(A + al.b2);
+  g.U = reinterpret_cast<float *>(W + wl.U);
+  g.urow = reinterpret_cast<int32_t *>(W + wl.urow);
+  g.X = W + wl.X;
+  g.rows_out = rows_out;
+  g.err = reinterpret_cast<int32_t *>(W + wl.err);
+
+  hipError_t e;
+  const bool validate = flags & COLD_SCORE_VALIDATE;
+  if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
+  if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
+    return hip_fail(m, e, "user_pool launch");
+  if (!topk) {
+    g.s_buf = importance;
+    if ((e = launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather_se launch");
+  } else {
+    float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
+    uint8_t *mask = W + wl.mask;
+    g.s_buf = sb;
+    if ((e = launch_gather_se(m->dtype, kWeightsOnly, false, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather_se (weights) launch");
+    if ((e = launch_group_mask(sb, b->req_off, Q, R, m->M, D.topk_k,
+                               reinterpret_cast<float *>(W + wl.partial), kMaskParts, mask,
+                               group_mask, s)) != hipSuccess)
+      return hip_fail(m, e, "group_mask launch");
+    g.mask = mask;
+    g.rows_out = nullptr;  // written by the first pass
+    if ((e = launch_gather_se(m->dtype, kApplyWeights, D.linear_log, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather_se (apply) launch");
+  }
+  // network: hidden layers ping-pong between two activation buffers
+  const int L = D.n_layers;
+  const void *in = W + wl.X;
+  unsigned char *bufs[2] = {W + wl.actA, W + wl.actB};
+  for (int l = 0; l + 1 < L; ++l) {
+    void *outp = bufs[l & 1];
+    if ((e = launch_dense_relu(m->dtype, in, A + al.w[l], reinterpret_cast<const float *>(A + al.b[l]),
+                               outp, R, m->widths[l + 1], m->widths[l], s)) != hipSuccess)
+      return hip_fail(m, e, "dense layer launch");
+    in = outp;
+  }
+  if ((e = launch_head(m->dtype, in, A + al.w[L - 1], reinterpret_cast<const float *>(A + al.b[L - 1]),
+                       scores, R, m->widths[L - 1], m->widths[L], s)) != hipSuccess)
+    return hip_fail(m, e, "head launch");
+  if (validate) {
+    int32_t flag = 0;
+    if ((e = hipMemcpyAsync(&flag, g.err, sizeof flag, hipMemcpyDeviceToHost, s)) != hipSuccess)
+      return hip_fail(m, e, "flag readback");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(m, e, "synchronize");
+    if (flag) return fail(m, COLD_ERR_ID_RANGE, "out-of-range %s%s", (flag & 1) ? "ids " : "",
+                          (flag & 2) ? "offsets" : "");
+  }
+  return COLD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,165 @@
+// cold_internal.h -- device helpers and kernel launchers shared by the HIP
+// sources of libcold.so (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cold {
+
+enum Dtype { kF32 = 0, kBF16 = 1, kF16 = 2 };
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+// --------------------------------------------------------------- storage types
+// Element conversions between a 16-byte chunk of storage and fp32 registers.
+template <typename TS> struct Elem;
+
+template <> struct Elem<float> {
+  static constexpr int kPerChunk = 4;
+  __device__ static inline void unpack(const uint4 &u, float *v) {
+    v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y);
+    v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
+  }
+  __device__ static inline uint4 pack(const float *v) {
+    return make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                      __float_as_uint(v[2]), __float_as_uint(v[3]));
+  }
+  __device__ static inline float to_f32(float x) { return x; }
+  __device__ static inline float from_f32(float x) { return x; }
+};
+
+template <> struct Elem<__bf16> {
+  static constexpr int kPerChunk = 8;
+  __device__ static inline void unpack(const uint4 &u, float *v) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static inline uint16_t bits(float x) {
+    __bf16 b = static_cast<__bf16>(x);  // round to nearest even
+    return __builtin_bit_cast(uint16_t, b);
+  }
+  __device__ static inline uint4 pack(const float *v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)bits(v[2 * i]) | ((uint32_t)bits(v[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __device__ static inline float to_f32(__bf16 x) { return static_cast<float>(x); }
+  __device__ static inline __bf16 from_f32(float x) { return static_cast<__bf16>(x); }
+};
+
+template <> struct Elem<_Float16> {
+  static constexpr int kPerChunk = 8;
+  __device__ static inline void unpack(const uint4 &u, float *v) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = static_cast<float>(__builtin_bit_cast(_Float16, (uint16_t)(w[i] & 0xFFFFu)));
+      v[2 * i + 1] = static_cast<float>(__builtin_bit_cast(_Float16, (uint16_t)(w[i] >> 16)));
+    }
+  }
+  __device__ static inline uint16_t bits(float x) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));  // RNE, overflow -> inf
+  }
+  __device__ static inline uint4 pack(const float *v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)bits(v[2 * i]) | ((uint32_t)bits(v[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __device__ static inline float to_f32(_Float16 x) { return static_cast<float>(x); }
+  __device__ static inline _Float16 from_f32(float x) { return static_cast<_Float16>(x); }
+};
+
+// ------------------------------------------------------------ id resolution
+// SplitMix64 output function (Steele, Lea, Flood, OOPSLA 2014).
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// h mod n for n < 2^31 with magic = floor((2^64 - 1) / n): the Barrett
+// estimate q = mulhi(h, magic) is at most two below the true quotient, so at
+// most two corrections give the exact remainder.
+__device__ __forceinline__ uint32_t mod_barrett(uint64_t h, uint64_t n, uint64_t magic) {
+  uint64_t q = __umul64hi(h, magic);
+  uint64_t r = h - q * n;
+  if (r >= n) r -= n;
+  if (r >= n) r -= n;
+  return (uint32_t)r;
+}
+
+// Table row of an id of feature group g, or -1 (and an error bit) for a
+// direct id outside [0, rows).
+template <bool HASHED>
+__device__ __forceinline__ int32_t resolve_row(const void *ids, int64_t i, int g, int64_t rows,
+                                               uint64_t magic, int32_t *err) {
+  if constexpr (HASHED) {
+    const uint64_t raw = static_cast<const uint64_t *>(ids)[i];
+    const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+    return (int32_t)mod_barrett(mix64(raw ^ salt), (uint64_t)rows, magic);
+  } else {
+    const int32_t id = static_cast<const int32_t *>(ids)[i];
+    if (id < 0 || (int64_t)id >= rows) {
+      atomicOr(err, 1);
+      return -1;
+    }
+    return id;
+  }
+}
+
+// ------------------------------------------------------------ kernel params
+struct GatherArgs {
+  int32_t M, n_user, n_seq, n_ad, n_cross, d, H;
+  int32_t rows_per_tile;          // T
+  int64_t R, Q, n_seq_ids;
+  const int32_t *req_off;         // [Q+1]
+  const void *user_ids;           // [n_user][Q]
+  const void *ad_ids;             // [n_ad][R]
+  const void *cross_ids;          // [n_cross][R]
+  const int32_t *seq_off;         // [n_seq*Q+1]
+  const void *seq_ids;            // [n_seq_ids]
+  const void *const *tables;      // device [M]
+  const int64_t *table_rows;      // device [M]
+  const uint64_t *table_magic;    // device [M]
+  const float *w1, *b1, *w2, *b2; // SE parameters
+  float *U;                       // [Q][n_user+n_seq][d] pooled user side
+  int32_t *urow;                  // [Q][max(n_user,1)] resolved user rows
+  void *X;                        // [R][M*d] network input
+  float *s_buf;                   // [R][M] SE weights (written, or read in apply mode)
+  const uint8_t *mask;            // [Q][M] kept groups (apply mode)
+  int32_t *rows_out;              // [M][R] or null
+  int32_t *err;                   // error bits
+};
+
+enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2 };
+
+// launchers (return hipError_t of the launch)
+hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s);
+hipError_t launch_gather_se(int dtype, int mode, bool linear_log, bool hashed,
+                            const GatherArgs &a, hipStream_t s);
+hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t Q, int64_t R,
+                             int32_t M, int32_t k, float *partial, int32_t n_parts,
+                             uint8_t *mask, uint8_t *mask_out, hipStream_t s);
+hipError_t launch_clear_flag(int32_t *err, hipStream_t s);
+
+hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
+                             int64_t R, int32_t N, int32_t K, hipStream_t s);
+hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, float *scores,
+                       int64_t R, int32_t K, int32_t n_out, hipStream_t s);
+
+constexpr int kGatherThreads = 256;
+constexpr int kGatherChunksPerThread = 8;
+constexpr int kMaskParts = 64;
+
+}  // namespace cold

@@ -167,12 +167,27 @@ def _zipf_cdf(n: int, s: float) -> np.ndarray:
     return _CDF_CACHE[key]
 
 
-def zipf_ranks(rng: np.random.Generator, n: int, s: float, size: int) -> np.ndarray:
+_TORCH_CDF: dict = {}
+
+
+def zipf_ranks(rng: np.random.Generator, n: int, s: float, size: int,
+               device=None) -> np.ndarray:
     """0-based ranks k with P(k) proportional to (k+1)^(-s), k < n.  Bounded,
-    so any s > 0 (including s <= 1) is valid."""
+    so any s > 0 (including s <= 1) is valid.  With ``device`` the inverse-CDF
+    search runs in torch there; the comparisons are exact fp64 either way, so
+    the ranks are identical."""
     cdf = _zipf_cdf(n, s)
     u = rng.random(size)
-    k = np.searchsorted(cdf, u, side="right")
+    if device is None or size < (1 << 20):
+        k = np.searchsorted(cdf, u, side="right")
+    else:
+        import torch
+        key = (n, s, str(device))
+        if key not in _TORCH_CDF:
+            _TORCH_CDF.clear()
+            _TORCH_CDF[key] = torch.from_numpy(cdf).to(device)
+        k = torch.searchsorted(_TORCH_CDF[key], torch.from_numpy(u).to(device),
+                               right=True).cpu().numpy()
     return np.minimum(k, n - 1).astype(np.int64)
 
 
@@ -183,11 +198,11 @@ def _coprime_multiplier(rng: np.random.Generator, n: int) -> int:
             return a
 
 
-def _ids_for_field(rng, cfg: ColdConfig, size: int) -> np.ndarray:
+def _ids_for_field(rng, cfg: ColdConfig, size: int, device=None) -> np.ndarray:
     """Ids of one field: Zipf ranks mapped to ids by a per-field bijection so
     the hot ids are scattered over the table (direct ids, int32) or over the
     64-bit raw id space (hashed ids, uint64)."""
-    ranks = zipf_ranks(rng, cfg.vocab, cfg.zipf_s, size)
+    ranks = zipf_ranks(rng, cfg.vocab, cfg.zipf_s, size, device)
     if not cfg.hashed:
         a = _coprime_multiplier(rng, cfg.vocab)
         b = int(rng.integers(0, cfg.vocab))
@@ -200,7 +215,7 @@ def _ids_for_field(rng, cfg: ColdConfig, size: int) -> np.ndarray:
 
 
 def make_batch(cfg: ColdConfig, seed: Optional[int] = None,
-               cand_per_request=None) -> dict:
+               cand_per_request=None, device=None) -> dict:
     """One request batch in the column (field-major) layout.
 
     Returns numpy arrays::
@@ -213,7 +228,8 @@ def make_batch(cfg: ColdConfig, seed: Optional[int] = None,
         seq_ids   [total]
 
     ``cand_per_request`` may be a list of per-request candidate counts
-    (ragged batches, empty requests allowed).
+    (ragged batches, empty requests allowed).  ``device`` (e.g. "cuda")
+    only speeds up the Zipf inverse-CDF search; the result is the same.
     """
     seed = cfg.seed if seed is None else seed
     ss = np.random.SeedSequence([seed, 0xB47C])
@@ -244,11 +260,11 @@ def make_batch(cfg: ColdConfig, seed: Optional[int] = None,
         g += 1
     ad_ids = np.zeros((cfg.n_ad, n_rows), dtype=id_dtype)
     for f in range(cfg.n_ad):
-        ad_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows)
+        ad_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows, device)
         g += 1
     cross_ids = np.zeros((cfg.n_cross, n_rows), dtype=id_dtype)
     for f in range(cfg.n_cross):
-        cross_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows)
+        cross_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows, device)
         g += 1
     return dict(req_off=req_off, user_ids=user_ids, ad_ids=ad_ids,
                 cross_ids=cross_ids, seq_off=seq_off, seq_ids=seq_ids,

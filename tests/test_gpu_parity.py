@@ -1,0 +1,269 @@
+"""GPU parity of the HIP scoring path (through the C ABI) against the CPU
+checker on the same seeded inputs.
+
+Tolerances: |dCTR| <= 1e-5 for the fp32 model, <= 2e-3 for bf16/fp16 models;
+gather indices and top-k group masks bit-exact.
+"""
+import numpy as np
+import pytest
+
+from paper_2007_16122_amd import binding, synth
+from tests.common import problem
+from tests.gpu_common import (GpuRun, compare_scores, device_table_from_numpy, log,
+                              run_oracle, sparse_host_tables)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+CONFIG_NAMES = list(synth.CONFIGS)
+DEV = "cuda"
+
+
+def mid(name, **kw):
+    """Full model shape (groups, dim, widths, dtype) at a size the checker
+    scores in seconds: ragged requests spanning several tiles, one empty."""
+    base = synth.CONFIGS[name]
+    over = dict(vocab=20_000, seq_len_max=base.seq_len_max)
+    over.update(kw)
+    return synth.config(name, **over)
+
+
+MID_CANDS = {"tiny_fp32": [300, 0, 1, 211], "serving_bf16": [257, 0, 1, 700],
+             "multivalued_fp16_ll": [257, 0, 1, 500], "large_fp16_ll": [129, 0, 1, 400],
+             "wide_prune_bf16": [333, 0, 150]}
+
+
+def load(cfg, tables, params):
+    return GpuRun(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
+
+
+def mask_gap(importance, k, nonempty):
+    """Smallest gap, over non-empty requests, between the k-th and (k+1)-th
+    largest importance."""
+    gaps = []
+    for q in nonempty:
+        s = np.sort(importance[q])[::-1]
+        if k < len(s):
+            gaps.append(s[k - 1] - s[k])
+    return min(gaps) if gaps else np.inf
+
+
+def check_mask(cfg, o, g, batch):
+    """Masks are unique only away from ties: require a clear gap at the k-th
+    group in the checker's fp64 importance, then compare bit for bit (an
+    empty request keeps the first k groups on both sides)."""
+    off = batch["req_off"]
+    nonempty = [q for q in range(len(off) - 1) if off[q + 1] > off[q]]
+    gap = mask_gap(o["importance"], cfg.topk_k, nonempty)
+    log(f"top-k boundary gap {gap:.3e}")
+    assert gap > 1e-4, "inputs put two groups within 1e-4 at the top-k boundary"
+    assert np.array_equal(g["mask"], o["mask"])
+
+
+@pytest.mark.parametrize("name", CONFIG_NAMES)
+def test_parity_mid(name):
+    cfg = mid(name)
+    log(f"test_parity_mid {name}: {MID_CANDS[name]}")
+    tables, params, batch = problem(cfg, seed=21, cand=MID_CANDS[name])
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True, want_s=True, want_mask=cfg.topk_k > 0)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_s=True)
+    req_of_row = np.searchsorted(batch["req_off"], np.arange(batch["n_rows"]), side="right") - 1
+    want_rows = o["rows"].T.astype(np.int32)   # [M][R]
+    assert np.array_equal(g["rows"], want_rows), "gather indices differ"
+    np.testing.assert_allclose(g["s"], o["s"], atol=2e-6, rtol=0)
+    if cfg.topk_k:
+        check_mask(cfg, o, g, batch)
+    compare_scores(cfg, g["scores"], o["scores"], f"mid {name}")
+    assert len(req_of_row) == batch["n_rows"]
+
+
+@pytest.mark.parametrize("name", CONFIG_NAMES)
+def test_parity_full_size_sampled(name):
+    """The full workload in the launch configuration the bench times; the
+    checker scores a seeded sample of rows (first and last row of every
+    request included)."""
+    cfg = synth.CONFIGS[name]
+    log(f"test_parity_full_size_sampled {name}: R={cfg.n_rows} vocab={cfg.vocab}")
+    batch = synth.make_batch(cfg, device=DEV)
+    params = synth.make_params(cfg)
+    tables_dev = [synth.table_torch(cfg, g, device=DEV) for g in range(cfg.n_groups)]
+    run = GpuRun(cfg, tables_dev, params, DEV)
+    try:
+        g = run.score(batch, want_rows=True, want_s=cfg.emit_importance, want_mask=cfg.topk_k > 0)
+    finally:
+        run.close()
+        del tables_dev
+        torch.cuda.empty_cache()
+    rng = np.random.default_rng(99)
+    off = batch["req_off"]
+    ends = np.concatenate([off[:-1], off[1:] - 1])
+    sample = np.unique(np.concatenate([rng.choice(batch["n_rows"], min(1024, batch["n_rows"]),
+                                                  replace=False), ends]))
+    sample = sample[(sample >= 0) & (sample < batch["n_rows"])]
+    tables = sparse_host_tables(cfg, batch, sample, whole_requests=cfg.topk_k > 0)
+    o = run_oracle(cfg, tables, params, batch, sample=sample, want_rows=True, want_s=True)
+    log(f"checker: {len(sample)} rows in {o['seconds']:.1f}s on {o['n_threads']} threads")
+    assert np.array_equal(g["rows"][:, sample], o["rows"].T.astype(np.int32))
+    if cfg.emit_importance:
+        np.testing.assert_allclose(g["s"][sample], o["s"], atol=2e-6, rtol=0)
+    if cfg.topk_k:
+        check_mask(cfg, o, g, batch)
+    compare_scores(cfg, g["scores"][sample], o["scores"], f"full {name}")
+    assert np.all(np.isfinite(g["scores"]))
+
+
+def test_table_generator_device_matches_numpy():
+    cfg = synth.CONFIGS["large_fp16_ll"]
+    rows = np.array([0, 1, 12345, cfg.vocab - 1, 7_777_777])
+    for g in (0, 40, cfg.n_groups - 1):
+        t = synth.table_torch(cfg, g, device=DEV)
+        got = t[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+        assert np.array_equal(got.view(np.uint16),
+                              synth.table_rows_numpy(cfg, g, rows).view(np.uint16))
+        del t
+
+
+def test_permutation_is_bitwise():
+    cfg = mid("serving_bf16")
+    tables, params, batch = problem(cfg, seed=31, cand=[300, 211, 97])
+    run = load(cfg, tables, params)
+    try:
+        base = run.score(batch)["scores"]
+        rng = np.random.default_rng(1)
+        off = batch["req_off"]
+        order_q = rng.permutation(3)
+        perm, new_off = [], [0]
+        for q in order_q:
+            rows = np.arange(off[q], off[q + 1])
+            perm.append(rng.permutation(rows))
+            new_off.append(new_off[-1] + len(rows))
+        perm = np.concatenate(perm)
+        nb = dict(batch)
+        nb["req_off"] = np.asarray(new_off, np.int32)
+        nb["user_ids"] = batch["user_ids"][:, order_q]
+        nb["ad_ids"] = batch["ad_ids"][:, perm]
+        nb["cross_ids"] = batch["cross_ids"][:, perm]
+        got = run.score(nb)["scores"]
+    finally:
+        run.close()
+    assert np.array_equal(got, base[perm])
+
+
+def test_user_broadcast_equals_per_row_bitwise():
+    """One request of C rows vs C one-row requests with copied user ids and
+    behaviour sequences: bitwise equal scores."""
+    from tests.test_oracle_pins import split_into_single_row_requests
+    cfg = mid("multivalued_fp16_ll")
+    tables, params, batch = problem(cfg, seed=32, cand=[150, 90])
+    run = load(cfg, tables, params)
+    try:
+        base = run.score(batch)["scores"]
+        got = run.score(split_into_single_row_requests(cfg, batch))["scores"]
+    finally:
+        run.close()
+    assert np.array_equal(got, base)
+
+
+def test_zero_se_gives_exact_half():
+    cfg = mid("serving_bf16")
+    tables, params, batch = problem(cfg, seed=33, cand=[100, 29])
+    for k in ("se_w1", "se_b1", "se_w2", "se_b2"):
+        params[k] = np.zeros_like(params[k])
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_s=True)
+    finally:
+        run.close()
+    assert np.all(g["s"] == 0.5)
+    o = run_oracle(cfg, tables, params, batch)
+    compare_scores(cfg, g["scores"], o["scores"], "zero SE")
+
+
+def test_fp16_without_linear_log_overflows():
+    """Section 3.3: sum-pooled inputs exceed the fp16 range; without
+    linear_log the half-precision network input overflows, with it the scores
+    stay finite and match the checker."""
+    cfg_ll = mid("multivalued_fp16_ll")
+    cfg_raw = mid("multivalued_fp16_ll", linear_log=False)
+    tables, params, batch = problem(cfg_ll, seed=34, cand=[200, 150])
+    run = load(cfg_raw, tables, params)
+    try:
+        raw = run.score(batch)["scores"]
+    finally:
+        run.close()
+    o_raw = run_oracle(cfg_raw, tables, params, batch)
+    bad = ~np.isfinite(raw) | (np.abs(raw - o_raw["scores"]) > 2e-3)
+    log(f"without linear_log: {bad.sum()} of {bad.size} rows non-finite or off")
+    assert bad.any()
+    run = load(cfg_ll, tables, params)
+    try:
+        ll = run.score(batch)["scores"]
+    finally:
+        run.close()
+    compare_scores(cfg_ll, ll, run_oracle(cfg_ll, tables, params, batch)["scores"], "with LL")
+
+
+def test_validate_reports_out_of_range_ids():
+    cfg = mid("serving_bf16")
+    tables, params, batch = problem(cfg, seed=35, cand=[40, 20])
+    run = load(cfg, tables, params)
+    try:
+        bad = dict(batch)
+        bad["ad_ids"] = batch["ad_ids"].copy()
+        bad["ad_ids"][3, 7] = cfg.vocab + 5
+        with pytest.raises(binding.ColdError) as ei:
+            run.score(bad, validate=True)
+        assert ei.value.status == binding.COLD_ERR_ID_RANGE
+        bad["ad_ids"][3, 7] = -1
+        with pytest.raises(binding.ColdError):
+            run.score(bad, validate=True)
+        # the clean batch still validates after the failure
+        g = run.score(batch, validate=True)
+    finally:
+        run.close()
+    compare_scores(cfg, g["scores"], run_oracle(cfg, tables, params, batch)["scores"], "after bad")
+
+
+def test_empty_batches_are_noops():
+    cfg = mid("serving_bf16")
+    tables, params, batch = problem(cfg, seed=36, cand=[0, 0])
+    run = load(cfg, tables, params)
+    try:
+        out = run.score(batch)
+        assert out["scores"].size == 0
+        tables2, params2, batch2 = problem(cfg, seed=36, cand=[0, 5, 0])
+        g = run.score(batch2)
+    finally:
+        run.close()
+    compare_scores(cfg, g["scores"], run_oracle(cfg, tables, params, batch2)["scores"], "empties")
+
+
+def test_deterministic():
+    cfg = mid("wide_prune_bf16")
+    tables, params, batch = problem(cfg, seed=37, cand=[400])
+    run = load(cfg, tables, params)
+    try:
+        a = run.score(batch, want_mask=True)
+        b = run.score(batch, want_mask=True)
+    finally:
+        run.close()
+    assert np.array_equal(a["scores"], b["scores"]) and np.array_equal(a["mask"], b["mask"])
+
+
+def test_weights_hot_swap():
+    cfg = mid("serving_bf16")
+    tables, params_a, batch = problem(cfg, seed=38, cand=[120, 80])
+    params_b = synth.make_params(cfg, seed=12345)
+    run = load(cfg, tables, params_a)
+    try:
+        ga = run.score(batch)["scores"]
+        run.model.load(run.tables_dev, binding.params_to_device(params_b, cfg.dtype, run.device))
+        gb = run.score(batch)["scores"]
+    finally:
+        run.close()
+    compare_scores(cfg, ga, run_oracle(cfg, tables, params_a, batch)["scores"], "params A")
+    compare_scores(cfg, gb, run_oracle(cfg, tables, params_b, batch)["scores"], "params B")
