@@ -1,0 +1,301 @@
+#!/usr/bin/env python3
+"""Throughput and latency of the COLD scoring path on one MI355X.
+
+One step = one cold_score call over the whole batch of the serving-shaped
+workload (32 requests x 2,000 candidate ads = 64,000 rows, 48 fields of dim
+16 over 1M-row bf16 tables, SE block, 768x1024x512x256x128x64x2 network),
+inputs resident in HBM before timing starts.  Prints one JSON line.
+
+Also measured: the p50/p99 host-side latency of scoring one 2,000-ad request
+(eager launches and HIP-graph replay), per-stage kernel times with HIP events
+on the scoring stream, the roofline fraction of the dominant kernel, and the
+CPU checker's throughput on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def stage_work(cfg, batch, stage):
+    """Algorithmic work of one launch of a stage: ('hbm', bytes) or
+    ('mfma', flops)."""
+    es = {"f32": 4, "bf16": 2, "f16": 2}[cfg.dtype]
+    idb = 8 if cfg.hashed else 4
+    R, Q = batch["n_rows"], len(batch["req_off"]) - 1
+    d, m = cfg.emb_dim, cfg.n_groups
+    nus = cfg.n_user + cfg.n_seq
+    nax = cfg.n_ad + cfg.n_cross
+    if stage == "user_pool":
+        seq = int(batch["seq_off"][-1]) if cfg.n_seq else 0
+        return "hbm", Q * cfg.n_user * (idb + d * es) + seq * (idb + d * es) + Q * nus * d * 4
+    if stage in ("gather_se", "gather_apply", "se_weights"):
+        # ids + gathered ad/cross rows + network input written + pooled user rows
+        out = R * cfg.d_in * es if stage != "se_weights" else R * m * 4
+        return "hbm", R * nax * (idb + d * es) + out + Q * nus * d * 4
+    if stage.startswith("dense"):
+        li = int(stage[5:])
+        return "mfma", 2.0 * R * cfg.widths[li] * cfg.widths[li + 1]
+    if stage == "head":
+        k = cfg.widths[-2]
+        return "hbm", R * k * es + R * 4
+    if stage == "group_mask":
+        return "hbm", R * m * 4
+    return "hbm", 0
+
+
+def roofline_entry(cfg, batch, stage, ms):
+    kind, work = stage_work(cfg, batch, stage)
+    if kind == "mfma":
+        ach = work / (ms * 1e-3) / 1e12
+        peak = PEAK_MFMA_TFLOPS[cfg.dtype]
+        return {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "work_per_launch": work}
+    ach = work / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4), "work_per_launch": work}
+
+
+def request_slice(batch, q, cfg):
+    """Request q of a batch as a one-request batch (numpy)."""
+    off = batch["req_off"]
+    lo, hi = int(off[q]), int(off[q + 1])
+    Q = len(off) - 1
+    out = dict(req_off=np.array([0, hi - lo], np.int32),
+               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q + 1]),
+               ad_ids=np.ascontiguousarray(batch["ad_ids"][:, lo:hi]),
+               cross_ids=np.ascontiguousarray(batch["cross_ids"][:, lo:hi]),
+               n_rows=hi - lo, n_requests=1)
+    if cfg.n_seq:
+        so = batch["seq_off"]
+        segs = [batch["seq_ids"][so[f * Q + q]:so[f * Q + q + 1]] for f in range(cfg.n_seq)]
+        out["seq_off"] = np.concatenate([[0], np.cumsum([len(s) for s in segs])]).astype(np.int32)
+        out["seq_ids"] = np.concatenate(segs)
+    else:
+        out["seq_off"] = np.zeros(1, np.int32)
+        out["seq_ids"] = np.zeros(0, batch["ad_ids"].dtype)
+    return out
+
+
+def latency(model, dev_batch, scores, iters, torch, graph):
+    stream = torch.cuda.current_stream()
+    times = []
+    if graph:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            model.score(dev_batch, scores=scores)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            model.score(dev_batch, scores=scores)
+        g.replay()
+        torch.cuda.synchronize()
+        for _ in range(iters):
+            t0 = time.perf_counter()
+            g.replay()
+            stream.synchronize()
+            times.append(time.perf_counter() - t0)
+    else:
+        for _ in range(iters):
+            t0 = time.perf_counter()
+            model.score(dev_batch, scores=scores)
+            stream.synchronize()
+            times.append(time.perf_counter() - t0)
+    t = np.array(times) * 1e3
+    return float(np.median(t)), float(np.quantile(t, 0.99))
+
+
+def cpu_baseline(cfg, batch, params, target_s):
+    """The CPU checker, as it stands, on a bounded sample of the workload."""
+    import oracle
+    from paper_2007_16122_amd import synth
+    dims = dict(n_user=cfg.n_user, n_seq=cfg.n_seq, n_ad=cfg.n_ad, n_cross=cfg.n_cross,
+                emb_dim=cfg.emb_dim, se_hidden=cfg.se_hidden, dtype=cfg.dtype,
+                hashed=cfg.hashed, linear_log=cfg.linear_log, topk_k=cfg.topk_k,
+                widths=list(cfg.widths))
+    stored = dict(params)
+    stored["mlp_w"] = [synth.mlp_weight_stored(w, cfg.dtype) for w in params["mlp_w"]]
+    np_dt = {"f32": np.float32, "f16": np.float16, "bf16": np.uint16}[cfg.dtype]
+
+    def tables_for(sample):
+        q_n = len(batch["req_off"]) - 1
+        reqs = np.unique(np.searchsorted(batch["req_off"], sample, side="right") - 1)
+        tabs = []
+        for g in range(cfg.n_groups):
+            kind = cfg.group_kind(g)
+            if kind == "user":
+                ids = batch["user_ids"][g][reqs]
+            elif kind == "seq":
+                f = g - cfg.n_user
+                so = batch["seq_off"]
+                ids = np.concatenate([batch["seq_ids"][so[f * q_n + q]:so[f * q_n + q + 1]]
+                                      for q in reqs])
+            elif kind == "ad":
+                ids = batch["ad_ids"][g - cfg.n_user - cfg.n_seq][sample]
+            else:
+                ids = batch["cross_ids"][g - cfg.n_user - cfg.n_seq - cfg.n_ad][sample]
+            rows = (np.array([oracle.hash_row(int(v), g, cfg.vocab) for v in np.unique(ids)])
+                    if cfg.hashed else np.unique(ids)).astype(np.int64)
+            t = np.zeros((cfg.vocab, cfg.emb_dim), np_dt)
+            t[rows] = synth.table_rows_numpy(cfg, g, rows)
+            tabs.append(t)
+        return tabs
+
+    threads = len(os.sched_getaffinity(0))
+    probe = np.arange(min(128, batch["n_rows"]))
+    tabs = tables_for(probe)
+    t0 = time.perf_counter()
+    oracle.score(dims, tabs, stored, batch, sample=probe, n_threads=threads)
+    per_row = (time.perf_counter() - t0) / len(probe)
+    n = int(min(batch["n_rows"], max(len(probe), target_s / max(per_row, 1e-9))))
+    sample = np.arange(n)
+    tabs = tables_for(sample)
+    t0 = time.perf_counter()
+    o = oracle.score(dims, tabs, stored, batch, sample=sample, n_threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 1), "unit": "ads/s", "cores": int(o["n_threads"]),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"first {n} rows (requests 0..{int(np.searchsorted(batch['req_off'], n - 1, side='right')) - 1}) "
+                      f"of the {cfg.name} batch, fp64 checker, {o['n_threads']} threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="serving_bf16")
+    ap.add_argument("--latency-iters", type=int, default=300)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the scoring path runs on a single MI355X "
+              f"(rows are independent; see DESIGN.md for how it would shard). Got --gpus {args.gpus}.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2007_16122_amd import binding, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.workload]
+    log(f"workload {cfg.name}: {cfg.n_requests} x {cfg.cand_per_request} rows, "
+        f"{cfg.n_groups} groups, vocab {cfg.vocab}, {cfg.dtype}")
+    t0 = time.perf_counter()
+    batch = synth.make_batch(cfg, device=dev)
+    params = synth.make_params(cfg)
+    tables = [synth.table_torch(cfg, g, device=dev) for g in range(cfg.n_groups)]
+    model = binding.ColdModel(cfg, device=dev)
+    model.load(tables, binding.params_to_device(params, cfg.dtype, dev))
+    dev_batch = binding.batch_to_device(batch, dev)
+    R = batch["n_rows"]
+    scores = torch.empty(R, dtype=torch.float32, device=dev)
+    model.ensure_workspace(R, len(batch["req_off"]) - 1)
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
+
+    for _ in range(args.warmup):
+        model.score(dev_batch, scores=scores)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(scores).all()), "non-finite scores"
+
+    binding.cold_profile_enable(model.h, True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        model.score(dev_batch, scores=scores)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    stages, n_calls = binding.cold_profile_read(model.h)
+    binding.cold_profile_enable(model.h, False)
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    value = R / (ms_per_step * 1e-3)
+    log(f"{args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f}), "
+        f"{value:.4g} ads/s")
+
+    stage_rows = []
+    for name, tot in stages:
+        ms = tot / max(n_calls, 1)
+        e = roofline_entry(cfg, batch, name, ms)
+        e.update(name=name, ms=round(ms, 5))
+        stage_rows.append(e)
+        log(f"  {name:12s} {ms * 1e3:9.2f} us  {e['achieved']:>9} {e['unit']}  ({100 * e['frac']:.1f}%)")
+    dom = max(stage_rows, key=lambda e: e["ms"])
+    roofline = {"bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
+                "unit": dom["unit"], "frac": dom["frac"], "traffic": None, "kernel": dom["name"],
+                "ms_per_launch": dom["ms"], "work_per_launch": dom["work_per_launch"]}
+    g_ms = sum(e["ms"] for e in stage_rows if e["bound"] == "hbm" and e["name"] != "head")
+    g_bytes = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "hbm" and e["name"] != "head")
+    m_ms = sum(e["ms"] for e in stage_rows if e["bound"] == "mfma")
+    m_flops = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "mfma")
+
+    lat_np = request_slice(batch, 0, cfg)
+    lat_dev = binding.batch_to_device(lat_np, dev)
+    lat_scores = torch.empty(lat_np["n_rows"], dtype=torch.float32, device=dev)
+    p50, p99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=False)
+    try:
+        g50, g99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=True)
+    except Exception as exc:  # graph capture is an optional measurement
+        log(f"graph replay unavailable: {exc}")
+        g50 = g99 = None
+    log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, batch, params, args.cpu_seconds)
+        log(f"cpu baseline {cpu}")
+
+    out = {
+        "metric": "candidate ads scored/sec on 1 GPU; p50 latency of a 2,000-ad request",
+        "value": round(value, 1), "unit": "ads/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "requests": cfg.n_requests,
+                   "candidates_per_request": cfg.cand_per_request, "rows": R,
+                   "groups": cfg.n_groups, "emb_dim": cfg.emb_dim, "vocab": cfg.vocab,
+                   "widths": list(cfg.widths), "parallelism": "none (1 GPU)"},
+        "p50_latency_ms": round(p50, 4), "p99_latency_ms": round(p99, 4),
+        "p50_latency_graph_ms": None if g50 is None else round(g50, 4),
+        "p99_latency_graph_ms": None if g99 is None else round(g99, 4),
+        "roofline": roofline,
+        "roofline_gather_se": {"bound": "hbm", "achieved": round(g_bytes / (g_ms * 1e-3) / 1e9, 1),
+                               "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                               "frac": round(g_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "roofline_mlp": {"bound": "mfma", "achieved": round(m_flops / (m_ms * 1e-3) / 1e12, 2),
+                         "peak": PEAK_MFMA_TFLOPS[cfg.dtype], "unit": "TFLOP/s",
+                         "frac": round(m_flops / (m_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[cfg.dtype], 4)},
+        "stages": [{k: e[k] for k in ("name", "ms", "bound", "achieved", "unit", "frac")}
+                   for e in stage_rows],
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -160,6 +160,22 @@ int cold_score(cold_model *model, const cold_batch *b, void *workspace, size_t w
                float *scores, float *importance, uint8_t *group_mask, int32_t *rows_out,
                int32_t flags, void *stream);
 
+/* Stage timing, for measurement tools.  While enabled, every cold_score
+ * call on this model records a HIP event on its stream before each kernel
+ * stage and one after the last; cold_profile_read synchronises those events
+ * and returns, per stage, its name and the summed elapsed milliseconds over
+ * all calls since the previous read (stages are matched by position; every
+ * profiled call of one model runs the same stage sequence).  Not for
+ * concurrent cold_score calls on one model.  Enabling creates HIP events;
+ * disabling destroys them.
+ *   names       host char[max_stages][32] or NULL
+ *   total_ms    host float[max_stages]
+ *   n_stages    host: stages of the profiled calls
+ *   n_calls     host: profiled calls since the previous read */
+int cold_profile_enable(cold_model *model, int32_t enable);
+int cold_profile_read(cold_model *model, int32_t max_stages, char (*names)[32], float *total_ms,
+                      int32_t *n_stages, int32_t *n_calls);
+
 /* Static text of a status code. */
 const char *cold_status_string(int status);
 

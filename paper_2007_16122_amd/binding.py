@@ -31,7 +31,8 @@ DTYPES = {"f32": COLD_F32, "bf16": COLD_BF16, "f16": COLD_F16}
 
 EXPORTS = ("cold_create_model", "cold_destroy_model", "cold_weight_arena_bytes",
            "cold_workspace_bytes", "cold_load_weights", "cold_score",
-           "cold_status_string", "cold_last_error")
+           "cold_status_string", "cold_last_error", "cold_profile_enable",
+           "cold_profile_read")
 
 
 class ColdError(RuntimeError):
@@ -95,6 +96,10 @@ def lib():
         L.cold_status_string.restype = ctypes.c_char_p
         L.cold_last_error.argtypes = [vp]
         L.cold_last_error.restype = ctypes.c_char_p
+        L.cold_profile_enable.argtypes = [vp, i32]
+        L.cold_profile_enable.restype = ctypes.c_int
+        L.cold_profile_read.argtypes = [vp, i32, vp, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.cold_profile_read.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -137,6 +142,25 @@ def cold_status_string(st: int) -> str:
 
 def cold_last_error(h) -> str:
     return lib().cold_last_error(h).decode()
+
+
+def cold_profile_enable(h, enable: bool) -> int:
+    return lib().cold_profile_enable(h, int(bool(enable)))
+
+
+def cold_profile_read(h, max_stages: int = 32):
+    """Per-stage summed milliseconds of the profiled calls since the last
+    read: (list of (name, ms), n_calls)."""
+    names = (ctypes.c_char * 32 * max_stages)()
+    total = (ctypes.c_float * max_stages)()
+    ns, nc = ctypes.c_int32(), ctypes.c_int32()
+    st = lib().cold_profile_read(h, max_stages, ctypes.addressof(names), ctypes.addressof(total),
+                                 ctypes.byref(ns), ctypes.byref(nc))
+    if st != COLD_OK:
+        raise ColdError(st, "cold_profile_read: " + cold_last_error(h))
+    out = [(bytes(names[i]).split(b"\0")[0].decode(), float(total[i]))
+           for i in range(min(ns.value, max_stages))]
+    return out, nc.value
 
 
 def make_desc(n_user, n_seq, n_ad, n_cross, emb_dim, dtype, se_reduction,

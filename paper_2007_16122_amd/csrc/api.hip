@@ -30,6 +30,11 @@ struct WorkLayout {
 
 }  // namespace
 
+struct ProfSet {
+  std::vector<hipEvent_t> ev;       // ev[i] precedes stage i; the last ends the call
+  std::vector<const char *> names;
+};
+
 struct cold_model {
   cold_model_desc desc;
   std::vector<int32_t> widths;
@@ -43,6 +48,9 @@ struct cold_model {
   std::vector<uint64_t> host_magic;
   mutable std::mutex mu;
   std::string last_error;
+  bool prof_on = false;
+  std::vector<ProfSet> prof;        // one set of events per profiled call
+  size_t prof_used = 0;
 };
 
 namespace {
@@ -104,6 +112,33 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
 }
 
 bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+constexpr size_t kMaxProfiledCalls = 4096;
+
+// Records the stage boundaries of one cold_score call when profiling is on.
+struct StageMarks {
+  cold_model *m;
+  hipStream_t s;
+  ProfSet *set = nullptr;
+  size_t n = 0;
+  StageMarks(cold_model *m_, hipStream_t s_) : m(m_), s(s_) {
+    if (!m->prof_on || m->prof_used >= kMaxProfiledCalls) return;
+    if (m->prof_used == m->prof.size()) m->prof.emplace_back();
+    set = &m->prof[m->prof_used++];
+    set->names.clear();
+  }
+  hipError_t mark(const char *name) {  // name = NULL ends the call
+    if (!set) return hipSuccess;
+    if (n == set->ev.size()) {
+      hipEvent_t e;
+      hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return err;
+      set->ev.push_back(e);
+    }
+    if (name) set->names.push_back(name);
+    return hipEventRecord(set->ev[n++], s);
+  }
+};
 
 }  // namespace
 
@@ -185,7 +220,55 @@ int cold_create_model(const cold_model_desc *desc, cold_model **out) {
   return COLD_OK;
 }
 
-void cold_destroy_model(cold_model *m) { delete m; }
+static void destroy_events(cold_model *m) {
+  for (ProfSet &p : m->prof)
+    for (hipEvent_t e : p.ev) (void)hipEventDestroy(e);
+  m->prof.clear();
+  m->prof_used = 0;
+}
+
+void cold_destroy_model(cold_model *m) {
+  if (!m) return;
+  destroy_events(m);
+  delete m;
+}
+
+int cold_profile_enable(cold_model *m, int32_t enable) {
+  if (!m) return COLD_ERR_INVALID_ARG;
+  m->prof_on = enable != 0;
+  if (!m->prof_on) destroy_events(m);
+  m->prof_used = 0;
+  return COLD_OK;
+}
+
+int cold_profile_read(cold_model *m, int32_t max_stages, char (*names)[32], float *total_ms,
+                      int32_t *n_stages, int32_t *n_calls) {
+  if (!m || max_stages < 0 || (!total_ms && max_stages > 0) || !n_stages || !n_calls)
+    return COLD_ERR_INVALID_ARG;
+  *n_stages = 0;
+  *n_calls = (int32_t)m->prof_used;
+  for (int i = 0; i < max_stages; ++i) total_ms[i] = 0.0f;
+  for (size_t c = 0; c < m->prof_used; ++c) {
+    ProfSet &p = m->prof[c];
+    const int ns = (int)p.names.size();
+    if (c == 0) *n_stages = ns;
+    else if (ns != *n_stages) return fail(m, COLD_ERR_INVALID_ARG, "profiled calls differ in stages");
+    hipError_t e = hipEventSynchronize(p.ev[ns]);
+    if (e != hipSuccess) return hip_fail(m, e, "cold_profile_read: synchronize");
+    for (int i = 0; i < ns && i < max_stages; ++i) {
+      float ms = 0.0f;
+      if ((e = hipEventElapsedTime(&ms, p.ev[i], p.ev[i + 1])) != hipSuccess)
+        return hip_fail(m, e, "cold_profile_read: elapsed");
+      total_ms[i] += ms;
+      if (names && c == 0) {
+        std::strncpy(names[i], p.names[i], 31);
+        names[i][31] = 0;
+      }
+    }
+  }
+  m->prof_used = 0;
+  return COLD_OK;
+}
 
 size_t cold_weight_arena_bytes(const cold_model *m) { return m ? m->arena.total : 0; }
 
@@ -294,25 +377,33 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
 
   hipError_t e;
   const bool validate = flags & COLD_SCORE_VALIDATE;
+  StageMarks marks(m, s);
+  static const char *kDenseNames[] = {"dense0", "dense1", "dense2", "dense3", "dense4", "dense5",
+                                      "dense6", "dense7", "dense8", "dense9", "dense10", "dense11"};
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
+  if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
   if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
     return hip_fail(m, e, "user_pool launch");
   if (!topk) {
     g.s_buf = importance;
+    if ((e = marks.mark("gather_se")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se launch");
   } else {
     float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
     uint8_t *mask = W + wl.mask;
     g.s_buf = sb;
+    if ((e = marks.mark("se_weights")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_gather_se(m->dtype, kWeightsOnly, false, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se (weights) launch");
+    if ((e = marks.mark("group_mask")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_group_mask(sb, b->req_off, Q, R, m->M, D.topk_k,
                                reinterpret_cast<float *>(W + wl.partial), kMaskParts, mask,
                                group_mask, s)) != hipSuccess)
       return hip_fail(m, e, "group_mask launch");
     g.mask = mask;
     g.rows_out = nullptr;  // written by the first pass
+    if ((e = marks.mark("gather_apply")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_gather_se(m->dtype, kApplyWeights, D.linear_log, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se (apply) launch");
   }
@@ -322,14 +413,18 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   unsigned char *bufs[2] = {W + wl.actA, W + wl.actB};
   for (int l = 0; l + 1 < L; ++l) {
     void *outp = bufs[l & 1];
+    if ((e = marks.mark(l < 12 ? kDenseNames[l] : "dense")) != hipSuccess)
+      return hip_fail(m, e, "profile event");
     if ((e = launch_dense_relu(m->dtype, in, A + al.w[l], reinterpret_cast<const float *>(A + al.b[l]),
                                outp, R, m->widths[l + 1], m->widths[l], s)) != hipSuccess)
       return hip_fail(m, e, "dense layer launch");
     in = outp;
   }
+  if ((e = marks.mark("head")) != hipSuccess) return hip_fail(m, e, "profile event");
   if ((e = launch_head(m->dtype, in, A + al.w[L - 1], reinterpret_cast<const float *>(A + al.b[L - 1]),
                        scores, R, m->widths[L - 1], m->widths[L], s)) != hipSuccess)
     return hip_fail(m, e, "head launch");
+  if ((e = marks.mark(nullptr)) != hipSuccess) return hip_fail(m, e, "profile event");
   if (validate) {
     int32_t flag = 0;
     if ((e = hipMemcpyAsync(&flag, g.err, sizeof flag, hipMemcpyDeviceToHost, s)) != hipSuccess)
