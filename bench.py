@@ -186,6 +186,8 @@ def main():
     ap.add_argument("--latency-iters", type=int, default=300)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-latency", action="store_true",
+                    help="skip the 2,000-ad latency runs (kernel-trace profiles of the step only)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the scoring path runs on a single MI355X "
@@ -254,16 +256,17 @@ def main():
     m_ms = sum(e["ms"] for e in stage_rows if e["bound"] == "mfma")
     m_flops = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "mfma")
 
-    lat_np = request_slice(batch, 0, cfg)
-    lat_dev = binding.batch_to_device(lat_np, dev)
-    lat_scores = torch.empty(lat_np["n_rows"], dtype=torch.float32, device=dev)
-    p50, p99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=False)
-    try:
-        g50, g99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=True)
-    except Exception as exc:  # graph capture is an optional measurement
-        log(f"graph replay unavailable: {exc}")
-        g50 = g99 = None
-    log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
+    p50 = p99 = g50 = g99 = None
+    if not args.no_latency:
+        lat_np = request_slice(batch, 0, cfg)
+        lat_dev = binding.batch_to_device(lat_np, dev)
+        lat_scores = torch.empty(lat_np["n_rows"], dtype=torch.float32, device=dev)
+        p50, p99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=False)
+        try:
+            g50, g99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=True)
+        except Exception as exc:  # graph capture is an optional measurement
+            log(f"graph replay unavailable: {exc}")
+        log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -279,7 +282,8 @@ def main():
                    "candidates_per_request": cfg.cand_per_request, "rows": R,
                    "groups": cfg.n_groups, "emb_dim": cfg.emb_dim, "vocab": cfg.vocab,
                    "widths": list(cfg.widths), "parallelism": "none (1 GPU)"},
-        "p50_latency_ms": round(p50, 4), "p99_latency_ms": round(p99, 4),
+        "p50_latency_ms": None if p50 is None else round(p50, 4),
+        "p99_latency_ms": None if p99 is None else round(p99, 4),
         "p50_latency_graph_ms": None if g50 is None else round(g50, 4),
         "p99_latency_graph_ms": None if g99 is None else round(g99, 4),
         "roofline": roofline,
