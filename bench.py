@@ -186,6 +186,9 @@ def main():
     ap.add_argument("--latency-iters", type=int, default=300)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device once (a plain "
+                         "copy of known size, to calibrate HBM byte counters)")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the 2,000-ad latency runs (kernel-trace profiles of the step only)")
     args = ap.parse_args()
@@ -267,6 +270,16 @@ def main():
         except Exception as exc:  # graph capture is an optional measurement
             log(f"graph replay unavailable: {exc}")
         log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
+
+    if args.copy_probe_mb > 0:
+        n = args.copy_probe_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -22,7 +22,6 @@
 
 namespace cold {
 
-constexpr int kBM = 128;   // rows of X per tile
 constexpr int kBK = 32;    // K per step (one MFMA depth)
 constexpr int kPad = 8;    // elements of row padding in LDS
 constexpr int kLdsRow = kBK + kPad;
@@ -50,26 +49,28 @@ __device__ __forceinline__ int xcd_tile(int b, int total) {
   return start + slot;
 }
 
-template <typename TS, int BN>
-__global__ __launch_bounds__(256) void dense_relu_mfma_kernel(const TS *__restrict__ X,
-                                                              const TS *__restrict__ W,
-                                                              const float *__restrict__ bias,
-                                                              TS *__restrict__ Y, int64_t R, int N,
-                                                              int K, int tiles_n, int tiles_total) {
+// Block tile BR rows x BN output features, 4 waves as 2 x 2, each wave
+// (BR/2) x (BN/2).  Per 32-deep K step a wave reads BR/32 + BN/32 fragments
+// of 16 bytes per lane and issues (BR/32)*(BN/32) MFMAs.
+template <typename TS, int BR, int BN>
+__global__ __launch_bounds__(256, 2) void dense_relu_mfma_kernel(const TS *__restrict__ X,
+                                                                 const TS *__restrict__ W,
+                                                                 const float *__restrict__ bias,
+                                                                 TS *__restrict__ Y, int64_t R, int N,
+                                                                 int K, int tiles_n, int tiles_total) {
   typedef typename Mfma<TS>::frag frag;
-  constexpr int NI = BN / 2 / 16;          // 16-wide output-feature blocks per wave
-  constexpr int RJ = 4;                    // 16-wide row blocks per wave (64 rows)
-  constexpr int A_CHUNKS = BN * kBK / 8;   // 16-byte chunks of the W tile
-  constexpr int B_CHUNKS = kBM * kBK / 8;
-  constexpr int A_PER_T = A_CHUNKS / 256, B_PER_T = B_CHUNKS / 256;
-  static_assert(A_CHUNKS % 256 == 0 && B_CHUNKS % 256 == 0, "tile/thread mismatch");
+  constexpr int NI = BN / 32;              // 16-wide feature blocks per wave
+  constexpr int RJ = BR / 32;              // 16-wide row blocks per wave
+  constexpr int A_PER_T = BN * kBK / 8 / 256;   // 16-byte chunks of the W tile per thread
+  constexpr int B_PER_T = BR * kBK / 8 / 256;
+  static_assert(A_PER_T >= 1 && B_PER_T >= 1, "tile/thread mismatch");
 
   __shared__ __align__(16) TS sA[2][BN * kLdsRow];
-  __shared__ __align__(16) TS sB[2][kBM * kLdsRow];
+  __shared__ __align__(16) TS sB[2][BR * kLdsRow];
 
   const int tile = xcd_tile(blockIdx.x, tiles_total);
   const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
-  const int64_t r0 = (int64_t)tr * kBM;
+  const int64_t r0 = (int64_t)tr * BR;
   const int n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave & 1, wr = wave >> 1;
@@ -119,17 +120,16 @@ __global__ __launch_bounds__(256) void dense_relu_mfma_kernel(const TS *__restri
   for (int ks = 0; ks < ksteps; ++ks) {
     const int buf = ks & 1;
     if (ks + 1 < ksteps) load_global((ks + 1) * kBK);
-    frag fa[NI], fb[RJ];
+    frag fa[NI];
 #pragma unroll
     for (int i = 0; i < NI; ++i)
       fa[i] = *reinterpret_cast<const frag *>(&sA[buf][(wn * (BN / 2) + i * 16 + frow) * kLdsRow + fk]);
 #pragma unroll
-    for (int j = 0; j < RJ; ++j)
-      fb[j] = *reinterpret_cast<const frag *>(&sB[buf][(wr * 64 + j * 16 + frow) * kLdsRow + fk]);
+    for (int j = 0; j < RJ; ++j) {
+      const frag fb = *reinterpret_cast<const frag *>(&sB[buf][(wr * (BR / 2) + j * 16 + frow) * kLdsRow + fk]);
 #pragma unroll
-    for (int i = 0; i < NI; ++i)
-#pragma unroll
-      for (int j = 0; j < RJ; ++j) acc[i][j] = Mfma<TS>::mac(fa[i], fb[j], acc[i][j]);
+      for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+    }
     if (ks + 1 < ksteps) store_lds(buf ^ 1);
     __syncthreads();
   }
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void dense_relu_mfma_kernel(const TS *__restri
     for (int e = 0; e < 4; ++e) bv[e] = (n + e < N) ? bias[n + e] : 0.0f;
 #pragma unroll
     for (int j = 0; j < RJ; ++j) {
-      const int64_t r = r0 + wr * 64 + j * 16 + dr;
+      const int64_t r = r0 + wr * (BR / 2) + j * 16 + dr;
       if (r >= R) continue;
       float o[4];
 #pragma unroll
@@ -162,6 +162,167 @@ __global__ __launch_bounds__(256) void dense_relu_mfma_kernel(const TS *__restri
         for (int e = 0; e < 4 && n + e < N; ++e) Y[r * N + n + e] = Elem<TS>::from_f32(o[e]);
       }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined layer: operand tiles stream global -> LDS with the gfx950 direct
+// loads (global_load_lds_dwordx4: each lane's 16 bytes land at
+// base + 16 * lane, no VGPR staging) into an S-stage ring, issued S-1 K steps
+// ahead; each wave waits only for its own loads of the stage it is about to
+// read (vmcnt), then one barrier per K step.  LDS rows are 64 bytes (32
+// elements); chunk c of row r sits in slot c ^ swz(r), which makes the
+// 16-byte fragment reads conflict-free whether the LDS serves 8 or 16 lanes
+// per cycle.  The output tile is staged in LDS after the K loop so every row
+// segment is written with full 16-byte stores.
+__device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// wait until at most N of this wave's global loads are in flight and all of
+// its LDS reads have returned
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+template <typename TS, int BR, int BN, int S>
+__global__ __launch_bounds__(256, 2) void dense_relu_pipe_kernel(const TS *__restrict__ X,
+                                                                 const TS *__restrict__ W,
+                                                                 const float *__restrict__ bias,
+                                                                 TS *__restrict__ Y, int64_t R, int N,
+                                                                 int K, int tiles_n, int tiles_total) {
+  typedef typename Mfma<TS>::frag frag;
+  typedef __attribute__((address_space(3))) void lds_void;
+  constexpr int NI = BN / 32, RJ = BR / 32;          // 16x16 blocks per wave
+  constexpr int ROWB = kBK * 2;                      // bytes per LDS row (64)
+  constexpr int STAGE = (BN + BR) * ROWB;            // bytes per stage
+  constexpr int LOADS = (BN + BR) / 16 / 4;          // 16-row loads per wave per stage
+  constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
+  constexpr int OUT_BYTES = BR * OUT_STRIDE * 2;
+  constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
+  static_assert((BN + BR) % 64 == 0, "loads must split evenly over 4 waves");
+  static_assert(S >= 2 && S <= 4, "stages");
+  __shared__ __align__(16) unsigned char smem[SMEM];
+
+  const int tile = xcd_tile(blockIdx.x, tiles_total);
+  const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
+  const int64_t r0 = (int64_t)tr * BR;
+  const int n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave & 1, wr = wave >> 1;
+
+  // this lane's source rows for each of its wave's loads (clamped in range:
+  // rows past the end are loaded but never stored)
+  const TS *src[LOADS];
+  int dst_off[LOADS];
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) {
+    const int ins = wave * LOADS + u;
+    const int row16 = lane >> 2, slot = lane & 3;
+    const int chunk = slot ^ lds_swz(row16);
+    if (ins < BN / 16) {
+      int n = n0 + ins * 16 + row16;
+      n = n < N ? n : N - 1;
+      src[u] = W + (int64_t)n * K + chunk * 8;
+      dst_off[u] = ins * 16 * ROWB;
+    } else {
+      int64_t r = r0 + (ins - BN / 16) * 16 + row16;
+      r = r < R ? r : R - 1;
+      src[u] = X + r * K + chunk * 8;
+      dst_off[u] = BN * ROWB + (ins - BN / 16) * 16 * ROWB;
+    }
+  }
+  auto issue = [&](int ks, int stage) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u)
+      __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[u] + ks * kBK),
+                                       (lds_void *)(smem + stage * STAGE + dst_off[u]), 16, 0, 0);
+  };
+
+  f32x4 acc[NI][RJ];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ksteps = K / kBK;
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < ksteps) issue(st, st);
+
+  const int frow = lane & 15, fc = lane >> 4;
+  const int a_off = (wn * (BN / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
+  const int b_off = BN * ROWB + (wr * (BR / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
+  int stage = 0;
+  for (int ks = 0; ks < ksteps; ++ks) {
+    // stage ks must have landed: later stages issued so far = min(S-2, ksteps-1-ks)
+    const int later = ksteps - 1 - ks;
+    if (S >= 4 && later >= 2) wait_vm<2 * LOADS>();
+    else if (S >= 3 && later >= 1) wait_vm<LOADS>();
+    else wait_vm<0>();
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    if (ks + S - 1 < ksteps) {
+      int st = stage + S - 1;
+      st = st >= S ? st - S : st;
+      issue(ks + S - 1, st);
+    }
+    const unsigned char *base = smem + stage * STAGE;
+    frag fa[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      fa[i] = *reinterpret_cast<const frag *>(base + a_off + i * 16 * ROWB);
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+      const frag fb = *reinterpret_cast<const frag *>(base + b_off + j * 16 * ROWB);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+    }
+    stage = stage + 1 == S ? 0 : stage + 1;
+  }
+
+  // epilogue: bias + ReLU, round, stage the tile in LDS, write rows with
+  // 16-byte stores.  lane holds D[4*(lane/16) + e][lane % 16] of each block.
+  wait_vm<0>();
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+  uint16_t *sout = reinterpret_cast<uint16_t *>(smem);
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int nl = wn * (BN / 2) + i * 16 + dn;
+    float bv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bv[e] = (n0 + nl + e < N) ? bias[n0 + nl + e] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+      const int rl = wr * (BR / 2) + j * 16 + dr;
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = acc[i][j][e] + bv[e];
+        o[e] = t > 0.0f ? t : 0.0f;
+      }
+      uint2 packed;
+      packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
+      packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
+      *reinterpret_cast<uint2 *>(sout + rl * OUT_STRIDE + nl) = packed;
+    }
+  }
+  compiler_fence();
+  __syncthreads();
+  constexpr int CPRW = BN / 8;  // 16-byte chunks per output row
+  for (int idx = tid; idx < BR * CPRW; idx += 256) {
+    const int rl = idx / CPRW, c = idx - rl * CPRW;
+    const int64_t r = r0 + rl;
+    const int n = n0 + c * 8;
+    if (r < R && n < N)
+      *reinterpret_cast<uint4 *>(Y + r * N + n) =
+          *reinterpret_cast<const uint4 *>(sout + rl * OUT_STRIDE + c * 8);
   }
 }
 
@@ -230,14 +391,27 @@ __global__ __launch_bounds__(256) void head_kernel(const TS *__restrict__ A, con
 }
 
 // ------------------------------------------------------------- launchers
-template <typename TS, int BN>
+template <typename TS, int BR, int BN>
 static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, void *y, int64_t R,
                                int N, int K, hipStream_t s) {
   const int tiles_n = (N + BN - 1) / BN;
-  const int64_t tiles_r = (R + kBM - 1) / kBM;
+  const int64_t tiles_r = (R + BR - 1) / BR;
   const int64_t total = tiles_r * tiles_n;
   if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_relu_mfma_kernel<TS, BN>), dim3((unsigned)total), dim3(256), 0, s,
+  hipLaunchKernelGGL((dense_relu_mfma_kernel<TS, BR, BN>), dim3((unsigned)total), dim3(256), 0, s,
+                     static_cast<const TS *>(x), static_cast<const TS *>(w), b,
+                     static_cast<TS *>(y), R, N, K, tiles_n, (int)total);
+  return hipGetLastError();
+}
+
+template <typename TS, int BR, int BN, int S>
+static hipError_t dense_pipe_t(const void *x, const void *w, const float *b, void *y, int64_t R,
+                               int N, int K, hipStream_t s) {
+  const int tiles_n = (N + BN - 1) / BN;
+  const int64_t tiles_r = (R + BR - 1) / BR;
+  const int64_t total = tiles_r * tiles_n;
+  if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((dense_relu_pipe_kernel<TS, BR, BN, S>), dim3((unsigned)total), dim3(256), 0, s,
                      static_cast<const TS *>(x), static_cast<const TS *>(w), b,
                      static_cast<TS *>(y), R, N, K, tiles_n, (int)total);
   return hipGetLastError();
@@ -246,8 +420,12 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
 template <typename TS>
 static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, void *y, int64_t R,
                                 int N, int K, hipStream_t s) {
-  if (N % 128 == 0) return dense_mfma_t<TS, 128>(x, w, b, y, R, N, K, s);
-  return dense_mfma_t<TS, 64>(x, w, b, y, R, N, K, s);
+  if (K % kBK == 0 && N % 8 == 0) {
+    if (N % 128 == 0) return dense_pipe_t<TS, 256, 128, 3>(x, w, b, y, R, N, K, s);
+    return dense_pipe_t<TS, 256, 64, 3>(x, w, b, y, R, N, K, s);
+  }
+  if (N % 128 == 0) return dense_mfma_t<TS, 256, 128>(x, w, b, y, R, N, K, s);
+  return dense_mfma_t<TS, 256, 64>(x, w, b, y, R, N, K, s);
 }
 
 hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
