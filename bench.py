@@ -52,6 +52,9 @@ def stage_work(cfg, batch, stage):
     if stage.startswith("dense"):
         li = int(stage[5:])
         return "mfma", 2.0 * R * cfg.widths[li] * cfg.widths[li + 1]
+    if stage == "tail":
+        w = cfg.widths
+        return "mfma", 2.0 * R * (w[-4] * w[-3] + w[-3] * w[-2] + w[-2] * w[-1])
     if stage == "head":
         k = cfg.widths[-2]
         return "hbm", R * k * es + R * 4

@@ -407,11 +407,15 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
     if ((e = launch_gather_se(m->dtype, kApplyWeights, D.linear_log, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se (apply) launch");
   }
-  // network: hidden layers ping-pong between two activation buffers
+  // network: hidden layers ping-pong between two activation buffers; the
+  // last two hidden layers and the head run fused when their widths allow
   const int L = D.n_layers;
+  const bool fuse_tail = L >= 3 && tail_supported(m->dtype, m->widths[L - 3], m->widths[L - 2],
+                                                  m->widths[L - 1], m->widths[L]);
+  const int n_separate = fuse_tail ? L - 3 : L - 1;
   const void *in = W + wl.X;
   unsigned char *bufs[2] = {W + wl.actA, W + wl.actB};
-  for (int l = 0; l + 1 < L; ++l) {
+  for (int l = 0; l < n_separate; ++l) {
     void *outp = bufs[l & 1];
     if ((e = marks.mark(l < 12 ? kDenseNames[l] : "dense")) != hipSuccess)
       return hip_fail(m, e, "profile event");
@@ -420,10 +424,19 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
       return hip_fail(m, e, "dense layer launch");
     in = outp;
   }
-  if ((e = marks.mark("head")) != hipSuccess) return hip_fail(m, e, "profile event");
-  if ((e = launch_head(m->dtype, in, A + al.w[L - 1], reinterpret_cast<const float *>(A + al.b[L - 1]),
-                       scores, R, m->widths[L - 1], m->widths[L], s)) != hipSuccess)
-    return hip_fail(m, e, "head launch");
+  if (fuse_tail) {
+    if ((e = marks.mark("tail")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_mlp_tail(m->dtype, in, A + al.w[L - 3], reinterpret_cast<const float *>(A + al.b[L - 3]),
+                             A + al.w[L - 2], reinterpret_cast<const float *>(A + al.b[L - 2]),
+                             A + al.w[L - 1], reinterpret_cast<const float *>(A + al.b[L - 1]),
+                             m->widths[L], scores, R, s)) != hipSuccess)
+      return hip_fail(m, e, "tail launch");
+  } else {
+    if ((e = marks.mark("head")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_head(m->dtype, in, A + al.w[L - 1], reinterpret_cast<const float *>(A + al.b[L - 1]),
+                         scores, R, m->widths[L - 1], m->widths[L], s)) != hipSuccess)
+      return hip_fail(m, e, "head launch");
+  }
   if ((e = marks.mark(nullptr)) != hipSuccess) return hip_fail(m, e, "profile event");
   if (validate) {
     int32_t flag = 0;

@@ -15,9 +15,13 @@
 //                   the workgroups sharing one row block of X run on the same
 //                   XCD (workgroup i is dispatched to XCD i mod 8) and reuse
 //                   it from that XCD's L2.
+//  mlp_tail         the last two hidden layers and the head fused over
+//                   64-row tiles held in LDS.
 //  dense_relu_f32   the same layer in fp32 FMA (the fp32 model).
 //  head             last layer (n_out = 1 or 2) in fp32 plus sigmoid or
 //                   two-way softmax; writes the CTR.
+#include <type_traits>
+
 #include "cold_internal.h"
 
 namespace cold {
@@ -37,6 +41,19 @@ template <> struct Mfma<_Float16> {
   typedef f16x8 frag;
   __device__ static inline f32x4 mac(const frag &a, const frag &b, const f32x4 &c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+template <typename TS> struct Mfma32;
+template <> struct Mfma32<__bf16> {
+  __device__ static inline f32x16 mac(const bf16x8 &a, const bf16x8 &b, const f32x16 &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma32<_Float16> {
+  __device__ static inline f32x16 mac(const f16x8 &a, const f16x8 &b, const f32x16 &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
 };
 
@@ -187,8 +204,8 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-template <typename TS, int BR, int BN, int S>
-__global__ __launch_bounds__(256, 2) void dense_relu_pipe_kernel(const TS *__restrict__ X,
+template <typename TS, int BR, int BN, int S, int MINW = 2>
+__global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__restrict__ X,
                                                                  const TS *__restrict__ W,
                                                                  const float *__restrict__ bias,
                                                                  TS *__restrict__ Y, int64_t R, int N,
@@ -326,6 +343,267 @@ __global__ __launch_bounds__(256, 2) void dense_relu_pipe_kernel(const TS *__res
   }
 }
 
+// The pipelined layer on v_mfma_f32_32x32x16 (in a register-only loop on
+// gfx950 this form sustains about 1.6x the rate of 16x16x32): WGR x WGN waves
+// per block (64 * WGR * WGN threads), block tile BR x BN, wave tile
+// (BR/WGR) x (BN/WGN) in 32 x 32 blocks.  Fragment of a 32-row block, half h
+// of a 32-deep K step: lane l reads row l % 32, chunk 2h + l / 32.
+// Accumulator element e of lane l holds D[8 (e / 4) + 4 (l / 32) + e % 4][l % 32].
+template <typename TS, int BR, int BN, int WGR, int WGN, int S, int MINW>
+__global__ __launch_bounds__(64 * WGR * WGN, MINW) void dense_relu_wg_kernel(
+    const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias,
+    TS *__restrict__ Y, int64_t R, int N, int K, int tiles_n, int tiles_total) {
+  typedef typename Mfma<TS>::frag frag;
+  typedef __attribute__((address_space(3))) void lds_void;
+  constexpr int NT = 64 * WGR * WGN, NW = WGR * WGN;
+  constexpr int WTR = BR / WGR, WTN = BN / WGN;        // wave tile
+  constexpr int NI = WTN / 32, RJ = WTR / 32;          // 32x32 blocks per wave
+  constexpr int ROWB = kBK * 2;
+  constexpr int STAGE = (BN + BR) * ROWB;
+  constexpr int LOADS = (BN + BR) / 16 / NW;           // 16-row loads per wave per stage
+  constexpr int OUT_STRIDE = BN + 8;
+  constexpr int OUT_BYTES = BR * OUT_STRIDE * 2;
+  constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
+  static_assert((BN + BR) % (16 * NW) == 0 && NI >= 1 && RJ >= 1, "tile shape");
+  static_assert(S >= 2 && S <= 4, "stages");
+  __shared__ __align__(16) unsigned char smem[SMEM];
+
+  const int tile = xcd_tile(blockIdx.x, tiles_total);
+  const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
+  const int64_t r0 = (int64_t)tr * BR;
+  const int n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave % WGN, wr = wave / WGN;
+
+  const TS *src[LOADS];
+  int dst_off[LOADS];
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) {
+    const int ins = wave * LOADS + u;
+    const int row16 = lane >> 2, slot = lane & 3;
+    const int chunk = slot ^ lds_swz(row16);
+    if (ins < BN / 16) {
+      int n = n0 + ins * 16 + row16;
+      n = n < N ? n : N - 1;
+      src[u] = W + (int64_t)n * K + chunk * 8;
+      dst_off[u] = ins * 16 * ROWB;
+    } else {
+      int64_t r = r0 + (ins - BN / 16) * 16 + row16;
+      r = r < R ? r : R - 1;
+      src[u] = X + r * K + chunk * 8;
+      dst_off[u] = BN * ROWB + (ins - BN / 16) * 16 * ROWB;
+    }
+  }
+  auto issue = [&](int ks, int stage) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u)
+      __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[u] + ks * kBK),
+                                       (lds_void *)(smem + stage * STAGE + dst_off[u]), 16, 0, 0);
+  };
+
+  f32x16 acc[NI][RJ];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int j = 0; j < RJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  const int ksteps = K / kBK;
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < ksteps) issue(st, st);
+
+  const int frow = lane & 31, fh = lane >> 5;
+  const int a_row = (wn * WTN + frow) * ROWB;
+  const int b_row = BN * ROWB + (wr * WTR + frow) * ROWB;
+  const int swz = lds_swz(frow & 15);
+  int stage = 0;
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int later = ksteps - 1 - ks;
+    if (S >= 4 && later >= 2) wait_vm<2 * LOADS>();
+    else if (S >= 3 && later >= 1) wait_vm<LOADS>();
+    else wait_vm<0>();
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    if (ks + S - 1 < ksteps) {
+      int st = stage + S - 1;
+      st = st >= S ? st - S : st;
+      issue(ks + S - 1, st);
+    }
+    const unsigned char *base = smem + stage * STAGE;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int coff = (((2 * h + fh) ^ swz) * 16);
+      frag fa[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        fa[i] = *reinterpret_cast<const frag *>(base + a_row + i * 32 * ROWB + coff);
+#pragma unroll
+      for (int j = 0; j < RJ; ++j) {
+        const frag fb = *reinterpret_cast<const frag *>(base + b_row + j * 32 * ROWB + coff);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) acc[i][j] = Mfma32<TS>::mac(fa[i], fb, acc[i][j]);
+      }
+    }
+    stage = stage + 1 == S ? 0 : stage + 1;
+  }
+
+  wait_vm<0>();
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+  uint16_t *sout = reinterpret_cast<uint16_t *>(smem);
+  const int dr = lane & 31, dq = (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int nl = wn * WTN + i * 32 + 8 * g + dq;
+      float bv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bv[e] = (n0 + nl + e < N) ? bias[n0 + nl + e] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < RJ; ++j) {
+        const int rl = wr * WTR + j * 32 + dr;
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float t = acc[i][j][4 * g + e] + bv[e];
+          o[e] = t > 0.0f ? t : 0.0f;
+        }
+        uint2 packed;
+        packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
+        packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
+        *reinterpret_cast<uint2 *>(sout + rl * OUT_STRIDE + nl) = packed;
+      }
+    }
+  }
+  compiler_fence();
+  __syncthreads();
+  constexpr int CPRW = BN / 8;
+  for (int idx = tid; idx < BR * CPRW; idx += NT) {
+    const int rl = idx / CPRW, c = idx - rl * CPRW;
+    const int64_t r = r0 + rl;
+    const int n = n0 + c * 8;
+    if (r < R && n < N)
+      *reinterpret_cast<uint4 *>(Y + r * N + n) =
+          *reinterpret_cast<const uint4 *>(sout + rl * OUT_STRIDE + c * 8);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fused tail: the last two hidden layers and the output head in one kernel,
+// K0 -> N1 -> N2 (ReLU) -> n_out (sigmoid or softmax), for 64-row tiles.  The
+// row tile lives in LDS between layers; the small weight matrices (N1 x K0 and
+// N2 x N1) are read as MFMA fragments straight from global memory, where
+// every workgroup finds them in L2.  Hidden activations are rounded to the
+// storage type between layers, as the separate layers do.
+template <typename TS, int K0, int N1, int N2>
+__global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
+                                                       const TS *__restrict__ W1,
+                                                       const float *__restrict__ b1,
+                                                       const TS *__restrict__ W2,
+                                                       const float *__restrict__ b2,
+                                                       const TS *__restrict__ Wh,
+                                                       const float *__restrict__ bh, int n_out,
+                                                       float *__restrict__ scores, int64_t R) {
+  typedef typename Mfma<TS>::frag frag;
+  constexpr int BR = 64;
+  constexpr int S0 = K0 + 8, S1 = N1 + 8, S2 = N2 + 8;   // padded LDS rows
+  static_assert(K0 % 32 == 0 && N1 % 32 == 0 && N2 % 32 == 0 && N1 % 64 == 0 && N2 % 64 == 0,
+                "tail widths");
+  __shared__ __align__(16) TS s_in[BR * S0];
+  __shared__ __align__(16) TS s_h1[BR * S1];
+  __shared__ __align__(16) TS s_h2[BR * S2];
+  __shared__ float s_wh[2 * N2];
+  __shared__ float s_bh[2];
+
+  const int64_t r0 = (int64_t)blockIdx.x * BR;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // input tile (rows past the end are clamped: loaded, never stored)
+  constexpr int CPR0 = K0 / 8;
+  for (int c = tid; c < BR * CPR0; c += 256) {
+    const int row = c / CPR0, kc = c - row * CPR0;
+    int64_t r = r0 + row;
+    r = r < R ? r : R - 1;
+    *reinterpret_cast<uint4 *>(&s_in[row * S0 + kc * 8]) =
+        *reinterpret_cast<const uint4 *>(A + r * K0 + kc * 8);
+  }
+  for (int i = tid; i < n_out * N2; i += 256) s_wh[i] = Elem<TS>::to_f32(Wh[i]);
+  if (tid < n_out) s_bh[tid] = bh[tid];
+  __syncthreads();
+
+  const int frow = lane & 15, fk = (lane >> 4) * 8;
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+  // one hidden layer on the tile: wave w owns outputs [w*NOUT/4, (w+1)*NOUT/4)
+  auto layer = [&](const TS *in, int s_in_stride, int kdim, const TS *Wg, const float *bg,
+                   TS *out, int s_out_stride, auto nout_tag) {
+    constexpr int NOUT = decltype(nout_tag)::value;
+    constexpr int NB = NOUT / 4 / 16;     // 16-wide output blocks per wave
+    f32x4 acc[NB][BR / 16];
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int j = 0; j < BR / 16; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nbase = wave * (NOUT / 4);
+    for (int k0 = 0; k0 < kdim; k0 += 32) {
+      frag fa[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        fa[i] = *reinterpret_cast<const frag *>(Wg + (int64_t)(nbase + i * 16 + frow) * kdim + k0 + fk);
+#pragma unroll
+      for (int j = 0; j < BR / 16; ++j) {
+        const frag fb = *reinterpret_cast<const frag *>(&in[(j * 16 + frow) * s_in_stride + k0 + fk]);
+#pragma unroll
+        for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int n = nbase + i * 16 + dn;
+#pragma unroll
+      for (int j = 0; j < BR / 16; ++j) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float t = acc[i][j][e] + bg[n + e];
+          o[e] = t > 0.0f ? t : 0.0f;
+        }
+        uint2 packed;
+        packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
+        packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
+        *reinterpret_cast<uint2 *>(&out[(j * 16 + dr) * s_out_stride + n]) = packed;
+      }
+    }
+  };
+  layer(s_in, S0, K0, W1, b1, s_h1, S1, std::integral_constant<int, N1>{});
+  __syncthreads();
+  layer(s_h1, S1, N1, W2, b2, s_h2, S2, std::integral_constant<int, N2>{});
+  __syncthreads();
+
+  // head: 4 threads per row, each over a quarter of the N2 inputs
+  const int row = tid >> 2, q = tid & 3;
+  float z0 = 0.0f, z1 = 0.0f;
+#pragma unroll 4
+  for (int k = q * (N2 / 4); k < (q + 1) * (N2 / 4); ++k) {
+    const float x = Elem<TS>::to_f32(s_h2[row * S2 + k]);
+    z0 += s_wh[k] * x;
+    if (n_out > 1) z1 += s_wh[N2 + k] * x;
+  }
+  z0 += __shfl_xor(z0, 1);
+  z0 += __shfl_xor(z0, 2);
+  z1 += __shfl_xor(z1, 1);
+  z1 += __shfl_xor(z1, 2);
+  const int64_t r = r0 + row;
+  if (q == 0 && r < R) {
+    z0 += s_bh[0];
+    if (n_out > 1) z1 += s_bh[1];
+    scores[r] = n_out == 1 ? 1.0f / (1.0f + expf(-z0)) : 1.0f / (1.0f + expf(z0 - z1));
+  }
+}
+
 // fp32 layer: 64 x 64 output tile, 4 x 4 per thread, K in steps of 16.
 __global__ __launch_bounds__(256) void dense_relu_f32_kernel(const float *__restrict__ X,
                                                              const float *__restrict__ W,
@@ -439,6 +717,28 @@ hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const floa
   }
   if (dtype == kBF16) return dense_mfma_dt<__bf16>(x, w, b, y, R, N, K, s);
   return dense_mfma_dt<_Float16>(x, w, b, y, R, N, K, s);
+}
+
+bool tail_supported(int dtype, int K0, int N1, int N2, int n_out) {
+  return dtype != kF32 && K0 == 256 && N1 == 128 && N2 == 64 && (n_out == 1 || n_out == 2);
+}
+
+hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float *b1,
+                           const void *w2, const float *b2, const void *wh, const float *bh,
+                           int32_t n_out, float *scores, int64_t R, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((R + 63) / 64));
+  if (dtype == kBF16)
+    hipLaunchKernelGGL((mlp_tail_kernel<__bf16, 256, 128, 64>), grid, dim3(256), 0, s,
+                       static_cast<const __bf16 *>(a), static_cast<const __bf16 *>(w1), b1,
+                       static_cast<const __bf16 *>(w2), b2, static_cast<const __bf16 *>(wh), bh,
+                       n_out, scores, R);
+  else
+    hipLaunchKernelGGL((mlp_tail_kernel<_Float16, 256, 128, 64>), grid, dim3(256), 0, s,
+                       static_cast<const _Float16 *>(a), static_cast<const _Float16 *>(w1), b1,
+                       static_cast<const _Float16 *>(w2), b2, static_cast<const _Float16 *>(wh), bh,
+                       n_out, scores, R);
+  return hipGetLastError();
 }
 
 hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, float *scores,
