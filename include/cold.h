@@ -69,8 +69,10 @@ extern "C" {
  * The SE block has H = max(1, M / se_reduction) hidden units.
  * widths[0] = D_in; widths[1..n_layers-1] are ReLU hidden layers;
  * widths[n_layers] is 1 (CTR = sigmoid) or 2 (softmax, CTR = class 1).
- * Supported: emb_dim * sizeof(dtype) a multiple of 16 bytes, M <= 1024,
- * hidden widths multiples of 8 (bf16/f16), last hidden width <= 1024. */
+ * Supported: emb_dim * sizeof(dtype) a multiple of 16 bytes, a network
+ * input row of at most 1024 such 16-byte chunks (M <= 512 at emb_dim 16 in
+ * bf16/fp16), hidden widths multiples of 8 (bf16/f16), last hidden width
+ * <= 8192 (fp32 head weights in 64 KB). */
 typedef struct cold_model_desc {
   int32_t n_user, n_seq, n_ad, n_cross;
   int32_t emb_dim;

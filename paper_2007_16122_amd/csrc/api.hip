@@ -25,7 +25,7 @@ struct ArenaLayout {
 };
 
 struct WorkLayout {
-  size_t err, U, urow, X, actA, actB, sbuf, partial, mask, total;
+  size_t err, U, zU, urow, X, actA, actB, sbuf, partial, mask, total;
 };
 
 }  // namespace
@@ -100,6 +100,7 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   const bool topk = m.desc.topk_k > 0;
   w.err = take(sizeof(int32_t));
   w.U = take(sizeof(float) * (size_t)Q * m.nus * m.d);
+  w.zU = take(sizeof(float) * (size_t)Q * m.nus);
   w.urow = take(sizeof(int32_t) * (size_t)Q * (m.desc.n_user > 0 ? m.desc.n_user : 1));
   w.X = take((size_t)m.es * R * m.D_in);
   w.actA = take((size_t)m.es * R * m.max_hidden);
@@ -181,7 +182,7 @@ int cold_create_model(const cold_model_desc *desc, cold_model **out) {
   if ((D.emb_dim * es) % 16 != 0 || !is_pow2(D.emb_dim / epc) || D.emb_dim / epc > 64)
     return COLD_ERR_DTYPE;
   const int cpr = M * (D.emb_dim / epc);
-  if (cpr > kGatherThreads * kGatherChunksPerThread) return COLD_ERR_SHAPE;
+  if (cpr > kGatherMaxChunksPerRow) return COLD_ERR_SHAPE;
   if (D.widths[0] != M * D.emb_dim) return COLD_ERR_SHAPE;
   const int n_out = D.widths[D.n_layers];
   if (n_out != 1 && n_out != 2) return COLD_ERR_SHAPE;
@@ -357,8 +358,6 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   GatherArgs g{};
   g.M = m->M; g.n_user = D.n_user; g.n_seq = D.n_seq; g.n_ad = D.n_ad; g.n_cross = D.n_cross;
   g.d = m->d; g.H = m->H;
-  const int cpr = m->M * (m->d * m->es / 16);
-  g.rows_per_tile = (kGatherThreads * kGatherChunksPerThread) / cpr;
   g.R = R; g.Q = Q; g.n_seq_ids = b->n_seq_ids;
   g.req_off = b->req_off; g.user_ids = b->user_ids; g.ad_ids = b->ad_ids; g.cross_ids = b->cross_ids;
   g.seq_off = b->seq_off; g.seq_ids = b->seq_ids;
@@ -370,6 +369,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   g.w2 = reinterpret_cast<const float *>(A + al.w2);
   g.b2 = reinterpret_cast<const float *>(A + al.b2);
   g.U = reinterpret_cast<float *>(W + wl.U);
+  g.zU = reinterpret_cast<float *>(W + wl.zU);
   g.urow = reinterpret_cast<int32_t *>(W + wl.urow);
   g.X = W + wl.X;
   g.rows_out = rows_out;

@@ -121,7 +121,10 @@ __device__ __forceinline__ int32_t resolve_row(const void *ids, int64_t i, int g
 // ------------------------------------------------------------ kernel params
 struct GatherArgs {
   int32_t M, n_user, n_seq, n_ad, n_cross, d, H;
-  int32_t rows_per_tile;          // T
+  int32_t rows_per_tile;          // rows per wave (set by the launcher)
+  int32_t wave_lds_bytes;         // LDS per wave (set by the launcher)
+  int32_t se_lds_bytes;           // LDS for SE parameters, 0 if read from global
+  int32_t se_in_lds;
   int64_t R, Q, n_seq_ids;
   const int32_t *req_off;         // [Q+1]
   const void *user_ids;           // [n_user][Q]
@@ -134,6 +137,7 @@ struct GatherArgs {
   const uint64_t *table_magic;    // device [M]
   const float *w1, *b1, *w2, *b2; // SE parameters
   float *U;                       // [Q][n_user+n_seq][d] pooled user side
+  float *zU;                      // [Q][n_user+n_seq] squeeze of the user groups
   int32_t *urow;                  // [Q][max(n_user,1)] resolved user rows
   void *X;                        // [R][M*d] network input
   float *s_buf;                   // [R][M] SE weights (written, or read in apply mode)
@@ -163,7 +167,7 @@ hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, 
                        int64_t R, int32_t K, int32_t n_out, hipStream_t s);
 
 constexpr int kGatherThreads = 256;
-constexpr int kGatherChunksPerThread = 8;
+constexpr int kGatherMaxChunksPerRow = 1024;  // 64 lanes x 16 chunks
 constexpr int kMaskParts = 64;
 
 }  // namespace cold

@@ -6,16 +6,16 @@
 //              once per request into fp32 and broadcast to every candidate
 //              row of the request later (Section 3.3, parallelism: user
 //              features are shared by the ads of a query).
-//  gather_se   one workgroup per tile of T rows.  Ids are read field by
-//              field (the column layout of Section 3.3); each thread then
-//              owns 16-byte chunks of the tile's network input, laid out so
-//              that the tile's output is one contiguous, fully coalesced
-//              region.  Chunks hold the gathered embedding in registers
-//              while the squeeze (group mean), the two SE layers and the
-//              sigmoid (Section 3.2, Eq. 2) run over the tile from LDS; the
-//              chunks are then reweighted by s_g (Section 3.2), optionally
-//              passed through linear_log (Eq. 3) in fp32, and rounded once
-//              to the storage type.
+//  gather_se   each wave owns a few consecutive rows and synchronises only
+//              within itself.  Ids are read field by field (the column
+//              layout of Section 3.3); each lane then owns 16-byte chunks of
+//              the wave's network input, laid out so that the wave's output
+//              is one contiguous, fully coalesced region.  Chunks hold the
+//              gathered embedding in registers while the squeeze (group
+//              mean), the two SE layers and the sigmoid (Section 3.2, Eq. 2)
+//              run from LDS; the chunks are then reweighted by s_g
+//              (Section 3.2), optionally passed through linear_log (Eq. 3)
+//              in fp32, and rounded once to the storage type.
 //  group_mask  per-request mean importance of each group over the request's
 //              rows, then the top-k groups (Section 3.2, feature group
 //              selection); ties go to the lower group index.
@@ -79,37 +79,79 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
     }
     a.U[(q * nus + g) * d + k] = acc;
   }
+  __syncthreads();
+  for (int g = threadIdx.x; g < nus; g += blockDim.x) {  // squeeze: mean over d
+    float acc = 0.0f;
+    for (int k = 0; k < d; ++k) acc += a.U[(q * nus + g) * d + k];
+    a.zU[q * nus + g] = acc / (float)d;
+  }
 }
 
 // ------------------------------------------------------------- gather_se
-template <typename TS, int MODE, bool LL, bool HASHED>
+// All synchronisation inside a wave: each wave owns Tw consecutive rows and
+// moves on without block barriers, so the 16 waves of a CU overlap their
+// gathers freely.  Lane l of a wave owns chunks l, l+64, ... of the wave's
+// contiguous output region (Tw rows x M*d elements, 16 bytes per chunk), so
+// the final store is coalesced; table chunks are held raw (4 VGPRs) between
+// the gather and the reweighting.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <typename TS, int MODE, bool LL, bool HASHED, int CPT>
 __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a) {
   constexpr int EPC = Elem<TS>::kPerChunk;  // elements per 16-byte chunk
-  constexpr int CPT = kGatherChunksPerThread;
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int M = a.M, d = a.d, H = a.H;
-  const int nu = a.n_user, nus = a.n_user + a.n_seq, nax = a.n_ad + a.n_cross;
-  const int T = a.rows_per_tile;
+  const int nus = a.n_user + a.n_seq, nax = a.n_ad + a.n_cross;
+  const int Tw = a.rows_per_tile;          // rows per wave
   const int CPG = d / EPC;                 // chunks per group (power of two)
   const int CPR = M * CPG;                 // chunks per row
+  const int lcpg = __builtin_ctz(CPG);
   const int64_t R = a.R, Q = a.Q;
-  const int64_t r0 = (int64_t)blockIdx.x * T;
-  const int tid = threadIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // (row, chunk) of this lane's first chunk; later chunks step by 64
+  const int t_first = lane / CPR, c_first = lane - t_first * CPR;
+  auto advance = [&](int &t, int &c) {
+    c += 64;
+    while (c >= CPR) { c -= CPR; ++t; }
+  };
 
-  int32_t *ridx = reinterpret_cast<int32_t *>(smem);   // [T][nax]
-  int32_t *rq = ridx + T * nax;                        // [T]
-  float *z = reinterpret_cast<float *>(rq + T);        // [T][M]
-  float *sw = z + T * M;                               // [T][M]
-  float *hid = sw + T * M;                             // [T][H]
+  // SE parameters of the block in LDS (when they fit), loaded once
+  float *w1 = const_cast<float *>(a.w1), *b1 = const_cast<float *>(a.b1);
+  float *w2 = const_cast<float *>(a.w2), *b2 = const_cast<float *>(a.b2);
+  unsigned char *wbase = smem;
+  if constexpr (MODE != kApplyWeights) {
+    if (a.se_in_lds) {
+      float *sw = reinterpret_cast<float *>(smem);
+      const int nw = H * M;
+      for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[i] = a.w1[i];
+      for (int i = threadIdx.x; i < H; i += kGatherThreads) sw[nw + i] = a.b1[i];
+      for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[nw + H + i] = a.w2[i];
+      for (int i = threadIdx.x; i < M; i += kGatherThreads) sw[2 * nw + H + i] = a.b2[i];
+      w1 = sw; b1 = sw + nw; w2 = sw + nw + H; b2 = sw + 2 * nw + H;
+      wbase = smem + a.se_lds_bytes;
+    }
+    __syncthreads();  // the only block-wide barrier
+  }
+  int32_t *ridx = reinterpret_cast<int32_t *>(wbase + (size_t)wave * a.wave_lds_bytes);  // [Tw][nax]
+  int32_t *rq = ridx + Tw * nax;                       // [Tw]
+  float *z = reinterpret_cast<float *>(rq + Tw);       // [Tw][M]
+  float *sv = z + Tw * M;                              // [Tw][M]
+  float *hid = sv + Tw * M;                            // [Tw][H]
 
-  // ---- phase 0: request of each row; ad/cross ids -> table rows (column-wise)
-  for (int t = tid; t < T; t += kGatherThreads) {
+  const int64_t r0 = ((int64_t)blockIdx.x * (kGatherThreads / 64) + wave) * Tw;
+  if (r0 >= R) return;
+
+  // ---- request of each row; ad/cross ids -> table rows (field by field)
+  for (int t = lane; t < Tw; t += 64) {
     const int64_t r = r0 + t;
     rq[t] = r < R ? (int32_t)request_of_row(a.req_off, Q, r) : 0;
   }
-  for (int i = tid; i < T * nax; i += kGatherThreads) {
-    const int f = i / T, t = i - f * T;
+  for (int i = lane; i < Tw * nax; i += 64) {
+    const int f = i / Tw, t = i - f * Tw;
     const int64_t r = r0 + t;
     const int g = nus + f;
     int32_t row = -1;
@@ -117,117 +159,119 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       const bool is_ad = f < a.n_ad;
       const void *ids = is_ad ? a.ad_ids : a.cross_ids;
       const int64_t idx = (int64_t)(is_ad ? f : f - a.n_ad) * R + r;
-      if constexpr (MODE == kApplyWeights) {
-        // masked-out groups are never read
+      bool keep = true;
+      if constexpr (MODE == kApplyWeights) {  // masked-out groups are never read
         const int64_t q = request_of_row(a.req_off, Q, r);
-        if (a.mask[q * M + g])
-          row = resolve_row<HASHED>(ids, idx, g, a.table_rows[g], a.table_magic[g], a.err);
-      } else {
-        row = resolve_row<HASHED>(ids, idx, g, a.table_rows[g], a.table_magic[g], a.err);
-        if (a.rows_out) a.rows_out[(int64_t)g * R + r] = row;
+        keep = a.mask[q * M + g] != 0;
       }
+      if (keep) row = resolve_row<HASHED>(ids, idx, g, a.table_rows[g], a.table_magic[g], a.err);
+      if (MODE != kApplyWeights && a.rows_out) a.rows_out[(int64_t)g * R + r] = row;
     }
     ridx[t * nax + f] = row;
   }
-  __syncthreads();
+  wave_sync();
   if (MODE != kApplyWeights && a.rows_out) {
-    for (int i = tid; i < T * nus; i += kGatherThreads) {
-      const int f = i / T, t = i - f * T;
+    for (int i = lane; i < Tw * nus; i += 64) {
+      const int f = i / Tw, t = i - f * Tw;
       const int64_t r = r0 + t;
-      if (r < R) a.rows_out[(int64_t)f * R + r] = f < nu ? a.urow[(int64_t)rq[t] * nu + f] : -1;
+      if (r < R)
+        a.rows_out[(int64_t)f * R + r] = f < a.n_user ? a.urow[(int64_t)rq[t] * a.n_user + f] : -1;
     }
   }
 
-  // ---- phase 1: gather chunks into registers, squeeze (mean over d)
-  float v[CPT][EPC];
+  // ---- gather every table chunk first (all loads in flight), then squeeze
+  uint4 raw[CPT];
+  {
+    int t = t_first, c = c_first;
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) {
-    const int i = tid + kGatherThreads * j;
-    const int t = i / CPR;
-    const int c = i - t * CPR;
-    const int g = c / CPG, p = c - g * CPG;
-    const bool valid = t < T && r0 + t < R;
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) v[j][e] = 0.0f;
-    if (valid) {
-      if (g < nus) {
-        bool keep = true;
-        if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
-        if (keep) {
-          const float4 *src = reinterpret_cast<const float4 *>(
-              a.U + ((int64_t)rq[t] * nus + g) * d + p * EPC);
-#pragma unroll
-          for (int e4 = 0; e4 < EPC / 4; ++e4) {
-            const float4 w = src[e4];
-            v[j][4 * e4] = w.x; v[j][4 * e4 + 1] = w.y;
-            v[j][4 * e4 + 2] = w.z; v[j][4 * e4 + 3] = w.w;
-          }
-        }
-      } else {
+    for (int j = 0; j < CPT; ++j) {
+      const int g = c >> lcpg, p = c & (CPG - 1);
+      raw[j] = make_uint4(0, 0, 0, 0);
+      if (t < Tw && r0 + t < R && g >= nus) {
         const int32_t row = ridx[t * nax + (g - nus)];
         if (row >= 0) {
           const TS *tab = static_cast<const TS *>(a.tables[g]);
-          const uint4 raw = *reinterpret_cast<const uint4 *>(tab + (int64_t)row * d + p * EPC);
-          Elem<TS>::unpack(raw, v[j]);
+          raw[j] = *reinterpret_cast<const uint4 *>(tab + (int64_t)row * d + p * EPC);
         }
       }
-    }
-    if constexpr (MODE != kApplyWeights) {
-      float part = 0.0f;
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) part += v[j][e];
-      for (int o = 1; o < CPG; o <<= 1) part += __shfl_xor(part, o);
-      if (t < T && p == 0) z[t * M + g] = valid ? part / (float)d : 0.0f;
+      advance(t, c);
     }
   }
-  __syncthreads();
-
-  // ---- phase 2: SE weights of the tile (Eq. 2), or stored weights x mask
   if constexpr (MODE != kApplyWeights) {
-    for (int it = tid; it < T * H; it += kGatherThreads) {
+    int t = t_first, c = c_first;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j, advance(t, c)) {
+      const int g = c >> lcpg, p = c & (CPG - 1);
+      float v[EPC];
+      Elem<TS>::unpack(raw[j], v);
+      float part = 0.0f;
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) part += v[e];
+      for (int o = 1; o < CPG; o <<= 1) part += __shfl_xor(part, o);
+      if (t < Tw && p == 0) {
+        float zz = 0.0f;
+        if (r0 + t < R) zz = g < nus ? a.zU[(int64_t)rq[t] * nus + g] : part / (float)d;
+        z[t * M + g] = zz;
+      }
+    }
+    wave_sync();
+
+    // ---- SE block of the wave's rows (Eq. 2)
+    for (int it = lane; it < Tw * H; it += 64) {
       const int t = it / H, jh = it - t * H;
-      float acc = a.b1[jh];
-      const float *w = a.w1 + (int64_t)jh * M;
+      float acc = b1[jh];
+      const float *w = w1 + jh * M;
       const float *zt = z + t * M;
       for (int g = 0; g < M; ++g) acc += w[g] * zt[g];
       hid[it] = acc > 0.0f ? acc : 0.0f;
     }
-    __syncthreads();
-    for (int it = tid; it < T * M; it += kGatherThreads) {
+    wave_sync();
+    for (int it = lane; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
-      float acc = a.b2[g];
-      const float *w = a.w2 + (int64_t)g * H;
+      float acc = b2[g];
+      const float *w = w2 + g * H;
       const float *ht = hid + t * H;
       for (int jh = 0; jh < H; ++jh) acc += w[jh] * ht[jh];
       const float sg = 1.0f / (1.0f + expf(-acc));
-      sw[it] = sg;
+      sv[it] = sg;
       if (a.s_buf && r0 + t < R) a.s_buf[r0 * M + it] = sg;
     }
   } else {
-    for (int it = tid; it < T * M; it += kGatherThreads) {
+    for (int it = lane; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
       float sg = 0.0f;
       if (r0 + t < R && a.mask[(int64_t)rq[t] * M + g]) sg = a.s_buf[r0 * M + it];
-      sw[it] = sg;
+      sv[it] = sg;
     }
   }
   if constexpr (MODE == kWeightsOnly) return;
-  __syncthreads();
+  wave_sync();
 
-  // ---- phase 3: reweight, linear_log, round, coalesced store
+  // ---- reweight, linear_log, round once, coalesced store
   TS *X = static_cast<TS *>(a.X);
+  int t = t_first, c = c_first;
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) {
-    const int i = tid + kGatherThreads * j;
-    const int t = i / CPR;
-    const int c = i - t * CPR;
-    const int g = c / CPG;
-    if (t < T && r0 + t < R) {
-      const float sg = sw[t * M + g];
+  for (int j = 0; j < CPT; ++j, advance(t, c)) {
+    const int i = lane + 64 * j;
+    const int g = c >> lcpg, p = c & (CPG - 1);
+    if (t < Tw && r0 + t < R) {
+      const float sg = sv[t * M + g];
+      float v[EPC];
+      if (g < nus) {
+        const float4 *src = reinterpret_cast<const float4 *>(
+            a.U + ((int64_t)rq[t] * nus + g) * d + p * EPC);
+#pragma unroll
+        for (int e4 = 0; e4 < EPC / 4; ++e4) {
+          const float4 w = src[e4];
+          v[4 * e4] = w.x; v[4 * e4 + 1] = w.y; v[4 * e4 + 2] = w.z; v[4 * e4 + 3] = w.w;
+        }
+      } else {
+        Elem<TS>::unpack(raw[j], v);
+      }
       float o[EPC];
 #pragma unroll
       for (int e = 0; e < EPC; ++e) {
-        const float x = sg * v[j][e];
+        const float x = sg * v[e];
         o[e] = LL ? linear_log(x) : x;
       }
       *reinterpret_cast<uint4 *>(X + (r0 * CPR + i) * EPC) = Elem<TS>::pack(o);
@@ -299,18 +343,35 @@ hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStre
   }
 }
 
+template <typename TS, int MODE, bool LL, int CPT>
+static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
+  constexpr int EPC = Elem<TS>::kPerChunk;
+  const int nax = a.n_ad + a.n_cross;
+  const int cpr = a.M * (a.d / EPC);
+  const int T = (64 * CPT) / cpr;  // rows per wave
+  a.rows_per_tile = T;
+  a.wave_lds_bytes = (int32_t)((sizeof(int32_t) * (size_t)(T * nax + T) +
+                                sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
+  const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
+  a.se_in_lds = MODE != kApplyWeights && se_floats * sizeof(float) <= 24 * 1024;
+  a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
+  const size_t shmem = (size_t)a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
+  const int64_t rows_per_block = 4 * (int64_t)T;
+  const dim3 grid((unsigned)((a.R + rows_per_block - 1) / rows_per_block));
+  if (hashed)
+    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, true, CPT>), grid, dim3(kGatherThreads), shmem, s, a);
+  else
+    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, false, CPT>), grid, dim3(kGatherThreads), shmem, s, a);
+  return hipGetLastError();
+}
+
+// chunks per lane: 16 when a row has more than 64 chunks (so a wave holds
+// several rows), else 8
 template <typename TS, int MODE, bool LL>
 static hipError_t gather_se_t(bool hashed, const GatherArgs &a, hipStream_t s) {
-  const int nax = a.n_ad + a.n_cross;
-  const int T = a.rows_per_tile;
-  const size_t shmem = sizeof(int32_t) * (size_t)(T * nax + T) +
-                       sizeof(float) * (size_t)(2 * T * a.M + T * a.H);
-  const dim3 grid((unsigned)((a.R + T - 1) / T));
-  if (hashed)
-    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, true>), grid, dim3(kGatherThreads), shmem, s, a);
-  else
-    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, false>), grid, dim3(kGatherThreads), shmem, s, a);
-  return hipGetLastError();
+  const int cpr = a.M * (a.d / Elem<TS>::kPerChunk);
+  if (cpr > 512) return gather_se_c<TS, MODE, LL, 16>(hashed, a, s);
+  return gather_se_c<TS, MODE, LL, 8>(hashed, a, s);
 }
 
 template <typename TS>
