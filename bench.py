@@ -26,6 +26,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+CSRC = os.path.join(ROOT, "paper_2007_16122_amd", "csrc")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic_{workload}.json")
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
 
 
@@ -180,6 +182,121 @@ def cpu_baseline(cfg, batch, params, target_s):
                       f"of the {cfg.name} batch, fp64 checker, {o['n_threads']} threads"}
 
 
+# ---------------------------------------------------------------------------
+# rocprofv3 post-processing (runs on the host after a profiled bench run)
+def _source_hashes():
+    import hashlib
+    out = {}
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(CSRC, name), "rb") as fh:
+                out[name] = hashlib.sha256(fh.read()).hexdigest()
+    return out
+
+
+def _stage_of(kernel_name, dense_index):
+    """Stage name of one of our kernels, in cold_score's launch order."""
+    if "user_pool" in kernel_name:
+        return "user_pool"
+    if "gather_se_kernel" in kernel_name:
+        return "gather_se"
+    if "mask_partial" in kernel_name or "mask_select" in kernel_name:
+        return "group_mask"
+    if "dense_relu" in kernel_name:
+        return f"dense{dense_index}"
+    if "mlp_tail" in kernel_name:
+        return "tail"
+    if "head_kernel" in kernel_name:
+        return "head"
+    return None
+
+
+def _last_call(rows, key_start="Start_Timestamp"):
+    """Dispatches of libcold kernels in the last complete scoring call,
+    as (stage, row) pairs in launch order."""
+    ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
+    ours.sort(key=lambda r: int(r[key_start]))
+    starts = [i for i, r in enumerate(ours) if "user_pool" in r["Kernel_Name"]]
+    if not starts:
+        return []
+    call = ours[starts[-1]:]
+    out, di = [], 0
+    for r in call:
+        st = _stage_of(r["Kernel_Name"], di)
+        if st and st.startswith("dense"):
+            di += 1
+        out.append((st, r))
+    return out
+
+
+def summarize_trace(trace_dir, command):
+    """Per-stage kernel durations (mean over the profiled calls) from a
+    rocprofv3 --kernel-trace CSV directory."""
+    import csv
+    import glob
+    path = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = list(csv.DictReader(open(path)))
+    ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
+    ours.sort(key=lambda r: int(r["Start_Timestamp"]))
+    starts = [i for i, r in enumerate(ours) if "user_pool" in r["Kernel_Name"]]
+    per_stage = {}
+    for a, b in zip(starts, starts[1:] + [len(ours)]):
+        di = 0
+        for r in ours[a:b]:
+            st = _stage_of(r["Kernel_Name"], di)
+            if st.startswith("dense"):
+                di += 1
+            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
+            per_stage.setdefault(st, {"us": [], "kernel": r["Kernel_Name"], "grid": r.get("Grid_Size_X", r.get("Grid_Size", "?"))})["us"].append(d)
+    lines = [f"# rocprofv3 kernel trace, per stage of one cold_score call", f"# command: {command}",
+             f"# {len(starts)} calls profiled", f"{'stage':12s} {'calls':>5s} {'mean_us':>9s} {'min_us':>9s} {'max_us':>9s}  grid  kernel"]
+    for st, v in per_stage.items():
+        us = v["us"]
+        lines.append(f"{st:12s} {len(us):5d} {np.mean(us):9.2f} {np.min(us):9.2f} {np.max(us):9.2f}  {v['grid']}  {v['kernel'][:90]}")
+    return "\n".join(lines) + "\n"
+
+
+def summarize_pmc(fetch_dir, write_dir, probe_mb, command, workload):
+    """HBM bytes per launch of each stage from FETCH_SIZE and WRITE_SIZE runs,
+    each scaled so that the plain copy probe of probe_mb MiB reads (writes)
+    exactly probe_mb MiB."""
+    import csv
+    import glob
+    res = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        copies.sort(key=lambda r: int(r["Start_Timestamp"]))
+        probe_kib = float(copies[-1]["Counter_Value"])      # the probe runs last
+        factor = probe_mb * 1024.0 / probe_kib
+        stages = {}
+        for st, r in _last_call(rows):
+            stages.setdefault(st, 0.0)
+            stages[st] += float(r["Counter_Value"]) * factor * 1024.0
+        res[counter] = {"factor": factor, "probe_raw_kib": probe_kib, "stages": stages}
+    stages = {}
+    for st in res["FETCH_SIZE"]["stages"]:
+        stages[st] = {"fetch_bytes": round(res["FETCH_SIZE"]["stages"][st]),
+                      "write_bytes": round(res["WRITE_SIZE"]["stages"].get(st, 0.0))}
+    return {"workload": workload, "command": command, "probe_mb": probe_mb,
+            "fetch_factor": res["FETCH_SIZE"]["factor"], "write_factor": res["WRITE_SIZE"]["factor"],
+            "stages": stages, "sources": _source_hashes()}
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per stage, or None when the kernel sources changed
+    since the counters were taken."""
+    path = TRAFFIC_JSON.format(workload=workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("sources") != _source_hashes():
+        return None
+    return t
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,7 +311,23 @@ def main():
                          "copy of known size, to calibrate HBM byte counters)")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the 2,000-ad latency runs (kernel-trace profiles of the step only)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--profile-command", default="", help="command recorded in summaries")
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.profile_command), end="")
+        return
+    if args.summarize_pmc:
+        t = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_probe_mb or 1024,
+                          args.profile_command, args.workload)
+        path = TRAFFIC_JSON.format(workload=args.workload)
+        with open(path, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t["stages"], indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the scoring path runs on a single MI355X "
               f"(rows are independent; see DESIGN.md for how it would shard). Got --gpus {args.gpus}.",
@@ -254,9 +387,16 @@ def main():
         stage_rows.append(e)
         log(f"  {name:12s} {ms * 1e3:9.2f} us  {e['achieved']:>9} {e['unit']}  ({100 * e['frac']:.1f}%)")
     dom = max(stage_rows, key=lambda e: e["ms"])
+    traffic = load_traffic(cfg.name)
+    dom_traffic = None
+    if traffic and dom["name"] in traffic["stages"]:
+        tb = traffic["stages"][dom["name"]]
+        dom_traffic = tb["fetch_bytes"] + tb["write_bytes"]
     roofline = {"bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
-                "unit": dom["unit"], "frac": dom["frac"], "traffic": None, "kernel": dom["name"],
-                "ms_per_launch": dom["ms"], "work_per_launch": dom["work_per_launch"]}
+                "unit": dom["unit"], "frac": dom["frac"], "traffic": dom_traffic,
+                "traffic_unit": "bytes per launch (HBM read + write)",
+                "kernel": dom["name"], "ms_per_launch": dom["ms"],
+                "work_per_launch": dom["work_per_launch"]}
     g_ms = sum(e["ms"] for e in stage_rows if e["bound"] == "hbm" and e["name"] != "head")
     g_bytes = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "hbm" and e["name"] != "head")
     m_ms = sum(e["ms"] for e in stage_rows if e["bound"] == "mfma")
@@ -309,7 +449,8 @@ def main():
         "roofline_mlp": {"bound": "mfma", "achieved": round(m_flops / (m_ms * 1e-3) / 1e12, 2),
                          "peak": PEAK_MFMA_TFLOPS[cfg.dtype], "unit": "TFLOP/s",
                          "frac": round(m_flops / (m_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS[cfg.dtype], 4)},
-        "stages": [{k: e[k] for k in ("name", "ms", "bound", "achieved", "unit", "frac")}
+        "stages": [dict({k: e[k] for k in ("name", "ms", "bound", "achieved", "unit", "frac")},
+                        traffic=(traffic["stages"].get(e["name"]) if traffic else None))
                    for e in stage_rows],
         "cpu_baseline": cpu,
     }
