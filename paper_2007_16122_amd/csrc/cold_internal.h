@@ -125,6 +125,7 @@ struct GatherArgs {
   int32_t wave_lds_bytes;         // LDS per wave (set by the launcher)
   int32_t se_lds_bytes;           // LDS for SE parameters, 0 if read from global
   int32_t se_in_lds;
+  int32_t meta_lds_bytes;         // LDS for per-group table metadata
   int64_t R, Q, n_seq_ids;
   const int32_t *req_off;         // [Q+1]
   const void *user_ids;           // [n_user][Q]
@@ -168,6 +169,7 @@ hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, 
 
 constexpr int kGatherThreads = 256;
 constexpr int kGatherMaxChunksPerRow = 1024;  // 64 lanes x 16 chunks
+constexpr int kGatherMaxIdsPerLane = 8;       // rows per wave x (ad + cross fields) <= 512
 constexpr int kMaskParts = 64;
 
 }  // namespace cold

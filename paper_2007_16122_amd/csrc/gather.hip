@@ -19,6 +19,8 @@
 //  group_mask  per-request mean importance of each group over the request's
 //              rows, then the top-k groups (Section 3.2, feature group
 //              selection); ties go to the lower group index.
+#include <type_traits>
+
 #include "cold_internal.h"
 
 namespace cold {
@@ -99,9 +101,12 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-template <typename TS, int MODE, bool LL, bool HASHED, int CPT>
+template <typename TS, int MODE, bool LL, bool HASHED, int CPT, bool SE_LDS>
 __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
   constexpr int EPC = Elem<TS>::kPerChunk;  // elements per 16-byte chunk
+  constexpr int IDMAX = kGatherMaxIdsPerLane;
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int M = a.M, d = a.d, H = a.H;
@@ -119,55 +124,105 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
     while (c >= CPR) { c -= CPR; ++t; }
   };
 
-  // SE parameters of the block in LDS (when they fit), loaded once
-  float *w1 = const_cast<float *>(a.w1), *b1 = const_cast<float *>(a.b1);
-  float *w2 = const_cast<float *>(a.w2), *b2 = const_cast<float *>(a.b2);
-  unsigned char *wbase = smem;
-  if constexpr (MODE != kApplyWeights) {
-    if (a.se_in_lds) {
-      float *sw = reinterpret_cast<float *>(smem);
+  // ---- block-wide: per-group table metadata and (when small) SE parameters in LDS
+  unsigned char *cursor = smem;
+  uint64_t *s_tab = reinterpret_cast<uint64_t *>(cursor);   // [M] table base addresses
+  uint64_t *s_magic = s_tab + M;                           // [M] Barrett constants
+  int32_t *s_rows = reinterpret_cast<int32_t *>(s_magic + M);  // [M] table rows
+  cursor += a.meta_lds_bytes;
+  for (int g = threadIdx.x; g < M; g += kGatherThreads) {
+    s_tab[g] = reinterpret_cast<uint64_t>(a.tables[g]);
+    s_magic[g] = a.table_magic[g];
+    s_rows[g] = (int32_t)a.table_rows[g];
+  }
+  const float *w1 = a.w1, *b1 = a.b1, *w2 = a.w2, *b2 = a.b2;
+  if constexpr (MODE != kApplyWeights && SE_LDS) {
+    {
+      float *sw = reinterpret_cast<float *>(cursor);
       const int nw = H * M;
       for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[i] = a.w1[i];
       for (int i = threadIdx.x; i < H; i += kGatherThreads) sw[nw + i] = a.b1[i];
       for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[nw + H + i] = a.w2[i];
       for (int i = threadIdx.x; i < M; i += kGatherThreads) sw[2 * nw + H + i] = a.b2[i];
       w1 = sw; b1 = sw + nw; w2 = sw + nw + H; b2 = sw + 2 * nw + H;
-      wbase = smem + a.se_lds_bytes;
+      cursor += a.se_lds_bytes;
     }
-    __syncthreads();  // the only block-wide barrier
   }
-  int32_t *ridx = reinterpret_cast<int32_t *>(wbase + (size_t)wave * a.wave_lds_bytes);  // [Tw][nax]
-  int32_t *rq = ridx + Tw * nax;                       // [Tw]
-  float *z = reinterpret_cast<float *>(rq + Tw);       // [Tw][M]
-  float *sv = z + Tw * M;                              // [Tw][M]
-  float *hid = sv + Tw * M;                            // [Tw][H]
+  __syncthreads();  // the only block-wide barrier
+
+  unsigned char *wb = cursor + (size_t)wave * a.wave_lds_bytes;
+  float *ust = reinterpret_cast<float *>(wb);              // [Tw][nus*d] pooled user rows
+  int32_t *ridx = reinterpret_cast<int32_t *>(ust + Tw * nus * d);  // [Tw][nax]
+  int32_t *rq = ridx + Tw * nax;                           // [Tw]
+  float *z = reinterpret_cast<float *>(rq + Tw);           // [Tw][M]
+  float *sv = z + Tw * M;                                  // [Tw][M]
+  float *hid = sv + Tw * M;                                // [Tw][H]
 
   const int64_t r0 = ((int64_t)blockIdx.x * (kGatherThreads / 64) + wave) * Tw;
   if (r0 >= R) return;
 
-  // ---- request of each row; ad/cross ids -> table rows (field by field)
+  // ---- request of each row
   for (int t = lane; t < Tw; t += 64) {
     const int64_t r = r0 + t;
     rq[t] = r < R ? (int32_t)request_of_row(a.req_off, Q, r) : 0;
   }
-  for (int i = lane; i < Tw * nax; i += 64) {
-    const int f = i / Tw, t = i - f * Tw;
-    const int64_t r = r0 + t;
-    const int g = nus + f;
-    int32_t row = -1;
-    if (r < R) {
-      const bool is_ad = f < a.n_ad;
-      const void *ids = is_ad ? a.ad_ids : a.cross_ids;
-      const int64_t idx = (int64_t)(is_ad ? f : f - a.n_ad) * R + r;
-      bool keep = true;
-      if constexpr (MODE == kApplyWeights) {  // masked-out groups are never read
-        const int64_t q = request_of_row(a.req_off, Q, r);
-        keep = a.mask[q * M + g] != 0;
+  // ---- ad/cross ids (all loads issued before any is used), then table rows
+  typedef typename std::conditional<HASHED, uint64_t, int32_t>::type id_t;
+  id_t idv[IDMAX];
+#pragma unroll
+  for (int k = 0; k < IDMAX; ++k) {
+    const int i = lane + 64 * k;
+    idv[k] = 0;
+    if (i < Tw * nax) {
+      const int f = i / Tw, t = i - f * Tw;
+      const int64_t r = r0 + t;
+      if (r < R) {
+        const bool is_ad = f < a.n_ad;
+        const id_t *ids = static_cast<const id_t *>(is_ad ? a.ad_ids : a.cross_ids);
+        idv[k] = ids[(int64_t)(is_ad ? f : f - a.n_ad) * R + r];
       }
-      if (keep) row = resolve_row<HASHED>(ids, idx, g, a.table_rows[g], a.table_magic[g], a.err);
-      if (MODE != kApplyWeights && a.rows_out) a.rows_out[(int64_t)g * R + r] = row;
     }
-    ridx[t * nax + f] = row;
+  }
+  wave_sync();  // rq visible
+#pragma unroll
+  for (int k = 0; k < IDMAX; ++k) {
+    const int i = lane + 64 * k;
+    if (i < Tw * nax) {
+      const int f = i / Tw, t = i - f * Tw;
+      const int64_t r = r0 + t;
+      const int g = nus + f;
+      int32_t row = -1;
+      if (r < R) {
+        bool keep = true;
+        if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
+        if constexpr (HASHED) {
+          const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+          row = (int32_t)mod_barrett(mix64((uint64_t)idv[k] ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+        } else {
+          row = (int32_t)idv[k];
+          if (row < 0 || row >= s_rows[g]) {
+            atomicOr(a.err, 1);
+            row = -1;
+          }
+        }
+        if (!keep) row = -1;
+        if (MODE != kApplyWeights && a.rows_out) a.rows_out[(int64_t)g * R + r] = row;
+      }
+      ridx[t * nax + f] = row;
+    }
+  }
+  // ---- pooled user rows of the wave's rows into LDS (independent loads)
+  const int ud4 = nus * d / 4;
+  for (int i = lane; i < Tw * ud4; i += 64) {
+    const int t = i / ud4, k4 = i - t * ud4;
+    reinterpret_cast<float4 *>(ust)[i] =
+        reinterpret_cast<const float4 *>(a.U + (int64_t)rq[t] * nus * d)[k4];
+  }
+  if constexpr (MODE != kApplyWeights) {
+    for (int i = lane; i < Tw * nus; i += 64) {
+      const int t = i / nus, g = i - t * nus;
+      z[t * M + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
+    }
   }
   wave_sync();
   if (MODE != kApplyWeights && a.rows_out) {
@@ -190,8 +245,10 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       if (t < Tw && r0 + t < R && g >= nus) {
         const int32_t row = ridx[t * nax + (g - nus)];
         if (row >= 0) {
-          const TS *tab = static_cast<const TS *>(a.tables[g]);
-          raw[j] = *reinterpret_cast<const uint4 *>(tab + (int64_t)row * d + p * EPC);
+          gl_u32x4 *src = reinterpret_cast<gl_u32x4 *>(
+              s_tab[g] + ((uint64_t)row * d + p * EPC) * sizeof(TS));
+          const u32x4 w = *src;
+          raw[j] = make_uint4(w.x, w.y, w.z, w.w);
         }
       }
       advance(t, c);
@@ -208,29 +265,27 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
 #pragma unroll
       for (int e = 0; e < EPC; ++e) part += v[e];
       for (int o = 1; o < CPG; o <<= 1) part += __shfl_xor(part, o);
-      if (t < Tw && p == 0) {
-        float zz = 0.0f;
-        if (r0 + t < R) zz = g < nus ? a.zU[(int64_t)rq[t] * nus + g] : part / (float)d;
-        z[t * M + g] = zz;
-      }
+      if (t < Tw && p == 0 && g >= nus) z[t * M + g] = r0 + t < R ? part / (float)d : 0.0f;
     }
     wave_sync();
 
     // ---- SE block of the wave's rows (Eq. 2)
     for (int it = lane; it < Tw * H; it += 64) {
       const int t = it / H, jh = it - t * H;
-      float acc = b1[jh];
       const float *w = w1 + jh * M;
       const float *zt = z + t * M;
+      float acc = b1[jh];
+#pragma unroll 8
       for (int g = 0; g < M; ++g) acc += w[g] * zt[g];
       hid[it] = acc > 0.0f ? acc : 0.0f;
     }
     wave_sync();
     for (int it = lane; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
-      float acc = b2[g];
       const float *w = w2 + g * H;
       const float *ht = hid + t * H;
+      float acc = b2[g];
+#pragma unroll 8
       for (int jh = 0; jh < H; ++jh) acc += w[jh] * ht[jh];
       const float sg = 1.0f / (1.0f + expf(-acc));
       sv[it] = sg;
@@ -258,13 +313,9 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       const float sg = sv[t * M + g];
       float v[EPC];
       if (g < nus) {
-        const float4 *src = reinterpret_cast<const float4 *>(
-            a.U + ((int64_t)rq[t] * nus + g) * d + p * EPC);
+        const float *src = ust + t * nus * d + g * d + p * EPC;
 #pragma unroll
-        for (int e4 = 0; e4 < EPC / 4; ++e4) {
-          const float4 w = src[e4];
-          v[4 * e4] = w.x; v[4 * e4 + 1] = w.y; v[4 * e4 + 2] = w.z; v[4 * e4 + 3] = w.w;
-        }
+        for (int e = 0; e < EPC; ++e) v[e] = src[e];
       } else {
         Elem<TS>::unpack(raw[j], v);
       }
@@ -343,6 +394,18 @@ hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStre
   }
 }
 
+template <typename TS, int MODE, bool LL, int CPT, bool SE_LDS>
+static hipError_t gather_se_l(bool hashed, const GatherArgs &a, const dim3 &grid, size_t shmem,
+                              hipStream_t s) {
+  if (hashed)
+    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, true, CPT, SE_LDS>), grid, dim3(kGatherThreads),
+                       shmem, s, a);
+  else
+    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, false, CPT, SE_LDS>), grid, dim3(kGatherThreads),
+                       shmem, s, a);
+  return hipGetLastError();
+}
+
 template <typename TS, int MODE, bool LL, int CPT>
 static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   constexpr int EPC = Elem<TS>::kPerChunk;
@@ -350,19 +413,20 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   const int cpr = a.M * (a.d / EPC);
   const int T = (64 * CPT) / cpr;  // rows per wave
   a.rows_per_tile = T;
-  a.wave_lds_bytes = (int32_t)((sizeof(int32_t) * (size_t)(T * nax + T) +
+  const int nus = a.n_user + a.n_seq;
+  a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * nus * a.d +
+                                sizeof(int32_t) * (size_t)(T * nax + T) +
                                 sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
+  a.meta_lds_bytes = (int32_t)((20 * (size_t)a.M + 15) / 16 * 16);
   const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
   a.se_in_lds = MODE != kApplyWeights && se_floats * sizeof(float) <= 24 * 1024;
   a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
-  const size_t shmem = (size_t)a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
+  const size_t shmem = (size_t)a.meta_lds_bytes + a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
+  if (T * nax > 64 * kGatherMaxIdsPerLane || shmem > 160 * 1024) return hipErrorInvalidValue;
   const int64_t rows_per_block = 4 * (int64_t)T;
   const dim3 grid((unsigned)((a.R + rows_per_block - 1) / rows_per_block));
-  if (hashed)
-    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, true, CPT>), grid, dim3(kGatherThreads), shmem, s, a);
-  else
-    hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, false, CPT>), grid, dim3(kGatherThreads), shmem, s, a);
-  return hipGetLastError();
+  if (a.se_in_lds) return gather_se_l<TS, MODE, LL, CPT, true>(hashed, a, grid, shmem, s);
+  return gather_se_l<TS, MODE, LL, CPT, false>(hashed, a, grid, shmem, s);
 }
 
 // chunks per lane: 16 when a row has more than 64 chunks (so a wave holds
