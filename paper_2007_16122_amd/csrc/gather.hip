@@ -411,7 +411,11 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   constexpr int EPC = Elem<TS>::kPerChunk;
   const int nax = a.n_ad + a.n_cross;
   const int cpr = a.M * (a.d / EPC);
-  const int T = (64 * CPT) / cpr;  // rows per wave
+  // rows per wave: as many as the chunk budget allows, fewer for small
+  // batches so that at least ~1024 waves are launched
+  const int t_max = (64 * CPT) / cpr;
+  const int64_t t_fill = (a.R + 1023) / 1024;
+  const int T = t_fill < t_max ? (t_fill < 1 ? 1 : (int)t_fill) : t_max;
   a.rows_per_tile = T;
   const int nus = a.n_user + a.n_seq;
   a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * nus * a.d +
@@ -429,8 +433,8 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   return gather_se_l<TS, MODE, LL, CPT, false>(hashed, a, grid, shmem, s);
 }
 
-// chunks per lane: 16 when a row has more than 64 chunks (so a wave holds
-// several rows), else 8
+// chunks per lane: 8 (a wave holds 512 / chunks-per-row rows); 16 only when a
+// row has more than 512 chunks
 template <typename TS, int MODE, bool LL>
 static hipError_t gather_se_t(bool hashed, const GatherArgs &a, hipStream_t s) {
   const int cpr = a.M * (a.d / Elem<TS>::kPerChunk);

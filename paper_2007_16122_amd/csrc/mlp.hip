@@ -699,6 +699,10 @@ template <typename TS>
 static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, void *y, int64_t R,
                                 int N, int K, hipStream_t s) {
   if (K % kBK == 0 && N % 8 == 0) {
+    // large batches: 256-row tiles; small ones (a single request of a few
+    // thousand ads) would leave most CUs idle, so use 64 x 64 tiles
+    const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
+    if (big_tiles < 256) return dense_pipe_t<TS, 64, 64, 3>(x, w, b, y, R, N, K, s);
     if (N % 128 == 0) return dense_pipe_t<TS, 256, 128, 3>(x, w, b, y, R, N, K, s);
     return dense_pipe_t<TS, 256, 64, 3>(x, w, b, y, R, N, K, s);
   }
