@@ -403,11 +403,20 @@ def main():
     m_flops = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "mfma")
 
     p50 = p99 = g50 = g99 = None
+    lat_stages = None
     if not args.no_latency:
         lat_np = request_slice(batch, 0, cfg)
         lat_dev = binding.batch_to_device(lat_np, dev)
         lat_scores = torch.empty(lat_np["n_rows"], dtype=torch.float32, device=dev)
         p50, p99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=False)
+        binding.cold_profile_enable(model.h, True)
+        for _ in range(20):
+            model.score(lat_dev, scores=lat_scores)
+        torch.cuda.synchronize()
+        lst, lcalls = binding.cold_profile_read(model.h)
+        binding.cold_profile_enable(model.h, False)
+        lat_stages = {name: round(tot / max(lcalls, 1) * 1e3, 2) for name, tot in lst}
+        log(f"2,000-ad request stages (us): {lat_stages}")
         try:
             g50, g99 = latency(model, lat_dev, lat_scores, args.latency_iters, torch, graph=True)
         except Exception as exc:  # graph capture is an optional measurement
@@ -441,6 +450,7 @@ def main():
         "p50_latency_ms": None if p50 is None else round(p50, 4),
         "p99_latency_ms": None if p99 is None else round(p99, 4),
         "p50_latency_graph_ms": None if g50 is None else round(g50, 4),
+        "latency_stages_us": lat_stages,
         "p99_latency_graph_ms": None if g99 is None else round(g99, 4),
         "roofline": roofline,
         "roofline_gather_se": {"bound": "hbm", "achieved": round(g_bytes / (g_ms * 1e-3) / 1e9, 1),

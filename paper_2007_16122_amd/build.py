@@ -24,21 +24,43 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def _filtered(res) -> str:
+    return "\n".join(l for l in (res.stdout + res.stderr).splitlines()
+                     if "packed-fp32-ops" not in l)
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source into ``libcold.so`` (always recompiles)."""
+    """Compile every HIP source into ``libcold.so`` (always recompiles; the
+    sources compile in parallel, then one link)."""
+    import tempfile
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           *sources(), "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    out = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
-                    if "packed-fp32-ops" not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
-    if out.strip() and verbose:
-        print(out, file=sys.stderr)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    with tempfile.TemporaryDirectory(prefix="cold_build_") as tmpdir:
+        procs = []
+        for src in sources():
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            cmd = [hipcc, *compile_flags, *inc, "-c", src, "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            procs.append((src, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE,
+                                                     stderr=subprocess.PIPE, text=True)))
+        objs = []
+        for src, obj, p in procs:
+            out, err = p.communicate()
+            res = subprocess.CompletedProcess(p.args, p.returncode, out, err)
+            if p.returncode != 0:
+                raise RuntimeError(f"hipcc failed on {src} ({p.returncode}):\n{_filtered(res)}")
+            if verbose and _filtered(res).strip():
+                print(_filtered(res), file=sys.stderr)
+            objs.append(obj)
+        tmp = LIB + ".tmp"
+        cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"hipcc link failed ({res.returncode}):\n{_filtered(res)}")
     os.replace(tmp, LIB)
     return LIB
 

@@ -1,23 +1,22 @@
 // mlp.hip -- the fully connected network of the COLD model (Section 4.1:
 // D_in x 1024 x 512 x 256 x 128 x 64 x 2) on gfx950.
 //
-//  dense_relu_mfma  Y = ReLU(X W^T + b) for bf16/fp16 X, W with fp32
+//  dense_relu_pipe  Y = ReLU(X W^T + b) for bf16/fp16 X, W with fp32
 //                   accumulation on the matrix cores
-//                   (v_mfma_f32_16x16x32_{bf16,f16}), one rounding of the
-//                   output to the storage type.  256 threads = 4 waves per
-//                   128-row tile; W plays the MFMA A operand (output features
-//                   on the rows) and X the B operand, so each lane ends with
-//                   4 consecutive output features of one row (one 8-byte
-//                   store).  Tiles of both operands go through LDS, double
-//                   buffered, one barrier per 32-deep K step; rows are
-//                   padded by 16 bytes so the 16-byte fragment reads of a
-//                   wave hit distinct LDS banks.  Tiles are numbered so that
-//                   the workgroups sharing one row block of X run on the same
-//                   XCD (workgroup i is dispatched to XCD i mod 8) and reuse
-//                   it from that XCD's L2.
+//                   (v_mfma_f32_16x16x32_{bf16,f16}) and one rounding of the
+//                   output to the storage type.  Operand tiles stream from
+//                   global memory straight into an LDS ring (no VGPR staging);
+//                   W plays the MFMA A operand (output features on the rows),
+//                   X the B operand.  Tiles are numbered so that the
+//                   workgroups sharing one row block of X run on the same XCD
+//                   (workgroup i is dispatched to XCD i mod 8) and reuse it
+//                   from that XCD's L2.  256 x 128 tiles for large batches,
+//                   64 x 64 for a single request.
+//  dense_relu_mfma  the same layer with register-staged, double-buffered LDS
+//                   tiles; used when K is not a multiple of 32.
 //  mlp_tail         the last two hidden layers and the head fused over
 //                   64-row tiles held in LDS.
-//  dense_relu_f32   the same layer in fp32 FMA (the fp32 model).
+//  dense_relu_f32   the layer in fp32 FMA (the fp32 model).
 //  head             last layer (n_out = 1 or 2) in fp32 plus sigmoid or
 //                   two-way softmax; writes the CTR.
 #include <type_traits>
@@ -41,19 +40,6 @@ template <> struct Mfma<_Float16> {
   typedef f16x8 frag;
   __device__ static inline f32x4 mac(const frag &a, const frag &b, const f32x4 &c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-  }
-};
-
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
-template <typename TS> struct Mfma32;
-template <> struct Mfma32<__bf16> {
-  __device__ static inline f32x16 mac(const bf16x8 &a, const bf16x8 &b, const f32x16 &c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-  }
-};
-template <> struct Mfma32<_Float16> {
-  __device__ static inline f32x16 mac(const f16x8 &a, const f16x8 &b, const f32x16 &c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
 };
 
@@ -334,156 +320,6 @@ __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__
   __syncthreads();
   constexpr int CPRW = BN / 8;  // 16-byte chunks per output row
   for (int idx = tid; idx < BR * CPRW; idx += 256) {
-    const int rl = idx / CPRW, c = idx - rl * CPRW;
-    const int64_t r = r0 + rl;
-    const int n = n0 + c * 8;
-    if (r < R && n < N)
-      *reinterpret_cast<uint4 *>(Y + r * N + n) =
-          *reinterpret_cast<const uint4 *>(sout + rl * OUT_STRIDE + c * 8);
-  }
-}
-
-// The pipelined layer on v_mfma_f32_32x32x16 (in a register-only loop on
-// gfx950 this form sustains about 1.6x the rate of 16x16x32): WGR x WGN waves
-// per block (64 * WGR * WGN threads), block tile BR x BN, wave tile
-// (BR/WGR) x (BN/WGN) in 32 x 32 blocks.  Fragment of a 32-row block, half h
-// of a 32-deep K step: lane l reads row l % 32, chunk 2h + l / 32.
-// Accumulator element e of lane l holds D[8 (e / 4) + 4 (l / 32) + e % 4][l % 32].
-template <typename TS, int BR, int BN, int WGR, int WGN, int S, int MINW>
-__global__ __launch_bounds__(64 * WGR * WGN, MINW) void dense_relu_wg_kernel(
-    const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias,
-    TS *__restrict__ Y, int64_t R, int N, int K, int tiles_n, int tiles_total) {
-  typedef typename Mfma<TS>::frag frag;
-  typedef __attribute__((address_space(3))) void lds_void;
-  constexpr int NT = 64 * WGR * WGN, NW = WGR * WGN;
-  constexpr int WTR = BR / WGR, WTN = BN / WGN;        // wave tile
-  constexpr int NI = WTN / 32, RJ = WTR / 32;          // 32x32 blocks per wave
-  constexpr int ROWB = kBK * 2;
-  constexpr int STAGE = (BN + BR) * ROWB;
-  constexpr int LOADS = (BN + BR) / 16 / NW;           // 16-row loads per wave per stage
-  constexpr int OUT_STRIDE = BN + 8;
-  constexpr int OUT_BYTES = BR * OUT_STRIDE * 2;
-  constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
-  static_assert((BN + BR) % (16 * NW) == 0 && NI >= 1 && RJ >= 1, "tile shape");
-  static_assert(S >= 2 && S <= 4, "stages");
-  __shared__ __align__(16) unsigned char smem[SMEM];
-
-  const int tile = xcd_tile(blockIdx.x, tiles_total);
-  const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
-  const int64_t r0 = (int64_t)tr * BR;
-  const int n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave % WGN, wr = wave / WGN;
-
-  const TS *src[LOADS];
-  int dst_off[LOADS];
-#pragma unroll
-  for (int u = 0; u < LOADS; ++u) {
-    const int ins = wave * LOADS + u;
-    const int row16 = lane >> 2, slot = lane & 3;
-    const int chunk = slot ^ lds_swz(row16);
-    if (ins < BN / 16) {
-      int n = n0 + ins * 16 + row16;
-      n = n < N ? n : N - 1;
-      src[u] = W + (int64_t)n * K + chunk * 8;
-      dst_off[u] = ins * 16 * ROWB;
-    } else {
-      int64_t r = r0 + (ins - BN / 16) * 16 + row16;
-      r = r < R ? r : R - 1;
-      src[u] = X + r * K + chunk * 8;
-      dst_off[u] = BN * ROWB + (ins - BN / 16) * 16 * ROWB;
-    }
-  }
-  auto issue = [&](int ks, int stage) {
-#pragma unroll
-    for (int u = 0; u < LOADS; ++u)
-      __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[u] + ks * kBK),
-                                       (lds_void *)(smem + stage * STAGE + dst_off[u]), 16, 0, 0);
-  };
-
-  f32x16 acc[NI][RJ];
-#pragma unroll
-  for (int i = 0; i < NI; ++i)
-#pragma unroll
-    for (int j = 0; j < RJ; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-  const int ksteps = K / kBK;
-#pragma unroll
-  for (int st = 0; st < S - 1; ++st)
-    if (st < ksteps) issue(st, st);
-
-  const int frow = lane & 31, fh = lane >> 5;
-  const int a_row = (wn * WTN + frow) * ROWB;
-  const int b_row = BN * ROWB + (wr * WTR + frow) * ROWB;
-  const int swz = lds_swz(frow & 15);
-  int stage = 0;
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int later = ksteps - 1 - ks;
-    if (S >= 4 && later >= 2) wait_vm<2 * LOADS>();
-    else if (S >= 3 && later >= 1) wait_vm<LOADS>();
-    else wait_vm<0>();
-    compiler_fence();
-    __builtin_amdgcn_s_barrier();
-    compiler_fence();
-    if (ks + S - 1 < ksteps) {
-      int st = stage + S - 1;
-      st = st >= S ? st - S : st;
-      issue(ks + S - 1, st);
-    }
-    const unsigned char *base = smem + stage * STAGE;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int coff = (((2 * h + fh) ^ swz) * 16);
-      frag fa[NI];
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-        fa[i] = *reinterpret_cast<const frag *>(base + a_row + i * 32 * ROWB + coff);
-#pragma unroll
-      for (int j = 0; j < RJ; ++j) {
-        const frag fb = *reinterpret_cast<const frag *>(base + b_row + j * 32 * ROWB + coff);
-#pragma unroll
-        for (int i = 0; i < NI; ++i) acc[i][j] = Mfma32<TS>::mac(fa[i], fb, acc[i][j]);
-      }
-    }
-    stage = stage + 1 == S ? 0 : stage + 1;
-  }
-
-  wait_vm<0>();
-  compiler_fence();
-  __builtin_amdgcn_s_barrier();
-  compiler_fence();
-  uint16_t *sout = reinterpret_cast<uint16_t *>(smem);
-  const int dr = lane & 31, dq = (lane >> 5) * 4;
-#pragma unroll
-  for (int i = 0; i < NI; ++i) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int nl = wn * WTN + i * 32 + 8 * g + dq;
-      float bv[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) bv[e] = (n0 + nl + e < N) ? bias[n0 + nl + e] : 0.0f;
-#pragma unroll
-      for (int j = 0; j < RJ; ++j) {
-        const int rl = wr * WTR + j * 32 + dr;
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float t = acc[i][j][4 * g + e] + bv[e];
-          o[e] = t > 0.0f ? t : 0.0f;
-        }
-        uint2 packed;
-        packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
-        packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
-        *reinterpret_cast<uint2 *>(sout + rl * OUT_STRIDE + nl) = packed;
-      }
-    }
-  }
-  compiler_fence();
-  __syncthreads();
-  constexpr int CPRW = BN / 8;
-  for (int idx = tid; idx < BR * CPRW; idx += NT) {
     const int rl = idx / CPRW, c = idx - rl * CPRW;
     const int64_t r = r0 + rl;
     const int n = n0 + c * 8;
