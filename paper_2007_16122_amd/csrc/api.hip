@@ -25,7 +25,7 @@ struct ArenaLayout {
 };
 
 struct WorkLayout {
-  size_t err, U, zU, urow, X, actA, actB, sbuf, partial, mask, total;
+  size_t err, U, zU, Uh, urow, X, actA, actB, sbuf, partial, mask, total;
 };
 
 }  // namespace
@@ -101,6 +101,7 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   w.err = take(sizeof(int32_t));
   w.U = take(sizeof(float) * (size_t)Q * m.nus * m.d);
   w.zU = take(sizeof(float) * (size_t)Q * m.nus);
+  w.Uh = take((size_t)m.es * Q * m.desc.n_user * m.d);
   w.urow = take(sizeof(int32_t) * (size_t)Q * (m.desc.n_user > 0 ? m.desc.n_user : 1));
   w.X = take((size_t)m.es * R * m.D_in);
   w.actA = take((size_t)m.es * R * m.max_hidden);
@@ -370,6 +371,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   g.b2 = reinterpret_cast<const float *>(A + al.b2);
   g.U = reinterpret_cast<float *>(W + wl.U);
   g.zU = reinterpret_cast<float *>(W + wl.zU);
+  g.Uh = W + wl.Uh;
   g.urow = reinterpret_cast<int32_t *>(W + wl.urow);
   g.X = W + wl.X;
   g.rows_out = rows_out;

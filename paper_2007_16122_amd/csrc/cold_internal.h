@@ -139,6 +139,7 @@ struct GatherArgs {
   const float *w1, *b1, *w2, *b2; // SE parameters
   float *U;                       // [Q][n_user+n_seq][d] pooled user side
   float *zU;                      // [Q][n_user+n_seq] squeeze of the user groups
+  void *Uh;                       // [Q][n_user][d] single-valued user rows, storage type
   int32_t *urow;                  // [Q][max(n_user,1)] resolved user rows
   void *X;                        // [R][M*d] network input
   float *s_buf;                   // [R][M] SE weights (written, or read in apply mode)

@@ -19,7 +19,9 @@
 //  group_mask  per-request mean importance of each group over the request's
 //              rows, then the top-k groups (Section 3.2, feature group
 //              selection); ties go to the lower group index.
+#include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "cold_internal.h"
 
@@ -64,7 +66,9 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
     const int32_t row = resolve_row<HASHED>(a.user_ids, (int64_t)f * Q + q, f, a.table_rows[f],
                                             a.table_magic[f], a.err);
     const TS *tab = static_cast<const TS *>(a.tables[f]);
-    a.U[(q * nus + f) * d + k] = row >= 0 ? Elem<TS>::to_f32(tab[(int64_t)row * d + k]) : 0.0f;
+    const TS v = row >= 0 ? tab[(int64_t)row * d + k] : Elem<TS>::from_f32(0.0f);
+    a.U[(q * nus + f) * d + k] = Elem<TS>::to_f32(v);
+    static_cast<TS *>(a.Uh)[(q * nu + f) * d + k] = v;   // exact copy in the storage type
     if (k == 0) a.urow[q * nu + f] = row;
   }
   for (int it = threadIdx.x; it < ns * d; it += blockDim.x) {
@@ -102,7 +106,7 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 template <typename TS, int MODE, bool LL, bool HASHED, int CPT, bool SE_LDS>
-__global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a) {
+__global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_kernel(GatherArgs a) {
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
   constexpr int EPC = Elem<TS>::kPerChunk;  // elements per 16-byte chunk
@@ -151,18 +155,28 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
   __syncthreads();  // the only block-wide barrier
 
   unsigned char *wb = cursor + (size_t)wave * a.wave_lds_bytes;
-  float *ust = reinterpret_cast<float *>(wb);              // [Tw][nus*d] pooled user rows
-  int32_t *ridx = reinterpret_cast<int32_t *>(ust + Tw * nus * d);  // [Tw][nax]
+  const int ns = a.n_seq, nu = a.n_user;
+  float *ust = reinterpret_cast<float *>(wb);              // [Tw][ns*d] pooled sequence rows
+  int32_t *ridx = reinterpret_cast<int32_t *>(ust + Tw * ns * d);  // [Tw][nax]
   int32_t *rq = ridx + Tw * nax;                           // [Tw]
   float *z = reinterpret_cast<float *>(rq + Tw);           // [Tw][M]
   float *sv = z + Tw * M;                                  // [Tw][M]
   float *hid = sv + Tw * M;                                // [Tw][H]
+  const TS *Uh = static_cast<const TS *>(a.Uh);
 
-  const int64_t r0 = ((int64_t)blockIdx.x * (kGatherThreads / 64) + wave) * Tw;
-  if (r0 >= R) return;
+  // persistent: each wave walks the row tiles wave_id, wave_id + waves, ...
+  const int64_t n_tiles = (R + Tw - 1) / Tw;
+  const int64_t stride = (int64_t)gridDim.x * (kGatherThreads / 64);
+  for (int64_t wt = (int64_t)blockIdx.x * (kGatherThreads / 64) + wave; wt < n_tiles; wt += stride) {
+  const int64_t r0 = wt * Tw;
+  wave_sync();  // the previous tile's LDS reads are done
+  // chunk coordinates, opaque to the compiler so that nothing derived from
+  // them is hoisted out of the tile loop (which would pin registers)
+  int tf = t_first, cf = c_first, ln = lane;
+  asm volatile("" : "+v"(tf), "+v"(cf), "+v"(ln));
 
   // ---- request of each row
-  for (int t = lane; t < Tw; t += 64) {
+  for (int t = ln; t < Tw; t += 64) {
     const int64_t r = r0 + t;
     rq[t] = r < R ? (int32_t)request_of_row(a.req_off, Q, r) : 0;
   }
@@ -171,7 +185,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
   id_t idv[IDMAX];
 #pragma unroll
   for (int k = 0; k < IDMAX; ++k) {
-    const int i = lane + 64 * k;
+    const int i = ln + 64 * k;
     idv[k] = 0;
     if (i < Tw * nax) {
       const int f = i / Tw, t = i - f * Tw;
@@ -186,7 +200,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
   wave_sync();  // rq visible
 #pragma unroll
   for (int k = 0; k < IDMAX; ++k) {
-    const int i = lane + 64 * k;
+    const int i = ln + 64 * k;
     if (i < Tw * nax) {
       const int f = i / Tw, t = i - f * Tw;
       const int64_t r = r0 + t;
@@ -211,43 +225,50 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       ridx[t * nax + f] = row;
     }
   }
-  // ---- pooled user rows of the wave's rows into LDS (independent loads)
-  const int ud4 = nus * d / 4;
-  for (int i = lane; i < Tw * ud4; i += 64) {
-    const int t = i / ud4, k4 = i - t * ud4;
+  // ---- pooled sequence rows of the wave's rows into LDS (fp32: sums can
+  //      exceed the storage range), squeeze of the user groups
+  const int sd4 = ns * d / 4;
+  for (int i = ln; i < Tw * sd4; i += 64) {
+    const int t = i / sd4, k4 = i - t * sd4;
     reinterpret_cast<float4 *>(ust)[i] =
-        reinterpret_cast<const float4 *>(a.U + (int64_t)rq[t] * nus * d)[k4];
+        reinterpret_cast<const float4 *>(a.U + ((int64_t)rq[t] * nus + nu) * d)[k4];
   }
   if constexpr (MODE != kApplyWeights) {
-    for (int i = lane; i < Tw * nus; i += 64) {
+    for (int i = ln; i < Tw * nus; i += 64) {
       const int t = i / nus, g = i - t * nus;
       z[t * M + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
     }
   }
   wave_sync();
   if (MODE != kApplyWeights && a.rows_out) {
-    for (int i = lane; i < Tw * nus; i += 64) {
+    for (int i = ln; i < Tw * nus; i += 64) {
       const int f = i / Tw, t = i - f * Tw;
       const int64_t r = r0 + t;
-      if (r < R)
-        a.rows_out[(int64_t)f * R + r] = f < a.n_user ? a.urow[(int64_t)rq[t] * a.n_user + f] : -1;
+      if (r < R) a.rows_out[(int64_t)f * R + r] = f < nu ? a.urow[(int64_t)rq[t] * nu + f] : -1;
     }
   }
 
-  // ---- gather every table chunk first (all loads in flight), then squeeze
+  // ---- gather every chunk first (all loads in flight): table rows, and the
+  //      request's single-valued user rows (storage type), then squeeze
   uint4 raw[CPT];
   {
-    int t = t_first, c = c_first;
+    int t = tf, c = cf;
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
       const int g = c >> lcpg, p = c & (CPG - 1);
       raw[j] = make_uint4(0, 0, 0, 0);
-      if (t < Tw && r0 + t < R && g >= nus) {
-        const int32_t row = ridx[t * nax + (g - nus)];
-        if (row >= 0) {
-          gl_u32x4 *src = reinterpret_cast<gl_u32x4 *>(
-              s_tab[g] + ((uint64_t)row * d + p * EPC) * sizeof(TS));
-          const u32x4 w = *src;
+      if (t < Tw && r0 + t < R && (g < nu || g >= nus)) {
+        uint64_t addr = 0;
+        if (g < nu) {
+          bool keep = true;
+          if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
+          if (keep) addr = reinterpret_cast<uint64_t>(Uh + ((int64_t)rq[t] * nu + g) * d + p * EPC);
+        } else {
+          const int32_t row = ridx[t * nax + (g - nus)];
+          if (row >= 0) addr = s_tab[g] + ((uint64_t)row * d + p * EPC) * sizeof(TS);
+        }
+        if (addr) {
+          const u32x4 w = *reinterpret_cast<gl_u32x4 *>(addr);
           raw[j] = make_uint4(w.x, w.y, w.z, w.w);
         }
       }
@@ -255,7 +276,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
     }
   }
   if constexpr (MODE != kApplyWeights) {
-    int t = t_first, c = c_first;
+    int t = tf, c = cf;
 #pragma unroll
     for (int j = 0; j < CPT; ++j, advance(t, c)) {
       const int g = c >> lcpg, p = c & (CPG - 1);
@@ -270,7 +291,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
     wave_sync();
 
     // ---- SE block of the wave's rows (Eq. 2)
-    for (int it = lane; it < Tw * H; it += 64) {
+    for (int it = ln; it < Tw * H; it += 64) {
       const int t = it / H, jh = it - t * H;
       const float *w = w1 + jh * M;
       const float *zt = z + t * M;
@@ -280,7 +301,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       hid[it] = acc > 0.0f ? acc : 0.0f;
     }
     wave_sync();
-    for (int it = lane; it < Tw * M; it += 64) {
+    for (int it = ln; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
       const float *w = w2 + g * H;
       const float *ht = hid + t * H;
@@ -292,28 +313,28 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       if (a.s_buf && r0 + t < R) a.s_buf[r0 * M + it] = sg;
     }
   } else {
-    for (int it = lane; it < Tw * M; it += 64) {
+    for (int it = ln; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
       float sg = 0.0f;
       if (r0 + t < R && a.mask[(int64_t)rq[t] * M + g]) sg = a.s_buf[r0 * M + it];
       sv[it] = sg;
     }
   }
-  if constexpr (MODE == kWeightsOnly) return;
+  if constexpr (MODE != kWeightsOnly) {
   wave_sync();
 
   // ---- reweight, linear_log, round once, coalesced store
   TS *X = static_cast<TS *>(a.X);
-  int t = t_first, c = c_first;
+  int t = tf, c = cf;
 #pragma unroll
   for (int j = 0; j < CPT; ++j, advance(t, c)) {
-    const int i = lane + 64 * j;
+    const int i = ln + 64 * j;
     const int g = c >> lcpg, p = c & (CPG - 1);
     if (t < Tw && r0 + t < R) {
       const float sg = sv[t * M + g];
       float v[EPC];
-      if (g < nus) {
-        const float *src = ust + t * nus * d + g * d + p * EPC;
+      if (g >= nu && g < nus) {
+        const float *src = ust + t * ns * d + (g - nu) * d + p * EPC;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) v[e] = src[e];
       } else {
@@ -328,6 +349,8 @@ __global__ __launch_bounds__(kGatherThreads) void gather_se_kernel(GatherArgs a)
       *reinterpret_cast<uint4 *>(X + (r0 * CPR + i) * EPC) = Elem<TS>::pack(o);
     }
   }
+  }
+  }  // tile loop
 }
 
 // ------------------------------------------------------------- group_mask
@@ -394,9 +417,35 @@ hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStre
   }
 }
 
+// Resident workgroups of a kernel on the current device (cached): the
+// persistent gather launches no more than fit at once.
+static int resident_blocks(const void *kernel, size_t shmem) {
+  struct Entry { const void *k; size_t sh; int dev; int blocks; };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const Entry &e : cache)
+    if (e.k == kernel && e.sh == shmem && e.dev == dev) return e.blocks;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kGatherThreads, shmem) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  const int blocks = per_cu * cus;
+  cache.push_back({kernel, shmem, dev, blocks});
+  return blocks;
+}
+
 template <typename TS, int MODE, bool LL, int CPT, bool SE_LDS>
-static hipError_t gather_se_l(bool hashed, const GatherArgs &a, const dim3 &grid, size_t shmem,
+static hipError_t gather_se_l(bool hashed, const GatherArgs &a, int64_t blocks_needed, size_t shmem,
                               hipStream_t s) {
+  const void *k = hashed ? reinterpret_cast<const void *>(&gather_se_kernel<TS, MODE, LL, true, CPT, SE_LDS>)
+                         : reinterpret_cast<const void *>(&gather_se_kernel<TS, MODE, LL, false, CPT, SE_LDS>);
+  const int resident = resident_blocks(k, shmem);
+  int64_t nb = blocks_needed;
+  if (resident > 0 && nb > resident) nb = resident;
+  const dim3 grid((unsigned)nb);
   if (hashed)
     hipLaunchKernelGGL((gather_se_kernel<TS, MODE, LL, true, CPT, SE_LDS>), grid, dim3(kGatherThreads),
                        shmem, s, a);
@@ -417,8 +466,7 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   const int64_t t_fill = (a.R + 1023) / 1024;
   const int T = t_fill < t_max ? (t_fill < 1 ? 1 : (int)t_fill) : t_max;
   a.rows_per_tile = T;
-  const int nus = a.n_user + a.n_seq;
-  a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * nus * a.d +
+  a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * a.n_seq * a.d +
                                 sizeof(int32_t) * (size_t)(T * nax + T) +
                                 sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
   a.meta_lds_bytes = (int32_t)((20 * (size_t)a.M + 15) / 16 * 16);
@@ -428,9 +476,9 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   const size_t shmem = (size_t)a.meta_lds_bytes + a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
   if (T * nax > 64 * kGatherMaxIdsPerLane || shmem > 160 * 1024) return hipErrorInvalidValue;
   const int64_t rows_per_block = 4 * (int64_t)T;
-  const dim3 grid((unsigned)((a.R + rows_per_block - 1) / rows_per_block));
-  if (a.se_in_lds) return gather_se_l<TS, MODE, LL, CPT, true>(hashed, a, grid, shmem, s);
-  return gather_se_l<TS, MODE, LL, CPT, false>(hashed, a, grid, shmem, s);
+  const int64_t blocks = (a.R + rows_per_block - 1) / rows_per_block;
+  if (a.se_in_lds) return gather_se_l<TS, MODE, LL, CPT, true>(hashed, a, blocks, shmem, s);
+  return gather_se_l<TS, MODE, LL, CPT, false>(hashed, a, blocks, shmem, s);
 }
 
 // chunks per lane: 8 (a wave holds 512 / chunks-per-row rows); 16 only when a
