@@ -51,6 +51,7 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
   const int64_t q = blockIdx.x;
   const int64_t Q = a.Q;
   const int d = a.d, nu = a.n_user, ns = a.n_seq, nus = nu + ns;
+  extern __shared__ float s_u[];   // [nus][d] pooled rows of this request
   if (threadIdx.x == 0) {  // offsets sanity (reported in validate mode)
     bool bad = a.req_off[q + 1] < a.req_off[q];
     if (q == 0) bad |= a.req_off[0] != 0;
@@ -68,6 +69,7 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
     const TS *tab = static_cast<const TS *>(a.tables[f]);
     const TS v = row >= 0 ? tab[(int64_t)row * d + k] : Elem<TS>::from_f32(0.0f);
     a.U[(q * nus + f) * d + k] = Elem<TS>::to_f32(v);
+    s_u[f * d + k] = Elem<TS>::to_f32(v);
     static_cast<TS *>(a.Uh)[(q * nu + f) * d + k] = v;   // exact copy in the storage type
     if (k == 0) a.urow[q * nu + f] = row;
   }
@@ -84,11 +86,12 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
       if (row >= 0) acc += Elem<TS>::to_f32(tab[(int64_t)row * d + k]);
     }
     a.U[(q * nus + g) * d + k] = acc;
+    s_u[g * d + k] = acc;
   }
   __syncthreads();
   for (int g = threadIdx.x; g < nus; g += blockDim.x) {  // squeeze: mean over d
     float acc = 0.0f;
-    for (int k = 0; k < d; ++k) acc += a.U[(q * nus + g) * d + k];
+    for (int k = 0; k < d; ++k) acc += s_u[g * d + k];
     a.zU[q * nus + g] = acc / (float)d;
   }
 }
@@ -403,8 +406,10 @@ __global__ __launch_bounds__(256) void mask_select_kernel(const float *partial, 
 // ------------------------------------------------------------- launchers
 template <typename TS>
 static hipError_t user_pool_t(bool hashed, const GatherArgs &a, hipStream_t s) {
-  if (hashed) hipLaunchKernelGGL((user_pool_kernel<TS, true>), dim3(a.Q), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((user_pool_kernel<TS, false>), dim3(a.Q), dim3(256), 0, s, a);
+  // a row holds at most kGatherMaxChunksPerRow chunks, so nus * d floats fit in LDS
+  const size_t shmem = sizeof(float) * (size_t)(a.n_user + a.n_seq) * a.d;
+  if (hashed) hipLaunchKernelGGL((user_pool_kernel<TS, true>), dim3(a.Q), dim3(256), shmem, s, a);
+  else hipLaunchKernelGGL((user_pool_kernel<TS, false>), dim3(a.Q), dim3(256), shmem, s, a);
   return hipGetLastError();
 }
 

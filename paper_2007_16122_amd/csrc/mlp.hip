@@ -358,25 +358,59 @@ __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
 
   const int64_t r0 = (int64_t)blockIdx.x * BR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // input tile (rows past the end are clamped: loaded, never stored)
-  constexpr int CPR0 = K0 / 8;
-  for (int c = tid; c < BR * CPR0; c += 256) {
+  // input tile (rows past the end are clamped: loaded, never stored); every
+  // load is issued before the first LDS store so the tile costs one HBM
+  // round trip, not one per chunk
+  constexpr int CPR0 = K0 / 8, NLD = BR * CPR0 / 256;
+  static_assert((BR * CPR0) % 256 == 0, "tile chunks");
+  uint4 tile[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int c = tid + i * 256;
     const int row = c / CPR0, kc = c - row * CPR0;
     int64_t r = r0 + row;
     r = r < R ? r : R - 1;
-    *reinterpret_cast<uint4 *>(&s_in[row * S0 + kc * 8]) =
-        *reinterpret_cast<const uint4 *>(A + r * K0 + kc * 8);
+    tile[i] = *reinterpret_cast<const uint4 *>(A + r * K0 + kc * 8);
   }
-  for (int i = tid; i < n_out * N2; i += 256) s_wh[i] = Elem<TS>::to_f32(Wh[i]);
-  if (tid < n_out) s_bh[tid] = bh[tid];
-  __syncthreads();
 
   const int frow = lane & 15, fk = (lane >> 4) * 8;
   const int dn = (lane >> 4) * 4, dr = lane & 15;
+  // The weight fragments of both layers are loaded once, before the input
+  // tile is needed, so their L2 latency overlaps the tile load instead of
+  // stalling every K step.
+  constexpr int NB1 = N1 / 4 / 16, KS1 = K0 / 32;   // layer 1: blocks per wave, K steps
+  constexpr int NB2 = N2 / 4 / 16, KS2 = N1 / 32;   // layer 2
+  frag w1f[KS1][NB1], w2f[KS2][NB2];
+#pragma unroll
+  for (int k = 0; k < KS1; ++k)
+#pragma unroll
+    for (int i = 0; i < NB1; ++i)
+      w1f[k][i] = *reinterpret_cast<const frag *>(W1 + (int64_t)(wave * (N1 / 4) + i * 16 + frow) * K0 +
+                                                 k * 32 + fk);
+#pragma unroll
+  for (int k = 0; k < KS2; ++k)
+#pragma unroll
+    for (int i = 0; i < NB2; ++i)
+      w2f[k][i] = *reinterpret_cast<const frag *>(W2 + (int64_t)(wave * (N2 / 4) + i * 16 + frow) * N1 +
+                                                 k * 32 + fk);
+  static_assert(2 * N2 <= 256, "one head weight per thread");
+  const TS whv = Wh[tid < n_out * N2 ? tid : 0];
+  const float bhv = bh[tid < n_out ? tid : 0];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int c = tid + i * 256;
+    const int row = c / CPR0, kc = c - row * CPR0;
+    *reinterpret_cast<uint4 *>(&s_in[row * S0 + kc * 8]) = tile[i];
+  }
+  if (tid < n_out * N2) s_wh[tid] = Elem<TS>::to_f32(whv);
+  if (tid < n_out) s_bh[tid] = bhv;
+  __syncthreads();   // input tile and head weights in LDS
+
   // one hidden layer on the tile: wave w owns outputs [w*NOUT/4, (w+1)*NOUT/4)
-  auto layer = [&](const TS *in, int s_in_stride, int kdim, const TS *Wg, const float *bg,
-                   TS *out, int s_out_stride, auto nout_tag) {
+  auto layer = [&](const TS *in, int s_in_stride, const float *bg, TS *out, int s_out_stride,
+                   auto &wf, auto nout_tag, auto ks_tag) {
     constexpr int NOUT = decltype(nout_tag)::value;
+    constexpr int KS = decltype(ks_tag)::value;
     constexpr int NB = NOUT / 4 / 16;     // 16-wide output blocks per wave
     f32x4 acc[NB][BR / 16];
 #pragma unroll
@@ -384,16 +418,13 @@ __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
 #pragma unroll
       for (int j = 0; j < BR / 16; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int nbase = wave * (NOUT / 4);
-    for (int k0 = 0; k0 < kdim; k0 += 32) {
-      frag fa[NB];
 #pragma unroll
-      for (int i = 0; i < NB; ++i)
-        fa[i] = *reinterpret_cast<const frag *>(Wg + (int64_t)(nbase + i * 16 + frow) * kdim + k0 + fk);
+    for (int k = 0; k < KS; ++k) {
 #pragma unroll
       for (int j = 0; j < BR / 16; ++j) {
-        const frag fb = *reinterpret_cast<const frag *>(&in[(j * 16 + frow) * s_in_stride + k0 + fk]);
+        const frag fb = *reinterpret_cast<const frag *>(&in[(j * 16 + frow) * s_in_stride + k * 32 + fk]);
 #pragma unroll
-        for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+        for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
       }
     }
 #pragma unroll
@@ -414,9 +445,9 @@ __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
       }
     }
   };
-  layer(s_in, S0, K0, W1, b1, s_h1, S1, std::integral_constant<int, N1>{});
+  layer(s_in, S0, b1, s_h1, S1, w1f, std::integral_constant<int, N1>{}, std::integral_constant<int, KS1>{});
   __syncthreads();
-  layer(s_h1, S1, N1, W2, b2, s_h2, S2, std::integral_constant<int, N2>{});
+  layer(s_h1, S1, b2, s_h2, S2, w2f, std::integral_constant<int, N2>{}, std::integral_constant<int, KS2>{});
   __syncthreads();
 
   // head: 4 threads per row, each over a quarter of the N2 inputs
