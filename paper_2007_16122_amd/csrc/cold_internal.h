@@ -126,6 +126,7 @@ struct GatherArgs {
   int32_t se_lds_bytes;           // LDS for SE parameters, 0 if read from global
   int32_t se_in_lds;
   int32_t meta_lds_bytes;         // LDS for per-group table metadata
+  int32_t req_lds_bytes;          // LDS for the request offsets, 0 if searched in global
   int64_t R, Q, n_seq_ids;
   const int32_t *req_off;         // [Q+1]
   const void *user_ids;           // [n_user][Q]
@@ -172,5 +173,6 @@ constexpr int kGatherThreads = 256;
 constexpr int kGatherMaxChunksPerRow = 1024;  // 64 lanes x 16 chunks
 constexpr int kGatherMaxIdsPerLane = 8;       // rows per wave x (ad + cross fields) <= 512
 constexpr int kMaskParts = 64;
+constexpr int kGatherMaxReqLds = 1024;        // request offsets held in LDS up to this count
 
 }  // namespace cold

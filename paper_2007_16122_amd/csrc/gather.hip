@@ -142,6 +142,13 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     s_magic[g] = a.table_magic[g];
     s_rows[g] = (int32_t)a.table_rows[g];
   }
+  // request offsets in LDS when they fit: the row -> request search then
+  // costs LDS latency, not a chain of dependent global loads
+  int32_t *s_req = reinterpret_cast<int32_t *>(cursor);   // [Q+1] if req_in_lds
+  const bool req_in_lds = a.req_lds_bytes != 0;
+  if (req_in_lds)
+    for (int64_t i = threadIdx.x; i <= Q; i += kGatherThreads) s_req[i] = a.req_off[i];
+  cursor += a.req_lds_bytes;
   const float *w1 = a.w1, *b1 = a.b1, *w2 = a.w2, *b2 = a.b2;
   if constexpr (MODE != kApplyWeights && SE_LDS) {
     {
@@ -172,18 +179,14 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   const int64_t stride = (int64_t)gridDim.x * (kGatherThreads / 64);
   for (int64_t wt = (int64_t)blockIdx.x * (kGatherThreads / 64) + wave; wt < n_tiles; wt += stride) {
   const int64_t r0 = wt * Tw;
-  wave_sync();  // the previous tile's LDS reads are done
   // chunk coordinates, opaque to the compiler so that nothing derived from
   // them is hoisted out of the tile loop (which would pin registers)
   int tf = t_first, cf = c_first, ln = lane;
   asm volatile("" : "+v"(tf), "+v"(cf), "+v"(ln));
 
-  // ---- request of each row
-  for (int t = ln; t < Tw; t += 64) {
-    const int64_t r = r0 + t;
-    rq[t] = r < R ? (int32_t)request_of_row(a.req_off, Q, r) : 0;
-  }
-  // ---- ad/cross ids (all loads issued before any is used), then table rows
+  // ---- ad/cross ids first (all loads issued before any is used; they go
+  //      to registers, so they need not wait for the previous tile), then
+  //      the request of each row, then table rows
   typedef typename std::conditional<HASHED, uint64_t, int32_t>::type id_t;
   id_t idv[IDMAX];
 #pragma unroll
@@ -199,6 +202,13 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
         idv[k] = ids[(int64_t)(is_ad ? f : f - a.n_ad) * R + r];
       }
     }
+  }
+  wave_sync();  // the previous tile's LDS reads are done
+  for (int t = ln; t < Tw; t += 64) {
+    const int64_t r = r0 + t;
+    int32_t q = 0;
+    if (r < R) q = (int32_t)(req_in_lds ? request_of_row(s_req, Q, r) : request_of_row(a.req_off, Q, r));
+    rq[t] = q;
   }
   wave_sync();  // rq visible
 #pragma unroll
@@ -475,10 +485,12 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
                                 sizeof(int32_t) * (size_t)(T * nax + T) +
                                 sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
   a.meta_lds_bytes = (int32_t)((20 * (size_t)a.M + 15) / 16 * 16);
+  a.req_lds_bytes = a.Q + 1 <= kGatherMaxReqLds ? (int32_t)((4 * (a.Q + 1) + 15) / 16 * 16) : 0;
   const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
   a.se_in_lds = MODE != kApplyWeights && se_floats * sizeof(float) <= 24 * 1024;
   a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
-  const size_t shmem = (size_t)a.meta_lds_bytes + a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
+  const size_t shmem = (size_t)a.meta_lds_bytes + a.req_lds_bytes + a.se_lds_bytes +
+                       4 * (size_t)a.wave_lds_bytes;
   if (T * nax > 64 * kGatherMaxIdsPerLane || shmem > 160 * 1024) return hipErrorInvalidValue;
   const int64_t rows_per_block = 4 * (int64_t)T;
   const int64_t blocks = (a.R + rows_per_block - 1) / rows_per_block;
