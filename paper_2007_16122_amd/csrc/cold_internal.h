@@ -80,6 +80,19 @@ template <> struct Elem<_Float16> {
   __device__ static inline _Float16 from_f32(float x) { return static_cast<_Float16>(x); }
 };
 
+// ------------------------------------------------------------ waits
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// wait until at most N of this wave's vector memory operations are in flight
+// and all of its LDS operations have returned (s_waitcnt: vmcnt low bits
+// [3:0], expcnt [6:4] left at its maximum, lgkmcnt [11:8] = 0, vmcnt high
+// bits [15:14])
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
 // ------------------------------------------------------------ id resolution
 // SplitMix64 output function (Steele, Lea, Flood, OOPSLA 2014).
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {

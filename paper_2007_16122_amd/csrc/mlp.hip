@@ -180,15 +180,6 @@ __global__ __launch_bounds__(256, 2) void dense_relu_mfma_kernel(const TS *__res
 // segment is written with full 16-byte stores.
 __device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 
-__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
-
-// wait until at most N of this wave's global loads are in flight and all of
-// its LDS reads have returned
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
-}
 
 template <typename TS, int BR, int BN, int S, int MINW = 2>
 __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__restrict__ X,
@@ -255,6 +246,18 @@ __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__
   for (int st = 0; st < S - 1; ++st)
     if (st < ksteps) issue(st, st);
 
+  // bias of this lane's output features, loaded now so that its latency
+  // hides behind the K loop (indices clamped; features past N are not stored)
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+  float bv[NI][4];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = n0 + wn * (BN / 2) + i * 16 + dn + e;
+      bv[i][e] = bias[n < N ? n : N - 1];
+    }
+
   const int frow = lane & 15, fc = lane >> 4;
   const int a_off = (wn * (BN / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
   const int b_off = BN * ROWB + (wr * (BR / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
@@ -294,20 +297,16 @@ __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__
   __builtin_amdgcn_s_barrier();
   compiler_fence();
   uint16_t *sout = reinterpret_cast<uint16_t *>(smem);
-  const int dn = (lane >> 4) * 4, dr = lane & 15;
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int nl = wn * (BN / 2) + i * 16 + dn;
-    float bv[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) bv[e] = (n0 + nl + e < N) ? bias[n0 + nl + e] : 0.0f;
 #pragma unroll
     for (int j = 0; j < RJ; ++j) {
       const int rl = wr * (BR / 2) + j * 16 + dr;
       float o[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float t = acc[i][j][e] + bv[e];
+        const float t = acc[i][j][e] + bv[i][e];
         o[e] = t > 0.0f ? t : 0.0f;
       }
       uint2 packed;
