@@ -309,6 +309,9 @@ def main():
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain "
                          "copy of known size, to calibrate HBM byte counters)")
+    ap.add_argument("--topn", type=int, default=200,
+                    help="after timing, time the per-request top-n selection by eCPM "
+                         "(0 = skip); not part of the timed step")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the 2,000-ad latency runs (kernel-trace profiles of the step only)")
     ap.add_argument("--summarize-trace", metavar="DIR",
@@ -423,6 +426,36 @@ def main():
             log(f"graph replay unavailable: {exc}")
         log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
 
+    topn = None
+    if args.topn > 0:
+        # per-request top-n by eCPM = CTR * bid after scoring (Section 2)
+        bids = torch.from_numpy(synth.make_bids(cfg, R)).to(dev)
+        req_off_t = dev_batch["req_off"]
+        binding.select_topn(scores, bids, req_off_t, args.topn)
+        torch.cuda.synchronize()
+        t_ev0, t_ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 20
+        t_ev0.record(stream)
+        for _ in range(reps):
+            binding.select_topn(scores, bids, req_off_t, args.topn)
+        t_ev1.record(stream)
+        torch.cuda.synchronize()
+        batch_us = t_ev0.elapsed_time(t_ev1) / reps * 1e3
+        one_off = req_off_t[:2].clone()
+        one_off[1] = min(cfg.cand_per_request, R)
+        t_ev0.record(stream)
+        for _ in range(reps):
+            binding.select_topn(scores, bids, one_off, args.topn)
+        t_ev1.record(stream)
+        torch.cuda.synchronize()
+        one_us = t_ev0.elapsed_time(t_ev1) / reps * 1e3
+        topn = {"n": args.topn, "us_per_batch": round(batch_us, 2),
+                "rows_per_s": round(R / (batch_us * 1e-6), 1),
+                "us_one_request": round(one_us, 2),
+                "share_of_step": round(batch_us * 1e-3 / ms_per_step, 4)}
+        log(f"top-{args.topn} by eCPM: {batch_us:.2f} us per batch, {one_us:.2f} us for one "
+            f"{cfg.cand_per_request}-ad request")
+
     if args.copy_probe_mb > 0:
         n = args.copy_probe_mb << 20
         src = torch.ones(n, dtype=torch.uint8, device=dev)
@@ -463,6 +496,7 @@ def main():
                         traffic=(traffic["stages"].get(e["name"]) if traffic else None))
                    for e in stage_rows],
         "cpu_baseline": cpu,
+        "topn": topn,
     }
     print(json.dumps(out), flush=True)
     model.close()

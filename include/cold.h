@@ -178,6 +178,30 @@ int cold_profile_enable(cold_model *model, int32_t enable);
 int cold_profile_read(cold_model *model, int32_t max_stages, char (*names)[32], float *total_ms,
                       int32_t *n_stages, int32_t *n_calls);
 
+/* Per-request top-n selection by eCPM (Section 2: the pre-ranking stage
+ * passes on the N candidates of each request with the highest eCPM; its
+ * footnote defines eCPM = pCTR * bid for CPC bidding).  Stateless: needs no
+ * model.
+ *   scores     device fp32 [n_rows]: CTR of each row (as cold_score writes it)
+ *   bids       device fp32 [n_rows]: bid of each row
+ *   req_off    device int32 [n_requests + 1], as in cold_batch (offsets are
+ *              clamped to [0, n_rows])
+ *   n_top      1 .. COLD_TOPN_MAX
+ *   top_rows   device int32 [n_requests][n_top]: row indices (into the batch,
+ *              not the request), best first
+ *   top_ecpm   device fp32 [n_requests][n_top] or NULL: their eCPM
+ * eCPM = scores[r] * bids[r], one fp32 multiplication.  Rows are ordered by
+ * eCPM under the IEEE-754 totalOrder (so -0 < +0 and NaNs sort by sign
+ * beyond the infinities), ties by ascending row index.  A request with
+ * fewer than n_top rows fills its remaining slots with row -1 and eCPM
+ * -infinity.  Asynchronous on `stream`; n_requests = 0 is a no-op.
+ * Returns COLD_ERR_INVALID_ARG for a negative size, n_rows or n_requests
+ * above 2^31 - 1, n_top out of range, or a NULL required pointer. */
+#define COLD_TOPN_MAX 1024
+int cold_select_topn(const float *scores, const float *bids, const int32_t *req_off,
+                     int64_t n_requests, int64_t n_rows, int32_t n_top, int32_t *top_rows,
+                     float *top_ecpm, void *stream);
+
 /* Static text of a status code. */
 const char *cold_status_string(int status);
 

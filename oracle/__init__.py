@@ -191,3 +191,57 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
         raise OracleError(_ERRORS.get(st, f"status {st}"))
     out["n_threads"] = n_threads
     return out
+
+
+# ----------------------------------------------------------------------------
+# Top-n selection by eCPM (Section 2 and its footnote: the pre-ranking stage
+# passes on the N candidates of a request with the highest eCPM, where
+# eCPM = pCTR * bid for CPC bidding).  Plain numpy, one request at a time.
+# ----------------------------------------------------------------------------
+def total_order_key(x32: np.ndarray) -> np.ndarray:
+    """IEEE-754 totalOrder position of fp32 values as int64 (larger = later
+    in the order): a non-negative value keeps its magnitude bits, a value
+    with the sign bit set becomes -(magnitude bits) - 1, which puts -0 just
+    below +0, larger negative magnitudes lower, and NaNs beyond the
+    infinities on the side of their sign."""
+    bits = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.int64)
+    mag = bits & 0x7FFFFFFF
+    return np.where(bits >> 31 == 1, -mag - 1, mag)
+
+
+def select_topn(scores, bids, req_off, n_top: int):
+    """Per request q: eCPM = scores * bids (one fp32 multiplication per row),
+    rows ordered by eCPM descending under totalOrder, ties by ascending row
+    index, the first n_top kept.  Returns (rows int32 [Q][n_top], ecpm fp32
+    [Q][n_top]); a request with fewer rows pads with -1 and -inf."""
+    scores = np.asarray(scores, dtype=np.float32)
+    bids = np.asarray(bids, dtype=np.float32)
+    req_off = np.asarray(req_off, dtype=np.int64)
+    n_req = req_off.size - 1
+    r_total = scores.size
+    rows = np.full((n_req, n_top), -1, dtype=np.int32)
+    ecpm = np.full((n_req, n_top), -np.inf, dtype=np.float32)
+    for q in range(n_req):
+        lo = min(max(int(req_off[q]), 0), r_total)
+        hi = min(max(int(req_off[q + 1]), lo), r_total)
+        if hi == lo:
+            continue
+        e = scores[lo:hi] * bids[lo:hi]                  # float32 * float32 -> float32
+        idx = np.arange(lo, hi, dtype=np.int64)
+        order = np.lexsort((idx, -total_order_key(e)))  # last key is the primary one
+        k = min(n_top, hi - lo)
+        rows[q, :k] = idx[order[:k]]
+        ecpm[q, :k] = e[order[:k]]
+    return rows, ecpm
+
+
+def recall_at(pre_rows, rank_rows) -> float:
+    """Eq. 4 of Section 4.1: |top-k by the pre-ranking model ∩ top-m by the
+    ranking model| / |top-m by the ranking model|, pooled over requests
+    (padding -1 entries are ignored)."""
+    hit = tot = 0
+    for a, b in zip(pre_rows, rank_rows):
+        ref = set(int(v) for v in b if v >= 0)
+        hit += len(ref & set(int(v) for v in a if v >= 0))
+        tot += len(ref)
+    return hit / tot if tot else 1.0

@@ -32,7 +32,8 @@ DTYPES = {"f32": COLD_F32, "bf16": COLD_BF16, "f16": COLD_F16}
 EXPORTS = ("cold_create_model", "cold_destroy_model", "cold_weight_arena_bytes",
            "cold_workspace_bytes", "cold_load_weights", "cold_score",
            "cold_status_string", "cold_last_error", "cold_profile_enable",
-           "cold_profile_read")
+           "cold_profile_read", "cold_select_topn")
+COLD_TOPN_MAX = 1024
 
 
 class ColdError(RuntimeError):
@@ -100,6 +101,8 @@ def lib():
         L.cold_profile_enable.restype = ctypes.c_int
         L.cold_profile_read.argtypes = [vp, i32, vp, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.cold_profile_read.restype = ctypes.c_int
+        L.cold_select_topn.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp]
+        L.cold_select_topn.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -161,6 +164,27 @@ def cold_profile_read(h, max_stages: int = 32):
     out = [(bytes(names[i]).split(b"\0")[0].decode(), float(total[i]))
            for i in range(min(ns.value, max_stages))]
     return out, nc.value
+
+
+def cold_select_topn(scores: int, bids: int, req_off: int, n_requests: int, n_rows: int,
+                     n_top: int, top_rows: int, top_ecpm: Optional[int], stream: int) -> int:
+    return lib().cold_select_topn(scores, bids, req_off, n_requests, n_rows, n_top, top_rows,
+                                  top_ecpm, stream)
+
+
+def select_topn(scores, bids, req_off, n_top: int, with_ecpm: bool = True):
+    """Top-n rows of every request by eCPM = score * bid on the current
+    stream: returns (rows int32 [Q][n_top], ecpm fp32 [Q][n_top] or None)."""
+    import torch
+    n_req = req_off.numel() - 1
+    rows = torch.empty((max(n_req, 0), n_top), dtype=torch.int32, device=scores.device)
+    ecpm = torch.empty((max(n_req, 0), n_top), dtype=torch.float32, device=scores.device) \
+        if with_ecpm else None
+    st = cold_select_topn(_ptr(scores), _ptr(bids), _ptr(req_off), n_req, scores.numel(), n_top,
+                          _ptr(rows), _ptr(ecpm), torch.cuda.current_stream().cuda_stream)
+    if st != COLD_OK:
+        raise ColdError(st, "cold_select_topn: " + cold_status_string(st))
+    return rows, ecpm
 
 
 def make_desc(n_user, n_seq, n_ad, n_cross, emb_dim, dtype, se_reduction,

@@ -179,6 +179,8 @@ bool tail_supported(int dtype, int K0, int N1, int N2, int n_out);
 hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float *b1,
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s);
+hipError_t launch_topn(const float *scores, const float *bids, const int32_t *req_off, int64_t Q,
+                       int64_t R, int32_t n_top, int32_t *top_rows, float *top_ecpm, hipStream_t s);
 hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, float *scores,
                        int64_t R, int32_t K, int32_t n_out, hipStream_t s);
 

@@ -30,7 +30,7 @@ import numpy as np
 
 __all__ = [
     "ColdConfig", "CONFIGS", "config", "make_batch", "make_params",
-    "table_numpy", "table_torch", "table_rows_numpy", "zipf_ranks",
+    "table_numpy", "table_torch", "table_rows_numpy", "zipf_ranks", "make_bids",
 ]
 
 MASK32 = 0xFFFFFFFF
@@ -215,6 +215,16 @@ def _ids_for_field(rng, cfg: ColdConfig, size: int, device=None) -> np.ndarray:
     b = np.uint64(int(rng.integers(0, 2**63)))
     with np.errstate(over="ignore"):
         return ranks.astype(np.uint64) * a + b
+
+
+def make_bids(cfg: ColdConfig, n_rows: int, seed: Optional[int] = None) -> np.ndarray:
+    """CPC bids of the candidate rows (fp32, whole cents, log-normal around
+    0.50 and clipped to 0.01 .. 50.00).  The paper's selection metric is
+    eCPM = pCTR * bid (Section 2); its bids are not published."""
+    seed = cfg.seed if seed is None else seed
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 0xB1D5]))
+    cents = np.rint(np.exp(rng.normal(np.log(50.0), 0.7, size=n_rows)))
+    return (np.clip(cents, 1, 5000) / 100.0).astype(np.float32)
 
 
 def make_batch(cfg: ColdConfig, seed: Optional[int] = None,

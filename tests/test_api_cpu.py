@@ -126,3 +126,19 @@ def test_status_strings():
     assert B.cold_status_string(-99) == "unknown status"
     assert B.lib().cold_last_error(None) == b"null model"
     B.lib().cold_destroy_model(None)   # no-op
+
+
+def test_select_topn_rejects_bad_calls_before_the_device():
+    fake = 0x1000   # never dereferenced: every call below fails its host checks
+    sel = B.cold_select_topn
+    assert sel(fake, fake, fake, 1, 10, 0, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, fake, 1, 10, B.COLD_TOPN_MAX + 1, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, fake, -1, 10, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, fake, 1, -1, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, fake, 1, 1 << 31, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, None, 1, 10, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, fake, fake, 1, 10, 5, None, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(None, fake, fake, 1, 10, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    assert sel(fake, None, fake, 1, 10, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
+    # no requests: nothing to do, nothing enqueued
+    assert sel(None, None, None, 0, 0, 5, None, None, None) == B.COLD_OK
