@@ -6,10 +6,13 @@ workload (32 requests x 2,000 candidate ads = 64,000 rows, 48 fields of dim
 16 over 1M-row bf16 tables, SE block, 768x1024x512x256x128x64x2 network),
 inputs resident in HBM before timing starts.  Prints one JSON line.
 
-Also measured: the p50/p99 host-side latency of scoring one 2,000-ad request
-(eager launches and HIP-graph replay), per-stage kernel times with HIP events
-on the scoring stream, the roofline fraction of the dominant kernel, and the
-CPU checker's throughput on a bounded sample of the same workload.
+Also measured: per-stage kernel times with HIP events on the scoring stream
+(a second pass of the same steps) and the roofline fraction of the dominant
+kernel; the p50/p99 host-side latency of scoring one 2,000-ad request (eager
+launches and HIP-graph replay); serving curves (one call over B requests,
+and single requests replayed on K concurrent streams); the per-request
+top-n selection by eCPM; and the CPU checker's throughput on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -77,24 +80,46 @@ def roofline_entry(cfg, batch, stage, ms):
             "frac": round(ach / PEAK_HBM_GBS, 4), "work_per_launch": work}
 
 
-def request_slice(batch, q, cfg):
-    """Request q of a batch as a one-request batch (numpy)."""
+def request_slice(batch, q, cfg, q_end=None):
+    """Requests q .. q_end-1 (default: request q alone) of a batch as a
+    batch of their own (numpy)."""
+    q_end = q + 1 if q_end is None else q_end
     off = batch["req_off"]
-    lo, hi = int(off[q]), int(off[q + 1])
+    lo, hi = int(off[q]), int(off[q_end])
     Q = len(off) - 1
-    out = dict(req_off=np.array([0, hi - lo], np.int32),
-               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q + 1]),
+    out = dict(req_off=(off[q:q_end + 1] - lo).astype(np.int32),
+               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q_end]),
                ad_ids=np.ascontiguousarray(batch["ad_ids"][:, lo:hi]),
                cross_ids=np.ascontiguousarray(batch["cross_ids"][:, lo:hi]),
-               n_rows=hi - lo, n_requests=1)
+               n_rows=hi - lo, n_requests=q_end - q)
     if cfg.n_seq:
         so = batch["seq_off"]
-        segs = [batch["seq_ids"][so[f * Q + q]:so[f * Q + q + 1]] for f in range(cfg.n_seq)]
+        segs = [batch["seq_ids"][so[f * Q + qq]:so[f * Q + qq + 1]]
+                for f in range(cfg.n_seq) for qq in range(q, q_end)]
         out["seq_off"] = np.concatenate([[0], np.cumsum([len(s) for s in segs])]).astype(np.int32)
         out["seq_ids"] = np.concatenate(segs)
     else:
         out["seq_off"] = np.zeros(1, np.int32)
         out["seq_ids"] = np.zeros(0, batch["ad_ids"].dtype)
+    return out
+
+
+def batching_curve(model, batch, cfg, sizes, iters, torch, binding):
+    """Latency of one cold_score call over B requests of the batch (host
+    wall clock to stream synchronisation) and the request rate a server that
+    batches B requests per call would reach: B / p50."""
+    out = []
+    n_req = len(batch["req_off"]) - 1
+    for b in sizes:
+        if b > n_req:
+            continue
+        sub = binding.batch_to_device(request_slice(batch, 0, cfg, b), model.device)
+        sc = torch.empty(max(sub["n_rows"], 1), dtype=torch.float32, device=model.device)
+        p50, p99 = latency(model, sub, sc, iters, torch, graph=False)
+        out.append({"requests_per_call": b, "p50_ms": round(p50, 4), "p99_ms": round(p99, 4),
+                    "requests_per_s": round(b / (p50 * 1e-3), 1)})
+        log(f"batching {b:2d} requests per call: p50 {p50:.4f} ms, p99 {p99:.4f} ms, "
+            f"{out[-1]['requests_per_s']:.0f} req/s")
     return out
 
 
@@ -126,6 +151,58 @@ def latency(model, dev_batch, scores, iters, torch, graph):
             times.append(time.perf_counter() - t0)
     t = np.array(times) * 1e3
     return float(np.median(t)), float(np.quantile(t, 0.99))
+
+
+def serving_curve(model, batch, cfg, streams, iters, torch, binding):
+    """Concurrent serving of single requests: K streams, each replaying a HIP
+    graph of one request's cold_score call back to back with its own
+    workspace (the in-process analogue of the paper's MPS setup, Section 3.3).
+    Per K: requests/s over the whole run and the per-request GPU latency
+    (events around each replay) p50 / p99."""
+    out = []
+    n_req = len(batch["req_off"]) - 1
+    for k in streams:
+        ss = [torch.cuda.Stream() for _ in range(k)]
+        graphs, keep = [], []
+        for i, st in enumerate(ss):
+            req = binding.batch_to_device(request_slice(batch, i % n_req, cfg), model.device)
+            ws = torch.empty(max(binding.cold_workspace_bytes(model.h, req["n_rows"], 1), 256),
+                             dtype=torch.uint8, device=model.device)
+            sc = torch.empty(req["n_rows"], dtype=torch.float32, device=model.device)
+            g = torch.cuda.CUDAGraph()
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                model.score(req, scores=sc, workspace=ws)      # warm-up outside the graph
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=st):
+                model.score(req, scores=sc, workspace=ws)
+            graphs.append(g)
+            keep.append((req, ws, sc))
+        torch.cuda.synchronize()
+        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(iters)] for _ in range(k)]
+        for i in range(k):                                     # one untimed round
+            with torch.cuda.stream(ss[i]):
+                graphs[i].replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for it in range(iters):
+            for i in range(k):
+                with torch.cuda.stream(ss[i]):
+                    ev[i][it][0].record(ss[i])
+                    graphs[i].replay()
+                    ev[i][it][1].record(ss[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        lat = np.array([a.elapsed_time(b) for row in ev for a, b in row])
+        out.append({"streams": k, "requests_per_s": round(k * iters / wall, 1),
+                    "ads_per_s": round(k * iters * cfg.cand_per_request / wall, 1),
+                    "p50_ms": round(float(np.median(lat)), 4),
+                    "p99_ms": round(float(np.quantile(lat, 0.99)), 4)})
+        log(f"serving {k:2d} streams: {out[-1]['requests_per_s']:9.1f} req/s, "
+            f"p50 {out[-1]['p50_ms']:.4f} ms, p99 {out[-1]['p99_ms']:.4f} ms")
+        del graphs, keep
+    return out
 
 
 def cpu_baseline(cfg, batch, params, target_s):
@@ -312,8 +389,17 @@ def main():
     ap.add_argument("--topn", type=int, default=200,
                     help="after timing, time the per-request top-n selection by eCPM "
                          "(0 = skip); not part of the timed step")
+    ap.add_argument("--serving-streams", default="1,2,4,8,16",
+                    help="after timing, concurrent single-request serving on this many streams "
+                         "(comma list; empty = skip)")
+    ap.add_argument("--serving-iters", type=int, default=200)
+    ap.add_argument("--batching", default="1,2,4,8,16,32",
+                    help="after timing, the latency of one call over this many requests "
+                         "(comma list; empty = skip)")
     ap.add_argument("--no-latency", action="store_true",
-                    help="skip the 2,000-ad latency runs (kernel-trace profiles of the step only)")
+                    help="skip every measurement after the timed steps: the 2,000-ad latency, "
+                         "the serving curves and the top-n selection (kernel-trace profiles of "
+                         "the step only)")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -364,7 +450,7 @@ def main():
     torch.cuda.synchronize()
     assert bool(torch.isfinite(scores).all()), "non-finite scores"
 
-    binding.cold_profile_enable(model.h, True)
+    # timed region: K steps, nothing recorded between the kernels
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -375,12 +461,26 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    stages, n_calls = binding.cold_profile_read(model.h)
-    binding.cold_profile_enable(model.h, False)
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
     value = R / (ms_per_step * 1e-3)
     log(f"{args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f}), "
         f"{value:.4g} ads/s")
+    # the same K steps again with a HIP event on the stream before every
+    # kernel stage: per-kernel durations for the rooflines (an event between
+    # two kernels stops the next one from starting early, so this pass is a
+    # little slower than the one above)
+    binding.cold_profile_enable(model.h, True)
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    p0.record(stream)
+    for _ in range(args.steps):
+        model.score(dev_batch, scores=scores)
+    p1.record(stream)
+    torch.cuda.synchronize()
+    stages, n_calls = binding.cold_profile_read(model.h)
+    binding.cold_profile_enable(model.h, False)
+    ms_profiled = p0.elapsed_time(p1) / args.steps
+    log(f"with stage events: {ms_profiled:.4f} ms/step")
 
     stage_rows = []
     for name, tot in stages:
@@ -425,6 +525,18 @@ def main():
         except Exception as exc:  # graph capture is an optional measurement
             log(f"graph replay unavailable: {exc}")
         log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
+
+    if args.no_latency:
+        args.batching, args.serving_streams, args.topn = "", "", 0
+    batching = None
+    if args.batching:
+        sizes = [int(v) for v in args.batching.split(",") if v]
+        batching = batching_curve(model, batch, cfg, sizes, args.serving_iters, torch, binding)
+
+    serving = None
+    if args.serving_streams:
+        ks = [int(v) for v in args.serving_streams.split(",") if v]
+        serving = serving_curve(model, batch, cfg, ks, args.serving_iters, torch, binding)
 
     topn = None
     if args.topn > 0:
@@ -474,7 +586,8 @@ def main():
     out = {
         "metric": "candidate ads scored/sec on 1 GPU; p50 latency of a 2,000-ad request",
         "value": round(value, 1), "unit": "ads/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step_with_stage_events": round(ms_profiled, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": cfg.name, "requests": cfg.n_requests,
                    "candidates_per_request": cfg.cand_per_request, "rows": R,
@@ -497,6 +610,11 @@ def main():
                    for e in stage_rows],
         "cpu_baseline": cpu,
         "topn": topn,
+        "serving_streams": serving,
+        "serving_batching": batching,
+        "usable_requests_per_s": None if not batching else {
+            f"p99<={lim}ms": max([e["requests_per_s"] for e in batching if e["p99_ms"] <= lim],
+                                 default=None) for lim in (0.1, 0.5, 1.0)},
     }
     print(json.dumps(out), flush=True)
     model.close()

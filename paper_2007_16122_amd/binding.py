@@ -275,12 +275,14 @@ class ColdModel:
                           seq_off=_ptr(batch.get("seq_off")), seq_ids=_ptr(batch.get("seq_ids")))
 
     def score(self, batch: dict, scores=None, importance=None, group_mask=None, rows_out=None,
-              validate=False):
+              validate=False, workspace=None):
         """Score every row; returns the fp32 score tensor (asynchronous on
-        the current stream unless validate)."""
+        the current stream unless validate).  Concurrent calls on different
+        streams pass distinct `workspace` tensors (uint8, device, at least
+        cold_workspace_bytes); by default the model's own workspace is used."""
         torch = self.torch
         b = self.make_batch_struct(batch)
-        ws = self.ensure_workspace(b.n_rows, b.n_requests)
+        ws = self.ensure_workspace(b.n_rows, b.n_requests) if workspace is None else workspace
         if scores is None:
             scores = torch.empty(b.n_rows, dtype=torch.float32, device=self.device)
         st = cold_score(self.h, b, _ptr(ws), ws.numel(), _ptr(scores), _ptr(importance),

@@ -181,6 +181,20 @@ __global__ __launch_bounds__(256, 2) void dense_relu_mfma_kernel(const TS *__res
 __device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 
 
+// wait until at most min(later, MAXL) stages of LOADS loads each are in flight
+template <int LOADS, int MAXL>
+__device__ __forceinline__ void wait_stages(int later) {
+  if constexpr (MAXL > 0) {
+    if (later >= MAXL) {
+      wait_vm<MAXL * LOADS>();
+      return;
+    }
+    wait_stages<LOADS, MAXL - 1>(later);
+  } else {
+    wait_vm<0>();
+  }
+}
+
 template <typename TS, int BR, int BN, int S, int MINW = 2>
 __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__restrict__ X,
                                                                  const TS *__restrict__ W,
@@ -197,7 +211,7 @@ __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__
   constexpr int OUT_BYTES = BR * OUT_STRIDE * 2;
   constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
   static_assert((BN + BR) % 64 == 0, "loads must split evenly over 4 waves");
-  static_assert(S >= 2 && S <= 4, "stages");
+  static_assert(S >= 2 && S <= 8, "stages");
   __shared__ __align__(16) unsigned char smem[SMEM];
 
   const int tile = xcd_tile(blockIdx.x, tiles_total);
@@ -265,9 +279,7 @@ __global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__
   for (int ks = 0; ks < ksteps; ++ks) {
     // stage ks must have landed: later stages issued so far = min(S-2, ksteps-1-ks)
     const int later = ksteps - 1 - ks;
-    if (S >= 4 && later >= 2) wait_vm<2 * LOADS>();
-    else if (S >= 3 && later >= 1) wait_vm<LOADS>();
-    else wait_vm<0>();
+    wait_stages<LOADS, S - 2>(later);
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
