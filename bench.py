@@ -212,7 +212,7 @@ def cpu_baseline(cfg, batch, params, target_s):
     dims = dict(n_user=cfg.n_user, n_seq=cfg.n_seq, n_ad=cfg.n_ad, n_cross=cfg.n_cross,
                 emb_dim=cfg.emb_dim, se_hidden=cfg.se_hidden, dtype=cfg.dtype,
                 hashed=cfg.hashed, linear_log=cfg.linear_log, topk_k=cfg.topk_k,
-                widths=list(cfg.widths))
+                widths=list(cfg.widths), cross_pairs=[list(p) for p in cfg.cross_pairs])
     stored = dict(params)
     stored["mlp_w"] = [synth.mlp_weight_stored(w, cfg.dtype) for w in params["mlp_w"]]
     np_dt = {"f32": np.float32, "f16": np.float16, "bf16": np.uint16}[cfg.dtype]
@@ -232,10 +232,20 @@ def cpu_baseline(cfg, batch, params, target_s):
                                       for q in reqs])
             elif kind == "ad":
                 ids = batch["ad_ids"][g - cfg.n_user - cfg.n_seq][sample]
+            elif cfg.cross_pairs:
+                uf, af = cfg.cross_pairs[g - cfg.n_user - cfg.n_seq - cfg.n_ad]
+                width = (1 << 64) - 1 if cfg.hashed else (1 << 32) - 1
+                req_of = np.searchsorted(batch["req_off"], sample, side="right") - 1
+                pairs = set(zip((int(v) & width for v in batch["user_ids"][uf][req_of]),
+                                (int(v) & width for v in batch["ad_ids"][af][sample])))
+                ids = None
+                rows = np.unique(np.array([oracle.hash_row(oracle.cross_key(u, a), g, cfg.vocab)
+                                           for u, a in pairs], np.int64))
             else:
                 ids = batch["cross_ids"][g - cfg.n_user - cfg.n_seq - cfg.n_ad][sample]
-            rows = (np.array([oracle.hash_row(int(v), g, cfg.vocab) for v in np.unique(ids)])
-                    if cfg.hashed else np.unique(ids)).astype(np.int64)
+            if ids is not None:
+                rows = (np.array([oracle.hash_row(int(v), g, cfg.vocab) for v in np.unique(ids)])
+                        if cfg.hashed else np.unique(ids)).astype(np.int64)
             t = np.zeros((cfg.vocab, cfg.emb_dim), np_dt)
             t[rows] = synth.table_rows_numpy(cfg, g, rows)
             tabs.append(t)
@@ -386,6 +396,9 @@ def main():
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain "
                          "copy of known size, to calibrate HBM byte counters)")
+    ap.add_argument("--gpu-cross", action="store_true",
+                    help="build every cross field on the GPU from a (user field, ad field) "
+                         "id pair instead of reading per-row cross ids")
     ap.add_argument("--topn", type=int, default=200,
                     help="after timing, time the per-request top-n selection by eCPM "
                          "(0 = skip); not part of the timed step")
@@ -430,6 +443,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = synth.CONFIGS[args.workload]
+    if args.gpu_cross:
+        # every cross field built on the GPU from a (user field, ad field) pair
+        cfg = synth.config(cfg.name, cross_pairs=tuple(
+            (f % cfg.n_user, f % cfg.n_ad) for f in range(cfg.n_cross)))
     log(f"workload {cfg.name}: {cfg.n_requests} x {cfg.cand_per_request} rows, "
         f"{cfg.n_groups} groups, vocab {cfg.vocab}, {cfg.dtype}")
     t0 = time.perf_counter()
@@ -592,7 +609,9 @@ def main():
         "config": {"workload": cfg.name, "requests": cfg.n_requests,
                    "candidates_per_request": cfg.cand_per_request, "rows": R,
                    "groups": cfg.n_groups, "emb_dim": cfg.emb_dim, "vocab": cfg.vocab,
-                   "widths": list(cfg.widths), "parallelism": "none (1 GPU)"},
+                   "widths": list(cfg.widths), "parallelism": "none (1 GPU)",
+                   "cross_features": "built on the GPU from user/ad id pairs" if cfg.cross_pairs
+                   else "ids given per row"},
         "p50_latency_ms": None if p50 is None else round(p50, 4),
         "p99_latency_ms": None if p99 is None else round(p99, 4),
         "p50_latency_graph_ms": None if g50 is None else round(g50, 4),

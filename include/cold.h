@@ -84,7 +84,20 @@ typedef struct cold_model_desc {
   const int64_t *table_rows;/* host [M], rows of each table, 1 .. 2^31-1 */
   int32_t linear_log;       /* 0/1: apply Eq. 3 to the network input */
   int32_t topk_k;           /* 0: off; else keep the k most important groups per request */
+  const int32_t *cross_pairs; /* host [n_cross][2] or NULL: see below */
 } cold_model_desc;
+
+/* User x ad cross features built on the GPU (desc.cross_pairs != NULL).
+ * The paper builds its cross features on the CPU next to the other feature
+ * computation (Section 3.3) and does not say how a cross value is formed.
+ * Here cross field f pairs user field u = cross_pairs[2f] (0 <= u < n_user)
+ * with ad field a = cross_pairs[2f+1] (0 <= a < n_ad): with uid and aid the
+ * two fields' raw ids (int32 ids zero-extended from their 32-bit pattern, or
+ * the uint64 raw ids of a hashed model), the pair's key is
+ *     key = mix64(uid) ^ aid
+ * and its table row is mix64(key ^ salt_g) mod rows with the group salt of
+ * the hashed id kind (group g = n_user + n_seq + n_ad + f), for either id
+ * kind.  cold_batch.cross_ids is then not read and may be NULL. */
 
 typedef struct cold_model cold_model;
 

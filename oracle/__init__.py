@@ -49,6 +49,7 @@ class _Problem(ctypes.Structure):
         ("ad_ids", ctypes.c_void_p), ("cross_ids", ctypes.c_void_p),
         ("seq_off", ctypes.c_void_p), ("seq_ids", ctypes.c_void_p),
         ("n_seq_ids", ctypes.c_int64),
+        ("cross_pairs", ctypes.c_void_p),
     ]
 
 
@@ -72,6 +73,8 @@ def lib():
         L.orc_mix64.argtypes = [ctypes.c_uint64]
         L.orc_hash_row.restype = ctypes.c_uint64
         L.orc_hash_row.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint64]
+        L.orc_cross_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.orc_cross_key.restype = ctypes.c_uint64
         _lib = L
     return _lib
 
@@ -99,12 +102,19 @@ def hash_row(raw: int, g: int, rows: int) -> int:
     return int(lib().orc_hash_row(raw & 0xFFFFFFFFFFFFFFFF, g, rows))
 
 
+def cross_key(user_id: int, ad_id: int) -> int:
+    """64-bit key of a user x ad cross value (see orc_cross_key)."""
+    return int(lib().orc_cross_key(user_id & 0xFFFFFFFFFFFFFFFF, ad_id & 0xFFFFFFFFFFFFFFFF))
+
+
 def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
           want_rows=False, want_s=False, want_x=False, n_threads=None) -> dict:
     """Score rows of a batch.
 
     dims: n_user, n_seq, n_ad, n_cross, emb_dim, se_hidden, dtype ('f32' |
-      'bf16' | 'f16'), hashed, linear_log, topk_k, widths.
+      'bf16' | 'f16'), hashed, linear_log, topk_k, widths, and optionally
+      cross_pairs ([n_cross][2] user field, ad field: cross ids are then
+      built from the pairs and batch['cross_ids'] is not read).
     tables: list of M arrays [rows][d] in stored form (float32, float16, or
       uint16 bf16 bit patterns).
     params: se_w1 [H][M], se_b1, se_w2 [M][H], se_b2 (float32); mlp_w list of
@@ -151,7 +161,12 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
     se_b2 = arr(params["se_b2"], np.float32)
     user_ids = arr(np.asarray(batch["user_ids"]).reshape(dims["n_user"], q), id_dt)
     ad_ids = arr(np.asarray(batch["ad_ids"]).reshape(dims["n_ad"], r), id_dt)
-    cross_ids = arr(np.asarray(batch["cross_ids"]).reshape(dims["n_cross"], r), id_dt)
+    pairs = dims.get("cross_pairs") or None
+    cross_pairs = None if pairs is None else arr(np.asarray(pairs).reshape(-1), np.int32)
+    if pairs is None:
+        cross_ids = arr(np.asarray(batch["cross_ids"]).reshape(dims["n_cross"], r), id_dt)
+    else:
+        cross_ids = None      # built from the user/ad id pairs
     seq_off = arr(batch.get("seq_off", np.zeros(1, np.int32)), np.int32)
     seq_ids = arr(batch.get("seq_ids", np.zeros(0, id_dt)), id_dt)
     if seq_ids.size == 0:
@@ -168,7 +183,8 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
         tables=_ptr(table_ptrs), se_w1=_ptr(se_w1), se_b1=_ptr(se_b1), se_w2=_ptr(se_w2),
         se_b2=_ptr(se_b2), mlp_w=_ptr(w_ptrs), mlp_b=_ptr(b_ptrs), req_off=_ptr(req_off),
         user_ids=_ptr(user_ids), ad_ids=_ptr(ad_ids), cross_ids=_ptr(cross_ids),
-        seq_off=_ptr(seq_off), seq_ids=_ptr(seq_ids), n_seq_ids=n_seq_ids)
+        seq_off=_ptr(seq_off), seq_ids=_ptr(seq_ids), n_seq_ids=n_seq_ids,
+        cross_pairs=_ptr(cross_pairs))
     sample = arr(np.arange(r) if sample is None else sample, np.int64)
     n = sample.size
     out = {"scores": np.zeros(n, np.float64)}

@@ -69,6 +69,8 @@ typedef struct {
   const int32_t *seq_off;         /* [n_seq * Q + 1], entry f*Q + q */
   const void *seq_ids;            /* [n_seq_ids] */
   int64_t n_seq_ids;
+  const int32_t *cross_pairs;     /* [n_cross][2] (user field, ad field), or NULL:
+                                     cross ids are then read from cross_ids */
 } orc_problem;
 
 /* ---------------------------------------------------------------- dtypes */
@@ -118,6 +120,20 @@ uint64_t orc_mix64(uint64_t z) {
 uint64_t orc_hash_row(uint64_t raw, int32_t g, uint64_t rows) {
   uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ULL;
   return orc_mix64(raw ^ salt) % rows;
+}
+
+/* A user x ad cross feature formed from the raw ids of one user field and
+ * one ad field (the paper forms its cross features on the CPU and does not
+ * say how; this is the reading used throughout): the pair's 64-bit key is
+ * mix64(user id) XOR ad id, with 32-bit ids taken as unsigned, and the key
+ * is hashed into the cross group's table like a raw id (orc_hash_row). */
+uint64_t orc_cross_key(uint64_t user_id, uint64_t ad_id) {
+  return orc_mix64(user_id) ^ ad_id;
+}
+
+static uint64_t raw_id(const orc_problem *p, const void *ids, int64_t i) {
+  if (p->hashed) return ((const uint64_t *)ids)[i];
+  return (uint64_t)(uint32_t)((const int32_t *)ids)[i];
 }
 
 /* row of group g for an id stored at element i of column array `ids`;
@@ -182,7 +198,14 @@ static int row_embeddings(const orc_problem *p, int64_t r, int64_t q, double *e,
       e[g * d + k] = load_stored(p->dtype, p->tables[g], row * d + k);
   }
   for (int32_t f = 0; f < p->n_cross; ++f, ++g) {
-    int64_t row = resolve(p, p->cross_ids, (int64_t)f * R + r, g);
+    int64_t row;
+    if (p->cross_pairs) {
+      uint64_t key = orc_cross_key(raw_id(p, p->user_ids, (int64_t)p->cross_pairs[2 * f] * Q + q),
+                                   raw_id(p, p->ad_ids, (int64_t)p->cross_pairs[2 * f + 1] * R + r));
+      row = (int64_t)orc_hash_row(key, g, (uint64_t)p->table_rows[g]);
+    } else {
+      row = resolve(p, p->cross_ids, (int64_t)f * R + r, g);
+    }
     if (row < 0) return ORC_ID_RANGE;
     rows_out[g] = row;
     for (int k = 0; k < d; ++k)

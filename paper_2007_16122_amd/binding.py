@@ -50,7 +50,8 @@ class cold_model_desc(ctypes.Structure):
                 ("n_layers", ctypes.c_int32),
                 ("widths", ctypes.POINTER(ctypes.c_int32)),
                 ("table_rows", ctypes.POINTER(ctypes.c_int64)),
-                ("linear_log", ctypes.c_int32), ("topk_k", ctypes.c_int32)]
+                ("linear_log", ctypes.c_int32), ("topk_k", ctypes.c_int32),
+                ("cross_pairs", ctypes.POINTER(ctypes.c_int32))]
 
 
 class cold_weights(ctypes.Structure):
@@ -189,18 +190,22 @@ def select_topn(scores, bids, req_off, n_top: int, with_ecpm: bool = True):
 
 def make_desc(n_user, n_seq, n_ad, n_cross, emb_dim, dtype, se_reduction,
               widths: Sequence[int], table_rows: Sequence[int], hashed=False,
-              linear_log=False, topk_k=0):
-    """A cold_model_desc plus the arrays it points to (keep both alive)."""
+              linear_log=False, topk_k=0, cross_pairs=None):
+    """A cold_model_desc plus the arrays it points to (keep both alive).
+    cross_pairs: None, or (user field, ad field) per cross field."""
     w = (ctypes.c_int32 * len(widths))(*widths)
     r = (ctypes.c_int64 * len(table_rows))(*table_rows)
+    flat = [v for pr in (cross_pairs or ()) for v in pr]
+    cp = (ctypes.c_int32 * len(flat))(*flat) if flat else None
     d = cold_model_desc(n_user=n_user, n_seq=n_seq, n_ad=n_ad, n_cross=n_cross,
                         emb_dim=emb_dim,
                         id_kind=COLD_IDS_HASHED_U64 if hashed else COLD_IDS_DIRECT_I32,
                         dtype=DTYPES[dtype] if isinstance(dtype, str) else dtype,
                         se_reduction=se_reduction, n_layers=len(widths) - 1,
                         widths=w, table_rows=r, linear_log=int(bool(linear_log)),
-                        topk_k=topk_k)
-    return d, (w, r)
+                        topk_k=topk_k,
+                        cross_pairs=ctypes.cast(cp, ctypes.POINTER(ctypes.c_int32)) if cp else None)
+    return d, (w, r, cp)
 
 
 # ---------------------------------------------------------------- wrapper
@@ -220,7 +225,8 @@ class ColdModel:
         self.desc, self._desc_keep = make_desc(
             cfg.n_user, cfg.n_seq, cfg.n_ad, cfg.n_cross, cfg.emb_dim, cfg.dtype,
             cfg.se_reduction, cfg.widths, [cfg.vocab] * cfg.n_groups, hashed=cfg.hashed,
-            linear_log=cfg.linear_log, topk_k=cfg.topk_k)
+            linear_log=cfg.linear_log, topk_k=cfg.topk_k,
+            cross_pairs=getattr(cfg, "cross_pairs", None) or None)
         self.h = cold_create_model(self.desc)
         self.arena = torch.empty(cold_weight_arena_bytes(self.h), dtype=torch.uint8,
                                  device=self.device)

@@ -19,7 +19,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct ArenaLayout {
-  size_t tables, rows, magic, w1, b1, w2, b2;
+  size_t tables, rows, magic, pairs, w1, b1, w2, b2;
   std::vector<size_t> w, b;
   size_t total;
 };
@@ -39,6 +39,7 @@ struct cold_model {
   cold_model_desc desc;
   std::vector<int32_t> widths;
   std::vector<int64_t> table_rows;
+  std::vector<int32_t> cross_pairs;   // [n_cross][2] or empty
   int M, D_in, H, d, dtype, es, nus, hashed;
   int max_hidden;
   ArenaLayout arena;
@@ -80,6 +81,7 @@ ArenaLayout arena_layout(const cold_model &m) {
   a.tables = take(sizeof(uint64_t) * m.M);
   a.rows = take(sizeof(int64_t) * m.M);
   a.magic = take(sizeof(uint64_t) * m.M);
+  a.pairs = take(sizeof(int32_t) * m.cross_pairs.size());
   a.w1 = take(sizeof(float) * m.H * m.M);
   a.b1 = take(sizeof(float) * m.H);
   a.w2 = take(sizeof(float) * m.M * m.H);
@@ -197,14 +199,21 @@ int cold_create_model(const cold_model_desc *desc, cold_model **out) {
   if ((size_t)n_out * last_in * sizeof(float) > 64 * 1024) return COLD_ERR_SHAPE;
   for (int g = 0; g < M; ++g)
     if (D.table_rows[g] < 1 || D.table_rows[g] > 0x7FFFFFFF) return COLD_ERR_SHAPE;
+  if (D.cross_pairs)
+    for (int f = 0; f < D.n_cross; ++f)
+      if (D.cross_pairs[2 * f] < 0 || D.cross_pairs[2 * f] >= D.n_user ||
+          D.cross_pairs[2 * f + 1] < 0 || D.cross_pairs[2 * f + 1] >= D.n_ad)
+        return COLD_ERR_SHAPE;
 
   cold_model *m = new (std::nothrow) cold_model();
   if (!m) return COLD_ERR_INVALID_ARG;
   m->desc = D;
   m->widths.assign(D.widths, D.widths + D.n_layers + 1);
   m->table_rows.assign(D.table_rows, D.table_rows + M);
+  if (D.cross_pairs && D.n_cross > 0) m->cross_pairs.assign(D.cross_pairs, D.cross_pairs + 2 * D.n_cross);
   m->desc.widths = m->widths.data();
   m->desc.table_rows = m->table_rows.data();
+  m->desc.cross_pairs = m->cross_pairs.empty() ? nullptr : m->cross_pairs.data();
   m->M = M;
   m->d = D.emb_dim;
   m->D_in = M * D.emb_dim;
@@ -306,6 +315,7 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
       {al.tables, m->host_tables.data(), sizeof(uint64_t) * m->M, hipMemcpyHostToDevice},
       {al.rows, m->table_rows.data(), sizeof(int64_t) * m->M, hipMemcpyHostToDevice},
       {al.magic, m->host_magic.data(), sizeof(uint64_t) * m->M, hipMemcpyHostToDevice},
+      {al.pairs, m->cross_pairs.data(), sizeof(int32_t) * m->cross_pairs.size(), hipMemcpyHostToDevice},
       {al.w1, w->se_w1, sizeof(float) * m->H * m->M, hipMemcpyDeviceToDevice},
       {al.b1, w->se_b1, sizeof(float) * m->H, hipMemcpyDeviceToDevice},
       {al.w2, w->se_w2, sizeof(float) * m->M * m->H, hipMemcpyDeviceToDevice},
@@ -316,6 +326,7 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
     copies.push_back({al.b[l], w->mlp_b[l], sizeof(float) * m->widths[l + 1], hipMemcpyDeviceToDevice});
   }
   for (const Copy &c : copies) {
+    if (c.bytes == 0) continue;
     hipError_t e = hipMemcpyAsync(A + c.off, c.src, c.bytes, c.kind, s);
     if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: copy");
   }
@@ -341,7 +352,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   const cold_model_desc &D = m->desc;
   if (!b->req_off || !scores || !workspace ||
       (D.n_user > 0 && !b->user_ids) || (D.n_ad > 0 && !b->ad_ids) ||
-      (D.n_cross > 0 && !b->cross_ids) || (D.n_seq > 0 && !b->seq_off) ||
+      (D.n_cross > 0 && !D.cross_pairs && !b->cross_ids) || (D.n_seq > 0 && !b->seq_off) ||
       (D.n_seq > 0 && b->n_seq_ids > 0 && !b->seq_ids))
     return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null pointer");
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
@@ -365,6 +376,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   g.tables = reinterpret_cast<const void *const *>(A + al.tables);
   g.table_rows = reinterpret_cast<const int64_t *>(A + al.rows);
   g.table_magic = reinterpret_cast<const uint64_t *>(A + al.magic);
+  g.cross_pairs = D.cross_pairs ? reinterpret_cast<const int32_t *>(A + al.pairs) : nullptr;
   g.w1 = reinterpret_cast<const float *>(A + al.w1);
   g.b1 = reinterpret_cast<const float *>(A + al.b1);
   g.w2 = reinterpret_cast<const float *>(A + al.w2);

@@ -150,6 +150,7 @@ struct GatherArgs {
   const void *const *tables;      // device [M]
   const int64_t *table_rows;      // device [M]
   const uint64_t *table_magic;    // device [M]
+  const int32_t *cross_pairs;     // device [n_cross][2] (user field, ad field) or null
   const float *w1, *b1, *w2, *b2; // SE parameters
   float *U;                       // [Q][n_user+n_seq][d] pooled user side
   float *zU;                      // [Q][n_user+n_seq] squeeze of the user groups

@@ -136,12 +136,17 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   uint64_t *s_tab = reinterpret_cast<uint64_t *>(cursor);   // [M] table base addresses
   uint64_t *s_magic = s_tab + M;                           // [M] Barrett constants
   int32_t *s_rows = reinterpret_cast<int32_t *>(s_magic + M);  // [M] table rows
+  int32_t *s_pair = s_rows + M;   // [n_cross] user field | ad field << 16 (GPU cross features)
   cursor += a.meta_lds_bytes;
   for (int g = threadIdx.x; g < M; g += kGatherThreads) {
     s_tab[g] = reinterpret_cast<uint64_t>(a.tables[g]);
     s_magic[g] = a.table_magic[g];
     s_rows[g] = (int32_t)a.table_rows[g];
   }
+  const bool gpu_cross = a.cross_pairs != nullptr;
+  if (gpu_cross)
+    for (int f = threadIdx.x; f < a.n_cross; f += kGatherThreads)
+      s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
   // request offsets in LDS when they fit: the row -> request search then
   // costs LDS latency, not a chain of dependent global loads
   int32_t *s_req = reinterpret_cast<int32_t *>(cursor);   // [Q+1] if req_in_lds
@@ -198,8 +203,10 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       const int64_t r = r0 + t;
       if (r < R) {
         const bool is_ad = f < a.n_ad;
-        const id_t *ids = static_cast<const id_t *>(is_ad ? a.ad_ids : a.cross_ids);
-        idv[k] = ids[(int64_t)(is_ad ? f : f - a.n_ad) * R + r];
+        // a cross field built on the GPU starts from its ad field's id
+        const int fa = is_ad ? f : (gpu_cross ? s_pair[f - a.n_ad] >> 16 : f - a.n_ad);
+        const id_t *ids = static_cast<const id_t *>(is_ad || gpu_cross ? a.ad_ids : a.cross_ids);
+        idv[k] = ids[(int64_t)fa * R + r];
       }
     }
   }
@@ -222,7 +229,22 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       if (r < R) {
         bool keep = true;
         if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
-        if constexpr (HASHED) {
+        if (gpu_cross && f >= a.n_ad) {
+          // user x ad cross value: key = mix64(user id) ^ ad id, hashed into
+          // the group's table (ids as their unsigned bit patterns)
+          const int fu = s_pair[f - a.n_ad] & 0xFFFF;
+          const id_t *uids = static_cast<const id_t *>(a.user_ids);
+          uint64_t uid, aid;
+          if constexpr (HASHED) {
+            uid = (uint64_t)uids[(int64_t)fu * Q + rq[t]];
+            aid = (uint64_t)idv[k];
+          } else {
+            uid = (uint64_t)(uint32_t)uids[(int64_t)fu * Q + rq[t]];
+            aid = (uint64_t)(uint32_t)idv[k];
+          }
+          const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+          row = (int32_t)mod_barrett(mix64((mix64(uid) ^ aid) ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+        } else if constexpr (HASHED) {
           const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
           row = (int32_t)mod_barrett(mix64((uint64_t)idv[k] ^ salt), (uint64_t)s_rows[g], s_magic[g]);
         } else {
@@ -484,7 +506,7 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * a.n_seq * a.d +
                                 sizeof(int32_t) * (size_t)(T * nax + T) +
                                 sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
-  a.meta_lds_bytes = (int32_t)((20 * (size_t)a.M + 15) / 16 * 16);
+  a.meta_lds_bytes = (int32_t)((24 * (size_t)a.M + 15) / 16 * 16);
   a.req_lds_bytes = a.Q + 1 <= kGatherMaxReqLds ? (int32_t)((4 * (a.Q + 1) + 15) / 16 * 16) : 0;
   const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
   a.se_in_lds = MODE != kApplyWeights && se_floats * sizeof(float) <= 24 * 1024;

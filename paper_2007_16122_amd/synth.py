@@ -70,6 +70,9 @@ class ColdConfig:
     out_gain: float = 6.0      # output-layer scale relative to He init ("he" init)
     out_bias: float = -2.0     # output-layer bias of the click class ("he" init)
     seed: int = 2007_16122
+    # () : cross ids come with the batch; else ((user field, ad field), ...)
+    # per cross field, and the cross ids are built on the GPU from the pair
+    cross_pairs: tuple = ()
 
     @property
     def n_groups(self) -> int:
@@ -275,10 +278,13 @@ def make_batch(cfg: ColdConfig, seed: Optional[int] = None,
     for f in range(cfg.n_ad):
         ad_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows, device)
         g += 1
-    cross_ids = np.zeros((cfg.n_cross, n_rows), dtype=id_dtype)
-    for f in range(cfg.n_cross):
-        cross_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows, device)
-        g += 1
+    if cfg.cross_pairs:      # built from the user and ad ids by the scorer
+        cross_ids = np.zeros((cfg.n_cross, 0), dtype=id_dtype)
+    else:
+        cross_ids = np.zeros((cfg.n_cross, n_rows), dtype=id_dtype)
+        for f in range(cfg.n_cross):
+            cross_ids[f] = _ids_for_field(rngs[4 + g], cfg, n_rows, device)
+            g += 1
     return dict(req_off=req_off, user_ids=user_ids, ad_ids=ad_ids,
                 cross_ids=cross_ids, seq_off=seq_off, seq_ids=seq_ids,
                 n_requests=q_count, n_rows=n_rows)

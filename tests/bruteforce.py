@@ -70,12 +70,27 @@ def forward(dims, tables_f64, se, mlp_w_f64, mlp_b, batch):
                 per_req[q, rr] += 1.0
         blocks.append((member.T @ per_req) @ tables_f64[g])
         rows_cols.append(np.full(r_n, -1, np.int64))
+    pairs = dims.get("cross_pairs") or None
+    ad_all = np.asarray(batch["ad_ids"]).reshape(na, r_n)
     for name, count_f, base in (("ad_ids", na, nu + ns), ("cross_ids", nx, nu + ns + na)):
-        ids = np.asarray(batch[name]).reshape(count_f, r_n)
+        if name == "cross_ids" and pairs:
+            ids = None
+        else:
+            ids = np.asarray(batch[name]).reshape(count_f, r_n)
         for f in range(count_f):
             g = base + f
             v = tables_f64[g].shape[0]
-            rr = _row_of(ids[f], g, v, hashed)
+            if ids is None:
+                # cross value from a user field and an ad field:
+                # key = mix64(user id) ^ ad id on unsigned integers, then hashed
+                uf, af = pairs[f]
+                width = 64 if hashed else 32
+                unsigned = lambda x: int(x) & ((1 << width) - 1)
+                rr = np.array([hashed_row(mix64_int(unsigned(user_ids[uf][req_of_row[i]]))
+                                          ^ unsigned(ad_all[af][i]), g, v)
+                               for i in range(r_n)], np.int64)
+            else:
+                rr = _row_of(ids[f], g, v, hashed)
             onehot = np.zeros((r_n, v))
             onehot[np.arange(r_n), rr] = 1.0
             blocks.append(onehot @ tables_f64[g])

@@ -66,6 +66,10 @@ def create_status(**kw):
     (dict(widths=[768, 1020, 2]), B.COLD_ERR_DTYPE),  # half hidden width % 8
     (dict(table_rows=[0] + [1000] * 47), B.COLD_ERR_SHAPE),
     (dict(table_rows=[2**31] + [1000] * 47), B.COLD_ERR_SHAPE),
+    (dict(cross_pairs=[(f, f) for f in range(12)]), B.COLD_OK),
+    (dict(cross_pairs=[(12, 0)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),   # user field >= n_user
+    (dict(cross_pairs=[(0, 24)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),   # ad field >= n_ad
+    (dict(cross_pairs=[(-1, 0)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),
 ])
 def test_create_model_validation(kw, status):
     assert create_status(**kw) == status

@@ -81,6 +81,25 @@ def test_parity_mid(name):
     assert len(req_of_row) == batch["n_rows"]
 
 
+@pytest.mark.parametrize("name", ["serving_bf16", "large_fp16_ll"])
+def test_parity_gpu_cross_features(name):
+    """Cross ids built on the GPU from (user field, ad field) pairs, direct
+    and hashed id kinds: gather indices bit-exact, scores within tolerance."""
+    base = synth.CONFIGS[name]
+    pairs = tuple((f % base.n_user, (5 * f + 2) % base.n_ad) for f in range(base.n_cross))
+    cfg = mid(name, cross_pairs=pairs)
+    log(f"test_parity_gpu_cross_features {name}")
+    tables, params, batch = problem(cfg, seed=23, cand=MID_CANDS[name])
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True)
+    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
+    compare_scores(cfg, g["scores"], o["scores"], f"gpu cross {name}")
+
+
 @pytest.mark.parametrize("name", CONFIG_NAMES)
 def test_parity_full_size_sampled(name):
     """The full workload in the launch configuration the bench times; the

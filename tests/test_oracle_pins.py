@@ -86,6 +86,34 @@ def test_hash_row_matches_integer_definition():
         assert oracle.hash_row(raw, g, rows) == bruteforce.hashed_row(raw, g, rows)
 
 
+def test_cross_key_matches_integer_definition():
+    rng = np.random.default_rng(6)
+    for _ in range(200):
+        u = int(rng.integers(0, 2**63)) * 2 + int(rng.integers(0, 2))
+        a = int(rng.integers(0, 2**63)) * 2 + int(rng.integers(0, 2))
+        assert oracle.cross_key(u, a) == bruteforce.mix64_int(u) ^ a
+    # the mixing function fixes 0, so a zero user id leaves the ad id as is
+    assert oracle.cross_key(0, 12345) == 12345
+
+
+@pytest.mark.parametrize("name,hashed", [("serving_bf16", False), ("large_fp16_ll", True)])
+def test_oracle_gpu_cross_features_match_bruteforce(name, hashed):
+    """Cross ids built from (user field, ad field) pairs: rows and scores
+    against the dense formulation, which derives the rows with Python
+    integers."""
+    base = tiny(name)
+    pairs = tuple((f % base.n_user, (3 * f + 1) % base.n_ad) for f in range(base.n_cross))
+    cfg = tiny(name, cross_pairs=pairs)
+    assert cfg.hashed == hashed
+    tables, params, batch = problem(cfg, seed=12, cand=[5, 0, 7])
+    assert batch["cross_ids"].shape[1] == 0
+    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_x=True)
+    b = run_brute(cfg, tables, params, batch)
+    assert np.array_equal(o["rows"], b["rows"])
+    np.testing.assert_allclose(o["x"], b["x"], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(o["scores"], b["scores"], rtol=1e-11, atol=1e-13)
+
+
 # ----------------------------------------- whole path vs dense formulation
 @pytest.mark.parametrize("name", CONFIG_NAMES)
 def test_oracle_matches_bruteforce(name):
