@@ -50,6 +50,7 @@ class _Problem(ctypes.Structure):
         ("seq_off", ctypes.c_void_p), ("seq_ids", ctypes.c_void_p),
         ("n_seq_ids", ctypes.c_int64),
         ("cross_pairs", ctypes.c_void_p),
+        ("se_form", ctypes.c_int32),
     ]
 
 
@@ -114,7 +115,9 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
     dims: n_user, n_seq, n_ad, n_cross, emb_dim, se_hidden, dtype ('f32' |
       'bf16' | 'f16'), hashed, linear_log, topk_k, widths, and optionally
       cross_pairs ([n_cross][2] user field, ad field: cross ids are then
-      built from the pairs and batch['cross_ids'] is not read).
+      built from the pairs and batch['cross_ids'] is not read) and se_form
+      (0: squeeze/excitation SE; 1: one FC over the concatenated embeddings,
+      se_w1 [M][M*d], se_b1 [M], se_w2/se_b2 unused).
     tables: list of M arrays [rows][d] in stored form (float32, float16, or
       uint16 bf16 bit patterns).
     params: se_w1 [H][M], se_b1, se_w2 [M][H], se_b2 (float32); mlp_w list of
@@ -184,7 +187,7 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
         se_b2=_ptr(se_b2), mlp_w=_ptr(w_ptrs), mlp_b=_ptr(b_ptrs), req_off=_ptr(req_off),
         user_ids=_ptr(user_ids), ad_ids=_ptr(ad_ids), cross_ids=_ptr(cross_ids),
         seq_off=_ptr(seq_off), seq_ids=_ptr(seq_ids), n_seq_ids=n_seq_ids,
-        cross_pairs=_ptr(cross_pairs))
+        cross_pairs=_ptr(cross_pairs), se_form=int(dims.get("se_form", 0)))
     sample = arr(np.arange(r) if sample is None else sample, np.int64)
     n = sample.size
     out = {"scores": np.zeros(n, np.float64)}

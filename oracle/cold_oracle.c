@@ -71,6 +71,9 @@ typedef struct {
   int64_t n_seq_ids;
   const int32_t *cross_pairs;     /* [n_cross][2] (user field, ad field), or NULL:
                                      cross ids are then read from cross_ids */
+  int32_t se_form;                /* 0: squeeze -> FC -> ReLU -> FC -> sigmoid;
+                                     1: one FC over the concatenated embeddings,
+                                        se_w1 [M][M*d], se_b1 [M] (Eq. 2 as printed) */
 } orc_problem;
 
 /* ---------------------------------------------------------------- dtypes */
@@ -220,6 +223,17 @@ static void se_weights(const orc_problem *p, const double *e, double *z, double 
                        double *s) {
   const int d = p->emb_dim, H = p->se_hidden;
   const int M = p->n_user + p->n_seq + p->n_ad + p->n_cross;
+  if (p->se_form == 1) {
+    /* Eq. 2 as printed: s = sigmoid(W [e_1, ..., e_M] + b), one fully
+     * connected layer from the whole concatenated embedding to M weights */
+    const int64_t D = (int64_t)M * d;
+    for (int g = 0; g < M; ++g) {
+      double acc = (double)p->se_b1[g];
+      for (int64_t j = 0; j < D; ++j) acc += (double)p->se_w1[(int64_t)g * D + j] * e[j];
+      s[g] = sigmoid(acc);
+    }
+    return;
+  }
   for (int g = 0; g < M; ++g) {
     double acc = 0.0;
     for (int k = 0; k < d; ++k) acc += e[g * d + k];

@@ -73,6 +73,9 @@ class ColdConfig:
     # () : cross ids come with the batch; else ((user field, ad field), ...)
     # per cross field, and the cross ids are built on the GPU from the pair
     cross_pairs: tuple = ()
+    # "squeeze": SE as squeeze -> FC -> ReLU -> FC -> sigmoid; "literal": one
+    # FC from the concatenated embeddings to the M weights (Eq. 2 as printed)
+    se_form: str = "squeeze"
 
     @property
     def n_groups(self) -> int:
@@ -423,6 +426,14 @@ def make_params(cfg: ColdConfig, seed: Optional[int] = None) -> dict:
         se_b1 = rng.normal(0, 0.1, h).astype(f32)
         se_w2 = rng.normal(0, 1.0 / math.sqrt(h), (m, h)).astype(f32)
         se_b2 = rng.normal(0, 1.0, m).astype(f32)
+    if cfg.se_form == "literal":
+        # se_w1 [M][D_in], se_b1 [M]; drawn from a stream of their own so the
+        # network weights are those of the squeeze form of the same workload
+        lrng = np.random.default_rng(np.random.SeedSequence([seed, 0x5E, 0x1E]))
+        se_w1 = lrng.normal(0, 30.0 / math.sqrt(cfg.d_in), (m, cfg.d_in)).astype(f32)
+        se_b1 = lrng.normal(0, 0.5, m).astype(f32)
+        se_w2 = np.zeros((m, 0), f32)
+        se_b2 = np.zeros(0, f32)
     ws, bs = [], []
     n_layers = len(cfg.widths) - 1
     for li in range(n_layers):

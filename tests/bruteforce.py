@@ -97,9 +97,13 @@ def forward(dims, tables_f64, se, mlp_w_f64, mlp_b, batch):
             rows_cols.append(rr)
     e = np.concatenate(blocks, axis=1)                     # [R][M*d]
     avg = np.kron(np.eye(m), np.full((d, 1), 1.0 / d))     # [M*d][M]
-    z = e @ avg
-    h = np.maximum(z @ se["se_w1"].astype(np.float64).T + se["se_b1"], 0.0)
-    s = 1.0 / (1.0 + np.exp(-(h @ se["se_w2"].astype(np.float64).T + se["se_b2"])))
+    if int(dims.get("se_form", 0)) == 1:
+        # Eq. 2 as printed: one dense layer from the concatenation to M logits
+        s = 1.0 / (1.0 + np.exp(-(e @ se["se_w1"].astype(np.float64).T + se["se_b1"])))
+    else:
+        z = e @ avg
+        h = np.maximum(z @ se["se_w1"].astype(np.float64).T + se["se_b1"], 0.0)
+        s = 1.0 / (1.0 + np.exp(-(h @ se["se_w2"].astype(np.float64).T + se["se_b2"])))
     k = int(dims.get("topk_k", 0))
     importance = mask = None
     keep = np.ones_like(s)

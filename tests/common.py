@@ -13,7 +13,8 @@ def dims_of(cfg: synth.ColdConfig) -> dict:
     return dict(n_user=cfg.n_user, n_seq=cfg.n_seq, n_ad=cfg.n_ad, n_cross=cfg.n_cross,
                 emb_dim=cfg.emb_dim, se_hidden=cfg.se_hidden, dtype=cfg.dtype,
                 hashed=cfg.hashed, linear_log=cfg.linear_log, topk_k=cfg.topk_k,
-                widths=list(cfg.widths), cross_pairs=[list(p) for p in cfg.cross_pairs])
+                widths=list(cfg.widths), cross_pairs=[list(p) for p in cfg.cross_pairs],
+                se_form=1 if cfg.se_form == "literal" else 0)
 
 
 def tiny(name: str, **kw) -> synth.ColdConfig:

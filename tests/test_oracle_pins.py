@@ -114,6 +114,43 @@ def test_oracle_gpu_cross_features_match_bruteforce(name, hashed):
     np.testing.assert_allclose(o["scores"], b["scores"], rtol=1e-11, atol=1e-13)
 
 
+@pytest.mark.parametrize("name", ["tiny_fp32", "serving_bf16", "multivalued_fp16_ll",
+                                  "wide_prune_bf16"])
+def test_oracle_literal_se_matches_bruteforce(name):
+    """Eq. 2 as printed (one FC over the concatenated embeddings): importance
+    weights, network input and scores against the dense formulation."""
+    cfg = tiny(name, se_form="literal")
+    tables, params, batch = problem(cfg, seed=13, cand=[4, 0, 9])
+    assert params["se_w1"].shape == (cfg.n_groups, cfg.d_in)
+    o = run_oracle(cfg, tables, params, batch, want_s=True, want_x=True)
+    b = run_brute(cfg, tables, params, batch)
+    np.testing.assert_allclose(o["s"], b["s"], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(o["x"], b["x"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(o["scores"], b["scores"], rtol=1e-11, atol=1e-13)
+    if cfg.topk_k:
+        assert np.array_equal(o["mask"], b["mask"])
+
+
+def test_literal_se_closed_forms():
+    """W = 0 gives s = sigmoid(b) for every row; a W that averages each
+    group's own block gives s_g = sigmoid(z_g + b_g), z_g the group mean."""
+    cfg = tiny("serving_bf16", se_form="literal")
+    tables, params, batch = problem(cfg, seed=14)
+    m, d = cfg.n_groups, cfg.emb_dim
+    p0 = dict(params, se_w1=np.zeros_like(params["se_w1"]))
+    o = run_oracle(cfg, tables, p0, batch, want_s=True)
+    want = 1.0 / (1.0 + np.exp(-params["se_b1"].astype(np.float64)))
+    np.testing.assert_allclose(o["s"], np.broadcast_to(want, o["s"].shape), rtol=0, atol=1e-15)
+    wavg = np.zeros((m, m * d), np.float32)
+    for g in range(m):
+        wavg[g, g * d:(g + 1) * d] = 1.0 / d          # exact in fp32 (d a power of two)
+    o = run_oracle(cfg, tables, dict(params, se_w1=wavg), batch, want_s=True, want_x=True)
+    s = o["s"]
+    e = o["x"].reshape(-1, m, d) / s[:, :, None]       # x = s * e
+    z = e.mean(axis=2)
+    np.testing.assert_allclose(s, 1.0 / (1.0 + np.exp(-(z + params["se_b1"]))), rtol=1e-12)
+
+
 # ----------------------------------------- whole path vs dense formulation
 @pytest.mark.parametrize("name", CONFIG_NAMES)
 def test_oracle_matches_bruteforce(name):
