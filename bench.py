@@ -17,6 +17,7 @@ sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -54,6 +55,11 @@ def stage_work(cfg, batch, stage):
         # ids + gathered ad/cross rows + network input written + pooled user rows
         out = R * cfg.d_in * es if stage != "se_weights" else R * m * 4
         return "hbm", R * nax * (idb + d * es) + out + Q * nus * d * 4
+    if stage == "gather_raw":
+        # ids + gathered ad/cross rows + the fp32 concatenated embedding written
+        return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * 4 + Q * nus * d * 4
+    if stage == "se_dense":
+        return "mfma_f32", 2.0 * R * cfg.d_in * m
     if stage.startswith("dense"):
         li = int(stage[5:])
         return "mfma", 2.0 * R * cfg.widths[li] * cfg.widths[li + 1]
@@ -70,9 +76,9 @@ def stage_work(cfg, batch, stage):
 
 def roofline_entry(cfg, batch, stage, ms):
     kind, work = stage_work(cfg, batch, stage)
-    if kind == "mfma":
+    if kind in ("mfma", "mfma_f32"):
         ach = work / (ms * 1e-3) / 1e12
-        peak = PEAK_MFMA_TFLOPS[cfg.dtype]
+        peak = PEAK_MFMA_TFLOPS["f32" if kind == "mfma_f32" else cfg.dtype]
         return {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4), "work_per_launch": work}
     ach = work / (ms * 1e-3) / 1e9
@@ -202,6 +208,43 @@ def serving_curve(model, batch, cfg, streams, iters, torch, binding):
         log(f"serving {k:2d} streams: {out[-1]['requests_per_s']:9.1f} req/s, "
             f"p50 {out[-1]['p50_ms']:.4f} ms, p99 {out[-1]['p99_ms']:.4f} ms")
         del graphs, keep
+    return out
+
+
+def groups_sweep(base, counts, steps, warmup, torch, binding, synth, dev):
+    """Throughput of lightweight models that keep K feature groups (Section
+    3.2, feature group selection: the offline tests weigh a model with the
+    top-K groups by GAUC, QPS and RT).  Each K gets a model of its own with
+    K groups split 1:2:1 over user, ad and cross fields and the serving
+    batch shape; only its speed is measured (synthetic weights)."""
+    out = []
+    for k in counts:
+        nu, nx = k // 4, k // 4
+        cfg = dataclasses.replace(base, n_user=nu, n_ad=k - nu - nx, n_cross=nx, n_seq=0,
+                                  topk_k=0, emit_importance=False,
+                                  widths=(k * base.emb_dim,) + tuple(base.widths[1:]))
+        batch = synth.make_batch(cfg, device=dev)
+        tables = [synth.table_torch(cfg, g, device=dev) for g in range(cfg.n_groups)]
+        model = binding.ColdModel(cfg, device=dev)
+        model.load(tables, binding.params_to_device(synth.make_params(cfg), cfg.dtype, dev))
+        dev_batch = binding.batch_to_device(batch, dev)
+        scores = torch.empty(batch["n_rows"], dtype=torch.float32, device=dev)
+        for _ in range(warmup):
+            model.score(dev_batch, scores=scores)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            model.score(dev_batch, scores=scores)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out.append({"groups": k, "d_in": cfg.d_in, "ms_per_step": round(ms, 5),
+                    "ads_per_s": round(batch["n_rows"] / (ms * 1e-3), 1)})
+        log(f"groups {k:4d} (D_in {cfg.d_in:5d}): {ms:.4f} ms/step, {out[-1]['ads_per_s']:.4g} ads/s")
+        model.close()
+        del tables, model, dev_batch, scores
+        torch.cuda.empty_cache()
     return out
 
 
@@ -396,6 +439,12 @@ def main():
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain "
                          "copy of known size, to calibrate HBM byte counters)")
+    ap.add_argument("--se-literal", action="store_true",
+                    help="use the SE block of Eq. 2 as printed (one FC over the concatenated "
+                         "embedding) instead of the squeeze/excitation form")
+    ap.add_argument("--groups-sweep", default="",
+                    help="after timing, the throughput of models keeping K groups, for each K "
+                         "of this comma list (serving batch shape, widths of --workload)")
     ap.add_argument("--gpu-cross", action="store_true",
                     help="build every cross field on the GPU from a (user field, ad field) "
                          "id pair instead of reading per-row cross ids")
@@ -443,6 +492,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = synth.CONFIGS[args.workload]
+    if args.se_literal:
+        cfg = synth.config(cfg.name, se_form="literal")
     if args.gpu_cross:
         # every cross field built on the GPU from a (user field, ad field) pair
         cfg = synth.config(cfg.name, cross_pairs=tuple(
@@ -544,7 +595,7 @@ def main():
         log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
 
     if args.no_latency:
-        args.batching, args.serving_streams, args.topn = "", "", 0
+        args.batching, args.serving_streams, args.topn, args.groups_sweep = "", "", 0, ""
     batching = None
     if args.batching:
         sizes = [int(v) for v in args.batching.split(",") if v]
@@ -554,6 +605,12 @@ def main():
     if args.serving_streams:
         ks = [int(v) for v in args.serving_streams.split(",") if v]
         serving = serving_curve(model, batch, cfg, ks, args.serving_iters, torch, binding)
+
+    sweep = None
+    if args.groups_sweep:
+        counts = [int(v) for v in args.groups_sweep.split(",") if v]
+        sweep = groups_sweep(synth.config(args.workload, n_requests=32, cand_per_request=2000),
+                             counts, max(5, args.steps // 2), 3, torch, binding, synth, dev)
 
     topn = None
     if args.topn > 0:
@@ -611,7 +668,7 @@ def main():
                    "groups": cfg.n_groups, "emb_dim": cfg.emb_dim, "vocab": cfg.vocab,
                    "widths": list(cfg.widths), "parallelism": "none (1 GPU)",
                    "cross_features": "built on the GPU from user/ad id pairs" if cfg.cross_pairs
-                   else "ids given per row"},
+                   else "ids given per row", "se_form": cfg.se_form},
         "p50_latency_ms": None if p50 is None else round(p50, 4),
         "p99_latency_ms": None if p99 is None else round(p99, 4),
         "p50_latency_graph_ms": None if g50 is None else round(g50, 4),
@@ -629,6 +686,7 @@ def main():
                    for e in stage_rows],
         "cpu_baseline": cpu,
         "topn": topn,
+        "groups_sweep": sweep,
         "serving_streams": serving,
         "serving_batching": batching,
         "usable_requests_per_s": None if not batching else {

@@ -85,7 +85,20 @@ typedef struct cold_model_desc {
   int32_t linear_log;       /* 0/1: apply Eq. 3 to the network input */
   int32_t topk_k;           /* 0: off; else keep the k most important groups per request */
   const int32_t *cross_pairs; /* host [n_cross][2] or NULL: see below */
+  int32_t se_form;          /* COLD_SE_SQUEEZE (0) or COLD_SE_LITERAL (1), see below */
 } cold_model_desc;
+
+/* Form of the SE block of Section 3.2 (Eq. 2, which prints as garbled):
+ *   COLD_SE_SQUEEZE  the squeeze-and-excitation block of Hu et al. that the
+ *                    section cites: z_g = mean of e_g, h = ReLU(W1 z + b1)
+ *                    (H = max(1, M / se_reduction) units), s = sigmoid(W2 h + b2);
+ *   COLD_SE_LITERAL  Eq. 2 as printed: s = sigmoid(W [e_1, ..., e_M] + b), one
+ *                    fully connected layer from the concatenated D_in-wide
+ *                    embedding to M weights: se_w1 is W [M][D_in], se_b1 is
+ *                    b [M], se_w2 and se_b2 are not read (may be NULL), and
+ *                    se_reduction is ignored. */
+#define COLD_SE_SQUEEZE 0
+#define COLD_SE_LITERAL 1
 
 /* User x ad cross features built on the GPU (desc.cross_pairs != NULL).
  * The paper builds its cross features on the CPU next to the other feature
@@ -106,6 +119,7 @@ typedef struct cold_model cold_model;
  *   tables[g]   device [table_rows[g]][emb_dim], dtype, 16-byte aligned
  *   se_w1       device fp32 [H][M]      se_b1 device fp32 [H]
  *   se_w2       device fp32 [M][H]      se_b2 device fp32 [M]
+ *               (literal SE form: se_w1 [M][D_in], se_b1 [M], se_w2/se_b2 unused)
  *   mlp_w[l]    device [widths[l+1]][widths[l]] (out x in), dtype
  *   mlp_b[l]    device fp32 [widths[l+1]]                                  */
 typedef struct cold_weights {

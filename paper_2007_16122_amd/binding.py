@@ -34,6 +34,7 @@ EXPORTS = ("cold_create_model", "cold_destroy_model", "cold_weight_arena_bytes",
            "cold_status_string", "cold_last_error", "cold_profile_enable",
            "cold_profile_read", "cold_select_topn")
 COLD_TOPN_MAX = 1024
+COLD_SE_SQUEEZE, COLD_SE_LITERAL = 0, 1
 
 
 class ColdError(RuntimeError):
@@ -51,7 +52,8 @@ class cold_model_desc(ctypes.Structure):
                 ("widths", ctypes.POINTER(ctypes.c_int32)),
                 ("table_rows", ctypes.POINTER(ctypes.c_int64)),
                 ("linear_log", ctypes.c_int32), ("topk_k", ctypes.c_int32),
-                ("cross_pairs", ctypes.POINTER(ctypes.c_int32))]
+                ("cross_pairs", ctypes.POINTER(ctypes.c_int32)),
+                ("se_form", ctypes.c_int32)]
 
 
 class cold_weights(ctypes.Structure):
@@ -190,7 +192,7 @@ def select_topn(scores, bids, req_off, n_top: int, with_ecpm: bool = True):
 
 def make_desc(n_user, n_seq, n_ad, n_cross, emb_dim, dtype, se_reduction,
               widths: Sequence[int], table_rows: Sequence[int], hashed=False,
-              linear_log=False, topk_k=0, cross_pairs=None):
+              linear_log=False, topk_k=0, cross_pairs=None, se_form=0):
     """A cold_model_desc plus the arrays it points to (keep both alive).
     cross_pairs: None, or (user field, ad field) per cross field."""
     w = (ctypes.c_int32 * len(widths))(*widths)
@@ -204,7 +206,8 @@ def make_desc(n_user, n_seq, n_ad, n_cross, emb_dim, dtype, se_reduction,
                         se_reduction=se_reduction, n_layers=len(widths) - 1,
                         widths=w, table_rows=r, linear_log=int(bool(linear_log)),
                         topk_k=topk_k,
-                        cross_pairs=ctypes.cast(cp, ctypes.POINTER(ctypes.c_int32)) if cp else None)
+                        cross_pairs=ctypes.cast(cp, ctypes.POINTER(ctypes.c_int32)) if cp else None,
+                        se_form=se_form)
     return d, (w, r, cp)
 
 
@@ -226,7 +229,9 @@ class ColdModel:
             cfg.n_user, cfg.n_seq, cfg.n_ad, cfg.n_cross, cfg.emb_dim, cfg.dtype,
             cfg.se_reduction, cfg.widths, [cfg.vocab] * cfg.n_groups, hashed=cfg.hashed,
             linear_log=cfg.linear_log, topk_k=cfg.topk_k,
-            cross_pairs=getattr(cfg, "cross_pairs", None) or None)
+            cross_pairs=getattr(cfg, "cross_pairs", None) or None,
+            se_form=COLD_SE_LITERAL if getattr(cfg, "se_form", "squeeze") == "literal"
+            else COLD_SE_SQUEEZE)
         self.h = cold_create_model(self.desc)
         self.arena = torch.empty(cold_weight_arena_bytes(self.h), dtype=torch.uint8,
                                  device=self.device)
@@ -254,8 +259,10 @@ class ColdModel:
         tabs = (ctypes.c_void_p * len(tables))(*[_ptr(t) for t in tables])
         ws = (ctypes.c_void_p * len(params["mlp_w"]))(*[_ptr(t) for t in params["mlp_w"]])
         bs = (ctypes.c_void_p * len(params["mlp_b"]))(*[_ptr(t) for t in params["mlp_b"]])
+        def opt(t):   # an empty tensor (unused SE parameters) travels as NULL
+            return None if t.numel() == 0 else _ptr(t)
         w = cold_weights(tables=tabs, se_w1=_ptr(params["se_w1"]), se_b1=_ptr(params["se_b1"]),
-                         se_w2=_ptr(params["se_w2"]), se_b2=_ptr(params["se_b2"]),
+                         se_w2=opt(params["se_w2"]), se_b2=opt(params["se_b2"]),
                          mlp_w=ws, mlp_b=bs)
         st = cold_load_weights(self.h, w, _ptr(self.arena), self.arena.numel(), self._stream())
         if st != COLD_OK:

@@ -25,7 +25,7 @@ struct ArenaLayout {
 };
 
 struct WorkLayout {
-  size_t err, U, zU, Uh, urow, X, actA, actB, sbuf, partial, mask, total;
+  size_t err, U, zU, Uh, urow, X, E, actA, actB, sbuf, partial, mask, total;
 };
 
 }  // namespace
@@ -41,6 +41,7 @@ struct cold_model {
   std::vector<int64_t> table_rows;
   std::vector<int32_t> cross_pairs;   // [n_cross][2] or empty
   int M, D_in, H, d, dtype, es, nus, hashed;
+  bool literal_se;
   int max_hidden;
   ArenaLayout arena;
   unsigned char *arena_ptr = nullptr;
@@ -82,10 +83,17 @@ ArenaLayout arena_layout(const cold_model &m) {
   a.rows = take(sizeof(int64_t) * m.M);
   a.magic = take(sizeof(uint64_t) * m.M);
   a.pairs = take(sizeof(int32_t) * m.cross_pairs.size());
-  a.w1 = take(sizeof(float) * m.H * m.M);
-  a.b1 = take(sizeof(float) * m.H);
-  a.w2 = take(sizeof(float) * m.M * m.H);
-  a.b2 = take(sizeof(float) * m.M);
+  if (m.literal_se) {            // W [M][D_in], b [M]
+    a.w1 = take(sizeof(float) * (size_t)m.M * m.D_in);
+    a.b1 = take(sizeof(float) * m.M);
+    a.w2 = take(0);
+    a.b2 = take(0);
+  } else {
+    a.w1 = take(sizeof(float) * m.H * m.M);
+    a.b1 = take(sizeof(float) * m.H);
+    a.w2 = take(sizeof(float) * m.M * m.H);
+    a.b2 = take(sizeof(float) * m.M);
+  }
   const int L = m.desc.n_layers;
   for (int l = 0; l < L; ++l) {
     a.w.push_back(take((size_t)m.es * m.widths[l] * m.widths[l + 1]));
@@ -100,15 +108,17 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
   const bool topk = m.desc.topk_k > 0;
+  const bool sbuf = topk || m.literal_se;
   w.err = take(sizeof(int32_t));
   w.U = take(sizeof(float) * (size_t)Q * m.nus * m.d);
   w.zU = take(sizeof(float) * (size_t)Q * m.nus);
   w.Uh = take((size_t)m.es * Q * m.desc.n_user * m.d);
   w.urow = take(sizeof(int32_t) * (size_t)Q * (m.desc.n_user > 0 ? m.desc.n_user : 1));
   w.X = take((size_t)m.es * R * m.D_in);
+  w.E = take(m.literal_se ? sizeof(float) * (size_t)R * m.D_in : 0);
   w.actA = take((size_t)m.es * R * m.max_hidden);
   w.actB = take((size_t)m.es * R * m.max_hidden);
-  w.sbuf = take(topk ? sizeof(float) * (size_t)R * m.M : 0);
+  w.sbuf = take(sbuf ? sizeof(float) * (size_t)R * m.M : 0);
   w.partial = take(topk ? sizeof(float) * (size_t)Q * kMaskParts * m.M : 0);
   w.mask = take(topk ? (size_t)Q * m.M : 0);
   w.total = off;
@@ -174,7 +184,8 @@ int cold_create_model(const cold_model_desc *desc, cold_model **out) {
   const cold_model_desc &D = *desc;
   if (D.n_user < 0 || D.n_seq < 0 || D.n_ad < 0 || D.n_cross < 0 || D.emb_dim <= 0 ||
       D.se_reduction < 1 || D.n_layers < 1 || !D.widths || !D.table_rows || D.topk_k < 0 ||
-      (D.linear_log != 0 && D.linear_log != 1))
+      (D.linear_log != 0 && D.linear_log != 1) ||
+      (D.se_form != COLD_SE_SQUEEZE && D.se_form != COLD_SE_LITERAL))
     return COLD_ERR_INVALID_ARG;
   if (D.dtype != COLD_F32 && D.dtype != COLD_BF16 && D.dtype != COLD_F16) return COLD_ERR_DTYPE;
   if (D.id_kind != COLD_IDS_DIRECT_I32 && D.id_kind != COLD_IDS_HASHED_U64) return COLD_ERR_DTYPE;
@@ -222,6 +233,7 @@ int cold_create_model(const cold_model_desc *desc, cold_model **out) {
   m->es = es;
   m->nus = D.n_user + D.n_seq;
   m->hashed = D.id_kind == COLD_IDS_HASHED_U64;
+  m->literal_se = D.se_form == COLD_SE_LITERAL;
   m->max_hidden = max_hidden;
   m->arena = arena_layout(*m);
   m->host_tables.assign(M, 0);
@@ -291,8 +303,8 @@ size_t cold_workspace_bytes(const cold_model *m, int64_t max_rows, int64_t max_r
 int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t arena_bytes,
                       void *stream) {
   if (!m) return COLD_ERR_INVALID_ARG;
-  if (!w || !arena || !w->tables || !w->se_w1 || !w->se_b1 || !w->se_w2 || !w->se_b2 || !w->mlp_w ||
-      !w->mlp_b)
+  if (!w || !arena || !w->tables || !w->se_w1 || !w->se_b1 ||
+      (!m->literal_se && (!w->se_w2 || !w->se_b2)) || !w->mlp_w || !w->mlp_b)
     return fail(m, COLD_ERR_INVALID_ARG, "cold_load_weights: null pointer");
   if (reinterpret_cast<uintptr_t>(arena) % kAlign)
     return fail(m, COLD_ERR_INVALID_ARG, "arena must be %zu-byte aligned", kAlign);
@@ -316,10 +328,11 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
       {al.rows, m->table_rows.data(), sizeof(int64_t) * m->M, hipMemcpyHostToDevice},
       {al.magic, m->host_magic.data(), sizeof(uint64_t) * m->M, hipMemcpyHostToDevice},
       {al.pairs, m->cross_pairs.data(), sizeof(int32_t) * m->cross_pairs.size(), hipMemcpyHostToDevice},
-      {al.w1, w->se_w1, sizeof(float) * m->H * m->M, hipMemcpyDeviceToDevice},
-      {al.b1, w->se_b1, sizeof(float) * m->H, hipMemcpyDeviceToDevice},
-      {al.w2, w->se_w2, sizeof(float) * m->M * m->H, hipMemcpyDeviceToDevice},
-      {al.b2, w->se_b2, sizeof(float) * m->M, hipMemcpyDeviceToDevice}};
+      {al.w1, w->se_w1, sizeof(float) * (m->literal_se ? (size_t)m->M * m->D_in : (size_t)m->H * m->M),
+       hipMemcpyDeviceToDevice},
+      {al.b1, w->se_b1, sizeof(float) * (m->literal_se ? m->M : m->H), hipMemcpyDeviceToDevice},
+      {al.w2, w->se_w2, m->literal_se ? 0 : sizeof(float) * m->M * m->H, hipMemcpyDeviceToDevice},
+      {al.b2, w->se_b2, m->literal_se ? 0 : sizeof(float) * m->M, hipMemcpyDeviceToDevice}};
   for (int l = 0; l < L; ++l) {
     copies.push_back({al.w[l], w->mlp_w[l], (size_t)m->es * m->widths[l] * m->widths[l + 1],
                       hipMemcpyDeviceToDevice});
@@ -398,7 +411,35 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
   if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
     return hip_fail(m, e, "user_pool launch");
-  if (!topk) {
+  if (m->literal_se) {
+    // Eq. 2 as printed: the concatenated embedding (fp32), one dense layer
+    // with a sigmoid to the M weights, then the reweighting pass
+    float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
+    g.X = W + wl.E;
+    if ((e = marks.mark("gather_raw")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_gather_se(m->dtype, kRawOut, false, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather (raw) launch");
+    if ((e = marks.mark("se_dense")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_dense_f32(reinterpret_cast<const float *>(W + wl.E), g.w1, g.b1, sb, R, m->M,
+                              m->D_in, 2, s)) != hipSuccess)
+      return hip_fail(m, e, "SE layer launch");
+    g.mask = nullptr;
+    if (topk) {
+      uint8_t *mask = W + wl.mask;
+      if ((e = marks.mark("group_mask")) != hipSuccess) return hip_fail(m, e, "profile event");
+      if ((e = launch_group_mask(sb, b->req_off, Q, R, m->M, D.topk_k,
+                                 reinterpret_cast<float *>(W + wl.partial), kMaskParts, mask,
+                                 group_mask, s)) != hipSuccess)
+        return hip_fail(m, e, "group_mask launch");
+      g.mask = mask;
+    }
+    g.s_buf = sb;
+    g.X = W + wl.X;
+    g.rows_out = nullptr;  // written by the first pass
+    if ((e = marks.mark("gather_apply")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_gather_se(m->dtype, kApplyWeights, D.linear_log, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather_se (apply) launch");
+  } else if (!topk) {
     g.s_buf = importance;
     if ((e = marks.mark("gather_se")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s)) != hipSuccess)

@@ -163,7 +163,11 @@ struct GatherArgs {
   int32_t *err;                   // error bits
 };
 
-enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2 };
+// kFull: SE and reweighting in one pass; kWeightsOnly: SE weights to s_buf;
+// kApplyWeights: reweight with s_buf (groups outside `mask`, when given,
+// read nothing and get weight 0); kRawOut: the concatenated embedding in
+// fp32 to X, for an SE computed elsewhere
+enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3 };
 
 // launchers (return hipError_t of the launch)
 hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s);
@@ -180,6 +184,8 @@ bool tail_supported(int dtype, int K0, int N1, int N2, int n_out);
 hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float *b1,
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s);
+hipError_t launch_dense_f32(const float *x, const float *w, const float *b, float *y, int64_t R,
+                            int32_t N, int32_t K, int act, hipStream_t s);
 hipError_t launch_topn(const float *scores, const float *bids, const int32_t *req_off, int64_t Q,
                        int64_t R, int32_t n_top, int32_t *top_rows, float *top_ecpm, hipStream_t s);
 hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, float *scores,

@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     for (int64_t i = threadIdx.x; i <= Q; i += kGatherThreads) s_req[i] = a.req_off[i];
   cursor += a.req_lds_bytes;
   const float *w1 = a.w1, *b1 = a.b1, *w2 = a.w2, *b2 = a.b2;
-  if constexpr (MODE != kApplyWeights && SE_LDS) {
+  if constexpr ((MODE == kFull || MODE == kWeightsOnly) && SE_LDS) {
     {
       float *sw = reinterpret_cast<float *>(cursor);
       const int nw = H * M;
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       int32_t row = -1;
       if (r < R) {
         bool keep = true;
-        if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
+        if constexpr (MODE == kApplyWeights) keep = !a.mask || a.mask[(int64_t)rq[t] * M + g] != 0;
         if (gpu_cross && f >= a.n_ad) {
           // user x ad cross value: key = mix64(user id) ^ ad id, hashed into
           // the group's table (ids as their unsigned bit patterns)
@@ -268,7 +268,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     reinterpret_cast<float4 *>(ust)[i] =
         reinterpret_cast<const float4 *>(a.U + ((int64_t)rq[t] * nus + nu) * d)[k4];
   }
-  if constexpr (MODE != kApplyWeights) {
+  if constexpr (MODE == kFull || MODE == kWeightsOnly) {
     for (int i = ln; i < Tw * nus; i += 64) {
       const int t = i / nus, g = i - t * nus;
       z[t * M + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
         uint64_t addr = 0;
         if (g < nu) {
           bool keep = true;
-          if constexpr (MODE == kApplyWeights) keep = a.mask[(int64_t)rq[t] * M + g] != 0;
+          if constexpr (MODE == kApplyWeights) keep = !a.mask || a.mask[(int64_t)rq[t] * M + g] != 0;
           if (keep) addr = reinterpret_cast<uint64_t>(Uh + ((int64_t)rq[t] * nu + g) * d + p * EPC);
         } else {
           const int32_t row = ridx[t * nax + (g - nus)];
@@ -310,7 +310,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       advance(t, c);
     }
   }
-  if constexpr (MODE != kApplyWeights) {
+  if constexpr (MODE == kFull || MODE == kWeightsOnly) {
     int t = tf, c = cf;
 #pragma unroll
     for (int j = 0; j < CPT; ++j, advance(t, c)) {
@@ -347,15 +347,39 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       sv[it] = sg;
       if (a.s_buf && r0 + t < R) a.s_buf[r0 * M + it] = sg;
     }
-  } else {
+  } else if constexpr (MODE == kApplyWeights) {
     for (int it = ln; it < Tw * M; it += 64) {
       const int t = it / M, g = it - t * M;
       float sg = 0.0f;
-      if (r0 + t < R && a.mask[(int64_t)rq[t] * M + g]) sg = a.s_buf[r0 * M + it];
+      if (r0 + t < R && (!a.mask || a.mask[(int64_t)rq[t] * M + g])) sg = a.s_buf[r0 * M + it];
       sv[it] = sg;
     }
   }
-  if constexpr (MODE != kWeightsOnly) {
+  if constexpr (MODE == kRawOut) {
+  // ---- the concatenated embedding itself, in fp32 (pooled sequence groups
+  //      are fp32 sums), for an SE computed by a separate dense layer
+  float *E = static_cast<float *>(a.X);
+  int t = tf, c = cf;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j, advance(t, c)) {
+    const int i = ln + 64 * j;
+    const int g = c >> lcpg, p = c & (CPG - 1);
+    if (t < Tw && r0 + t < R) {
+      float v[EPC];
+      if (g >= nu && g < nus) {
+        const float *src = ust + t * ns * d + (g - nu) * d + p * EPC;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) v[e] = src[e];
+      } else {
+        Elem<TS>::unpack(raw[j], v);
+      }
+      float4 *dst = reinterpret_cast<float4 *>(E + (r0 * CPR + i) * EPC);
+#pragma unroll
+      for (int e = 0; e < EPC / 4; ++e) dst[e] = make_float4(v[4 * e], v[4 * e + 1], v[4 * e + 2], v[4 * e + 3]);
+    }
+  }
+  }
+  if constexpr (MODE == kFull || MODE == kApplyWeights) {
   wave_sync();
 
   // ---- reweight, linear_log, round once, coalesced store
@@ -509,7 +533,7 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   a.meta_lds_bytes = (int32_t)((24 * (size_t)a.M + 15) / 16 * 16);
   a.req_lds_bytes = a.Q + 1 <= kGatherMaxReqLds ? (int32_t)((4 * (a.Q + 1) + 15) / 16 * 16) : 0;
   const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
-  a.se_in_lds = MODE != kApplyWeights && se_floats * sizeof(float) <= 24 * 1024;
+  a.se_in_lds = (MODE == kFull || MODE == kWeightsOnly) && se_floats * sizeof(float) <= 24 * 1024;
   a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
   const size_t shmem = (size_t)a.meta_lds_bytes + a.req_lds_bytes + a.se_lds_bytes +
                        4 * (size_t)a.wave_lds_bytes;
@@ -532,6 +556,7 @@ static hipError_t gather_se_t(bool hashed, const GatherArgs &a, hipStream_t s) {
 template <typename TS>
 static hipError_t gather_se_dt(int mode, bool ll, bool hashed, const GatherArgs &a, hipStream_t s) {
   if (mode == kWeightsOnly) return gather_se_t<TS, kWeightsOnly, false>(hashed, a, s);
+  if (mode == kRawOut) return gather_se_t<TS, kRawOut, false>(hashed, a, s);
   if (mode == kApplyWeights)
     return ll ? gather_se_t<TS, kApplyWeights, true>(hashed, a, s)
               : gather_se_t<TS, kApplyWeights, false>(hashed, a, s);

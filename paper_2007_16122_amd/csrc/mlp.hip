@@ -525,6 +525,99 @@ __global__ __launch_bounds__(256) void dense_relu_f32_kernel(const float *__rest
   }
 }
 
+// Y = act(X W^T + b) in fp32 on the matrix cores (v_mfma_f32_16x16x4_f32),
+// without LDS: each wave owns 16 rows x 16*NB outputs and loads its operands
+// straight into registers as 16-byte vectors.  In a 16-deep K chunk, lane l
+// (row or output l % 16, quarter q = l / 16) holds k = 16c + 4q .. 4q + 3 of
+// both operands, and the four MFMAs of the chunk take component 0, 1, 2, 3:
+// every k of the chunk meets its partner exactly once (the order of the sum
+// over k is permuted, which only moves fp32 rounding).  Four chunks are
+// loaded before their MFMAs so one memory latency covers 64 of K.  act 0:
+// none, 1: ReLU, 2: sigmoid.  Used for the SE layer of the literal Eq. 2
+// form (one FC from the concatenated embedding to the M weights).  K must
+// be a multiple of 4 (16-byte rows).
+template <int ACT, int NB>
+__global__ __launch_bounds__(256) void dense_f32_mfma_kernel(const float *__restrict__ X,
+                                                             const float *__restrict__ W,
+                                                             const float *__restrict__ bias,
+                                                             float *__restrict__ Y, int64_t R, int N,
+                                                             int K) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t rbase = (int64_t)blockIdx.x * 64 + wave * 16;
+  const int nbase = blockIdx.y * (16 * NB);
+  const int fr = lane & 15, q = lane >> 4;
+  int64_t xr = rbase + fr;
+  xr = xr < R ? xr : R - 1;                   // clamped: loaded, never stored
+  const float *xp = X + xr * K + 4 * q;
+  const float *wp[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    int n = nbase + i * 16 + fr;
+    n = n < N ? n : N - 1;
+    wp[i] = W + (int64_t)n * K + 4 * q;
+  }
+  f32x4 acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto ld = [&](const float *p, int k) -> float4 {   // k: chunk start; zero past K
+    return (k + 4 * q < K) ? *reinterpret_cast<const float4 *>(p + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  for (int k0 = 0; k0 < K; k0 += 64) {
+    float4 xv[4], wv[4][NB];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      xv[c] = ld(xp, k0 + 16 * c);
+#pragma unroll
+      for (int i = 0; i < NB; ++i) wv[c][i] = ld(wp[i], k0 + 16 * c);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float xs[4] = {xv[c].x, xv[c].y, xv[c].z, xv[c].w};
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const float ws[4] = {wv[c][i].x, wv[c][i].y, wv[c][i].z, wv[c][i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(ws[e], xs[e], acc[i], 0, 0, 0);
+      }
+    }
+  }
+  // lane holds D[4 (lane/16) + e][lane % 16]: output feature, then row
+  const int64_t r = rbase + fr;
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = nbase + i * 16 + 4 * q + e;
+      if (r < R && n < N) {
+        float t = acc[i][e] + bias[n];
+        if (ACT == 1) t = t > 0.0f ? t : 0.0f;
+        if (ACT == 2) t = 1.0f / (1.0f + expf(-t));
+        Y[r * N + n] = t;
+      }
+    }
+}
+
+template <int ACT>
+static hipError_t launch_dense_f32_act(const float *x, const float *w, const float *b, float *y,
+                                       int64_t R, int32_t N, int32_t K, hipStream_t s) {
+  const unsigned gx = (unsigned)((R + 63) / 64);
+  if (N <= 16) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 1>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
+  else if (N <= 32) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 2>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
+  else if (N <= 48) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 3>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
+  else hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 4>), dim3(gx, (unsigned)((N + 63) / 64)), dim3(256), 0, s, x, w, b, y, R, N, K);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_f32(const float *x, const float *w, const float *b, float *y, int64_t R,
+                            int32_t N, int32_t K, int act, hipStream_t s) {
+  if (R <= 0 || N <= 0) return hipSuccess;
+  if (K % 4 != 0) return hipErrorInvalidValue;
+  if (act == 2) return launch_dense_f32_act<2>(x, w, b, y, R, N, K, s);
+  if (act == 1) return launch_dense_f32_act<1>(x, w, b, y, R, N, K, s);
+  return launch_dense_f32_act<0>(x, w, b, y, R, N, K, s);
+}
+
 // last layer + sigmoid (n_out = 1) or softmax (n_out = 2, CTR = class 1)
 template <typename TS>
 __global__ __launch_bounds__(256) void head_kernel(const TS *__restrict__ A, const TS *__restrict__ W,

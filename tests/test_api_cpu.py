@@ -70,6 +70,8 @@ def create_status(**kw):
     (dict(cross_pairs=[(12, 0)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),   # user field >= n_user
     (dict(cross_pairs=[(0, 24)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),   # ad field >= n_ad
     (dict(cross_pairs=[(-1, 0)] + [(0, 0)] * 11), B.COLD_ERR_SHAPE),
+    (dict(se_form=B.COLD_SE_LITERAL), B.COLD_OK),
+    (dict(se_form=2), B.COLD_ERR_INVALID_ARG),
 ])
 def test_create_model_validation(kw, status):
     assert create_status(**kw) == status
@@ -146,3 +148,17 @@ def test_select_topn_rejects_bad_calls_before_the_device():
     assert sel(fake, None, fake, 1, 10, 5, fake, None, None) == B.COLD_ERR_INVALID_ARG
     # no requests: nothing to do, nothing enqueued
     assert sel(None, None, None, 0, 0, 5, None, None, None) == B.COLD_OK
+
+
+def test_literal_se_arena_holds_the_full_layer():
+    sizes = {}
+    for form in (B.COLD_SE_SQUEEZE, B.COLD_SE_LITERAL):
+        d, keep = desc(se_form=form)
+        h = B.cold_create_model(d)
+        try:
+            sizes[form] = B.cold_weight_arena_bytes(h)
+        finally:
+            B.cold_destroy_model(h)
+    # literal: W [48][768] + b [48] fp32 instead of W1 [12][48], b1, W2 [48][12], b2
+    grow = 4 * (48 * 768 + 48) - 4 * (12 * 48 + 12 + 48 * 12 + 48)
+    assert sizes[B.COLD_SE_LITERAL] - sizes[B.COLD_SE_SQUEEZE] >= grow - 4 * 256

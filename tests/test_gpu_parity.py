@@ -100,6 +100,30 @@ def test_parity_gpu_cross_features(name):
     compare_scores(cfg, g["scores"], o["scores"], f"gpu cross {name}")
 
 
+@pytest.mark.parametrize("name", ["tiny_fp32", "serving_bf16", "multivalued_fp16_ll",
+                                  "wide_prune_bf16"])
+def test_parity_literal_se(name):
+    """Eq. 2 as printed (one FC from the concatenated embedding to the M
+    weights, on the fp32 matrix cores): SE weights, masks, gather indices
+    and scores against the checker.  The SE logit is an fp32 sum of D_in
+    products (up to 3,200) in the kernel's order, so s is held to 1e-5
+    rather than the 2e-6 of the squeeze form, whose logits sum 12-50 terms."""
+    cfg = mid(name, se_form="literal")
+    log(f"test_parity_literal_se {name}: {MID_CANDS[name]}")
+    tables, params, batch = problem(cfg, seed=25, cand=MID_CANDS[name])
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True, want_s=True, want_mask=cfg.topk_k > 0)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_s=True)
+    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
+    np.testing.assert_allclose(g["s"], o["s"], atol=1e-5, rtol=0)
+    if cfg.topk_k:
+        check_mask(cfg, o, g, batch)
+    compare_scores(cfg, g["scores"], o["scores"], f"literal SE {name}")
+
+
 @pytest.mark.parametrize("name", CONFIG_NAMES)
 def test_parity_full_size_sampled(name):
     """The full workload in the launch configuration the bench times; the
