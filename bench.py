@@ -20,6 +20,7 @@ import argparse
 import dataclasses
 import json
 import os
+import re
 import sys
 import time
 
@@ -329,7 +330,13 @@ def _stage_of(kernel_name, dense_index):
     if "user_pool" in kernel_name:
         return "user_pool"
     if "gather_se_kernel" in kernel_name:
-        return "gather_se"
+        # the second template argument (mangled "Li<n>E") is the pass:
+        # full, weights, apply, raw
+        mt = re.search(r"gather_se_kernelI\w*?Li(\d+)E", kernel_name)
+        mode = mt.group(1) if mt else "0"
+        return {"0": "gather_se", "1": "se_weights", "2": "gather_apply", "3": "gather_raw"}.get(mode, "gather_se")
+    if "dense_f32" in kernel_name:
+        return "se_dense"
     if "mask_partial" in kernel_name or "mask_select" in kernel_name:
         return "group_mask"
     if "dense_relu" in kernel_name:
@@ -341,12 +348,26 @@ def _stage_of(kernel_name, dense_index):
     return None
 
 
+def _call_starts(ours):
+    """Indices of the first kernel of each scoring call: the per-request
+    user pooling, or, in a call without one, the first gather after the
+    previous call's last layer."""
+    out, prev = [], None
+    for i, r in enumerate(ours):
+        st = _stage_of(r["Kernel_Name"], 0)
+        if st == "user_pool" or (st in ("gather_se", "se_weights", "gather_raw") and prev != "user_pool"):
+            out.append(i)
+        if st is not None:
+            prev = st
+    return out
+
+
 def _last_call(rows, key_start="Start_Timestamp"):
     """Dispatches of libcold kernels in the last complete scoring call,
     as (stage, row) pairs in launch order."""
     ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
     ours.sort(key=lambda r: int(r[key_start]))
-    starts = [i for i, r in enumerate(ours) if "user_pool" in r["Kernel_Name"]]
+    starts = _call_starts(ours)
     if not starts:
         return []
     call = ours[starts[-1]:]
@@ -368,12 +389,12 @@ def summarize_trace(trace_dir, command):
     rows = list(csv.DictReader(open(path)))
     ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
     ours.sort(key=lambda r: int(r["Start_Timestamp"]))
-    starts = [i for i, r in enumerate(ours) if "user_pool" in r["Kernel_Name"]]
+    starts = _call_starts(ours)
     per_stage = {}
     for a, b in zip(starts, starts[1:] + [len(ours)]):
         di = 0
         for r in ours[a:b]:
-            st = _stage_of(r["Kernel_Name"], di)
+            st = _stage_of(r["Kernel_Name"], di) or "other"
             if st.startswith("dense"):
                 di += 1
             d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3

@@ -67,7 +67,7 @@ def lib():
         L.orc_score.argtypes = [ctypes.POINTER(_Problem), ctypes.c_void_p, ctypes.c_int64,
                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                ctypes.c_int]
+                                ctypes.c_void_p, ctypes.c_int]
         L.orc_linear_log.restype = ctypes.c_double
         L.orc_linear_log.argtypes = [ctypes.c_double]
         L.orc_mix64.restype = ctypes.c_uint64
@@ -109,7 +109,8 @@ def cross_key(user_id: int, ad_id: int) -> int:
 
 
 def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
-          want_rows=False, want_s=False, want_x=False, n_threads=None) -> dict:
+          want_rows=False, want_s=False, want_x=False, want_z=False,
+          n_threads=None) -> dict:
     """Score rows of a batch.
 
     dims: n_user, n_seq, n_ad, n_cross, emb_dim, se_hidden, dtype ('f32' |
@@ -125,8 +126,9 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
     batch: req_off, user_ids, ad_ids, cross_ids, seq_off, seq_ids.
     sample: row indices to score (default: every row).
 
-    Returns a dict with 'scores' and, on request, 'rows', 's', 'x', and (when
-    topk_k > 0) 'importance' and 'mask' per request.
+    Returns a dict with 'scores' and, on request, 'rows', 's', 'x', 'z' (the
+    SE squeeze, zero for the one-layer form), and (when topk_k > 0)
+    'importance' and 'mask' per request.
     """
     L = lib()
     m = dims["n_user"] + dims["n_seq"] + dims["n_ad"] + dims["n_cross"]
@@ -197,6 +199,8 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
         out["s"] = np.zeros((n, m), np.float64)
     if want_x:
         out["x"] = np.zeros((n, m * d), np.float64)
+    if want_z:
+        out["z"] = np.zeros((n, m), np.float64)
     topk = int(dims.get("topk_k", 0)) > 0
     if topk:
         out["importance"] = np.zeros((q, m), np.float64)
@@ -205,7 +209,7 @@ def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,
         n_threads = len(os.sched_getaffinity(0))
     st = L.orc_score(ctypes.byref(prob), _ptr(sample), n, _ptr(out["scores"]),
                      _ptr(out.get("rows")), _ptr(out.get("s")), _ptr(out.get("x")),
-                     _ptr(out.get("importance")), _ptr(out.get("mask")), int(n_threads))
+                     _ptr(out.get("z")), _ptr(out.get("importance")), _ptr(out.get("mask")), int(n_threads))
     if st != 0:
         raise OracleError(_ERRORS.get(st, f"status {st}"))
     out["n_threads"] = n_threads

@@ -348,12 +348,14 @@ static int group_masks(const orc_problem *p, double *imp, uint8_t *mask, int n_t
  *   s_out[n_sample][M]      (opt.)  SE importance weights (before any mask)
  *   x_out[n_sample][D_in]   (opt.)  network input (after reweighting, mask and
  *                                   linear_log)
+ *   z_out[n_sample][M]      (opt.)  squeeze z of the SE block (zero for the
+ *                                   one-layer form, which has none)
  *   imp_out[Q][M], mask_out[Q][M] (opt., only when topk_k > 0)
  * Returns ORC_OK, ORC_BAD_ARG, ORC_ID_RANGE or ORC_NO_MEM.
  */
 int orc_score(const orc_problem *p, const int64_t *sample, int64_t n_sample, double *scores,
-              int64_t *rows_out, double *s_out, double *x_out, double *imp_out,
-              uint8_t *mask_out, int n_threads) {
+              int64_t *rows_out, double *s_out, double *x_out, double *z_out,
+              double *imp_out, uint8_t *mask_out, int n_threads) {
   int st = check_problem(p);
   if (st != ORC_OK) return st;
   const int M = p->n_user + p->n_seq + p->n_ad + p->n_cross;
@@ -404,6 +406,10 @@ int orc_score(const orc_problem *p, const int64_t *sample, int64_t n_sample, dou
       if (rows_out) memcpy(rows_out + i * M, rows, sizeof(int64_t) * M);
       if (s_out) memcpy(s_out + i * M, s, sizeof(double) * M);
       if (x_out) memcpy(x_out + i * D, x, sizeof(double) * D);
+      if (z_out) {
+        if (p->se_form == 1) memset(z_out + i * M, 0, sizeof(double) * M);
+        else memcpy(z_out + i * M, z, sizeof(double) * M);
+      }
     }
     free(e); free(x); free(z); free(h); free(s); free(ba); free(bb); free(rows);
   }

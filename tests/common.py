@@ -54,3 +54,51 @@ def table_f64(cfg, t: np.ndarray) -> np.ndarray:
     if cfg.dtype == "bf16":
         return (t.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     return t.astype(np.float64)
+
+
+def se_weight_bound(params: dict, z: np.ndarray, s: np.ndarray, floor: float = 2e-6) -> np.ndarray:
+    """Per-element bound on |s_fp32 - s| for the squeeze-excitation weights
+    (Eq. 2: h = ReLU(W1 z + b1), s = sigmoid(W2 h + b2)) evaluated in fp32
+    by sequential sums that start from the bias and add the terms in index
+    order (the order the gather kernel uses).
+
+    The synthetic tables hold multiples of a power of two with few
+    significant bits and d is a power of two, so the squeeze z is exact in
+    fp32 (callers check this).  Each dot product is then off by at most
+    u * (sum_k |S_k| + sum_k |p_k|), u = 2^-24, over its partial sums S_k and
+    products p_k (running error analysis: one rounding per product and one
+    per addition, so fused or not); the hidden error passes through the ReLU
+    unamplified and into the logit through |W2|; the sigmoid's slope over
+    the logit's error interval scales the result, and `floor` covers the
+    sigmoid's own evaluation.  z: [n][M], s: [n][M] (fp64 reference).
+    """
+    u = 2.0 ** -24
+    w1, b1, w2, b2 = (np.asarray(params[k], np.float64) for k in ("se_w1", "se_b1", "se_w2", "se_b2"))
+
+    def dot_and_error(x, w, b):
+        p = x[:, None, :] * w[None, :, :]                  # [n][out][in]
+        partial = b[None, :, None] + np.cumsum(p, axis=2)
+        err = u * (np.abs(b)[None, :] + np.abs(partial).sum(axis=2) + np.abs(p).sum(axis=2))
+        return partial[:, :, -1], err * (1.0 + 4 * x.shape[1] * u)
+
+    a, da = dot_and_error(z, w1, b1)
+    h = np.maximum(a, 0.0)
+    logit, dl = dot_and_error(h, w2, b2)
+    dl = dl + da @ np.abs(w2).T
+    # steepest sigmoid slope on [logit - dl, logit + dl]
+    x = np.maximum(np.abs(logit) - dl, 0.0)
+    sx = 1.0 / (1.0 + np.exp(-x))
+    slope = sx * (1.0 - sx)
+    assert s.shape == dl.shape
+    return slope * dl + floor
+
+
+def assert_se_weights_close(params: dict, got: np.ndarray, o: dict) -> None:
+    """fp32 SE weights against the checker's, within se_weight_bound."""
+    z = o["z"]
+    assert np.array_equal(z.astype(np.float32).astype(np.float64), z), "squeeze not exact in fp32"
+    bound = se_weight_bound(params, z, o["s"])
+    err = np.abs(np.asarray(got, np.float64) - o["s"])
+    worst = np.unravel_index(np.argmax(err - bound), err.shape) if err.size else None
+    assert np.all(err <= bound), (f"SE weight off by {err[worst]:.3e} at {worst}, "
+                                  f"bound {bound[worst]:.3e}")
