@@ -408,9 +408,11 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   static const char *kDenseNames[] = {"dense0", "dense1", "dense2", "dense3", "dense4", "dense5",
                                       "dense6", "dense7", "dense8", "dense9", "dense10", "dense11"};
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
-  if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
-  if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
-    return hip_fail(m, e, "user_pool launch");
+  if (user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
+    if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "user_pool launch");
+  }
   if (m->literal_se) {
     // Eq. 2 as printed: the concatenated embedding (fp32), one dense layer
     // with a sigmoid to the M weights, then the reweighting pass

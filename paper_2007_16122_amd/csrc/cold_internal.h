@@ -140,6 +140,9 @@ struct GatherArgs {
   int32_t se_in_lds;
   int32_t meta_lds_bytes;         // LDS for per-group table metadata
   int32_t req_lds_bytes;          // LDS for the request offsets, 0 if searched in global
+  int32_t users_in_lds;           // user rows staged in LDS by the gather (no pooling pass)
+  int32_t urow_lds_bytes;         // LDS for their resolved rows
+  int32_t uval_lds_bytes;         // LDS for their values (storage type)
   int64_t R, Q, n_seq_ids;
   const int32_t *req_off;         // [Q+1]
   const void *user_ids;           // [n_user][Q]
@@ -170,6 +173,7 @@ struct GatherArgs {
 enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3 };
 
 // launchers (return hipError_t of the launch)
+bool user_pool_needed(int dtype, const GatherArgs &a);
 hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s);
 hipError_t launch_gather_se(int dtype, int mode, bool linear_log, bool hashed,
                             const GatherArgs &a, hipStream_t s);
@@ -196,5 +200,6 @@ constexpr int kGatherMaxChunksPerRow = 1024;  // 64 lanes x 16 chunks
 constexpr int kGatherMaxIdsPerLane = 8;       // rows per wave x (ad + cross fields) <= 512
 constexpr int kMaskParts = 64;
 constexpr int kGatherMaxReqLds = 1024;        // request offsets held in LDS up to this count
+constexpr int kGatherMaxUserValLds = 4096;    // user row bytes the gather stages in LDS itself
 
 }  // namespace cold

@@ -154,6 +154,35 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   if (req_in_lds)
     for (int64_t i = threadIdx.x; i <= Q; i += kGatherThreads) s_req[i] = a.req_off[i];
   cursor += a.req_lds_bytes;
+  // few requests without sequences: their single-valued user rows are
+  // resolved and staged in LDS (storage type) here, and no pooling pass runs
+  int32_t *s_urow = reinterpret_cast<int32_t *>(cursor);                       // [n_user][Q]
+  uint4 *s_uval = reinterpret_cast<uint4 *>(cursor + a.urow_lds_bytes);        // [Q][n_user][CPG]
+  const bool users_in_lds = a.users_in_lds != 0;
+  if (users_in_lds) {
+    const int64_t n_chunks = Q * a.n_user * CPG;
+    for (int64_t i = threadIdx.x; i < n_chunks; i += kGatherThreads) {
+      const int p = (int)(i & (CPG - 1));
+      const int64_t qf = i >> lcpg, q = qf / a.n_user;
+      const int f = (int)(qf - q * a.n_user);
+      const int32_t row = resolve_row<HASHED>(a.user_ids, (int64_t)f * Q + q, f, a.table_rows[f],
+                                              a.table_magic[f], a.err);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (row >= 0) v = reinterpret_cast<const uint4 *>(static_cast<const TS *>(a.tables[f]) + (int64_t)row * d)[p];
+      s_uval[i] = v;
+      if (p == 0) s_urow[(int64_t)f * Q + q] = row;
+    }
+    if constexpr (MODE != kApplyWeights) {   // request offsets sanity, otherwise done by the pooling pass
+      for (int64_t q = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x; q < Q;
+           q += (int64_t)gridDim.x * kGatherThreads) {
+        bool bad = a.req_off[q + 1] < a.req_off[q];
+        if (q == 0) bad |= a.req_off[0] != 0;
+        if (q == Q - 1) bad |= (int64_t)a.req_off[Q] != R;
+        if (bad) atomicOr(a.err, 2);
+      }
+    }
+  }
+  cursor += a.urow_lds_bytes + a.uval_lds_bytes;
   const float *w1 = a.w1, *b1 = a.b1, *w2 = a.w2, *b2 = a.b2;
   if constexpr ((MODE == kFull || MODE == kWeightsOnly) && SE_LDS) {
     {
@@ -268,9 +297,9 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     reinterpret_cast<float4 *>(ust)[i] =
         reinterpret_cast<const float4 *>(a.U + ((int64_t)rq[t] * nus + nu) * d)[k4];
   }
-  if constexpr (MODE == kFull || MODE == kWeightsOnly) {
-    for (int i = ln; i < Tw * nus; i += 64) {
-      const int t = i / nus, g = i - t * nus;
+  if constexpr (MODE == kFull || MODE == kWeightsOnly) {   // squeeze of the pooled sequences
+    for (int i = ln; i < Tw * ns; i += 64) {
+      const int t = i / ns, g = nu + (i - t * ns);
       z[t * M + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
     }
   }
@@ -279,7 +308,9 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     for (int i = ln; i < Tw * nus; i += 64) {
       const int f = i / Tw, t = i - f * Tw;
       const int64_t r = r0 + t;
-      if (r < R) a.rows_out[(int64_t)f * R + r] = f < nu ? a.urow[(int64_t)rq[t] * nu + f] : -1;
+      if (r < R)
+        a.rows_out[(int64_t)f * R + r] =
+            f >= nu ? -1 : users_in_lds ? s_urow[(int64_t)f * Q + rq[t]] : a.urow[(int64_t)rq[t] * nu + f];
     }
   }
 
@@ -297,7 +328,8 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
         if (g < nu) {
           bool keep = true;
           if constexpr (MODE == kApplyWeights) keep = !a.mask || a.mask[(int64_t)rq[t] * M + g] != 0;
-          if (keep) addr = reinterpret_cast<uint64_t>(Uh + ((int64_t)rq[t] * nu + g) * d + p * EPC);
+          if (keep && users_in_lds) raw[j] = s_uval[((int64_t)rq[t] * nu + g) * CPG + p];
+          else if (keep) addr = reinterpret_cast<uint64_t>(Uh + ((int64_t)rq[t] * nu + g) * d + p * EPC);
         } else {
           const int32_t row = ridx[t * nax + (g - nus)];
           if (row >= 0) addr = s_tab[g] + ((uint64_t)row * d + p * EPC) * sizeof(TS);
@@ -321,7 +353,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
 #pragma unroll
       for (int e = 0; e < EPC; ++e) part += v[e];
       for (int o = 1; o < CPG; o <<= 1) part += __shfl_xor(part, o);
-      if (t < Tw && p == 0 && g >= nus) z[t * M + g] = r0 + t < R ? part / (float)d : 0.0f;
+      if (t < Tw && p == 0 && (g < nu || g >= nus)) z[t * M + g] = r0 + t < R ? part / (float)d : 0.0f;
     }
     wave_sync();
 
@@ -469,8 +501,14 @@ static hipError_t user_pool_t(bool hashed, const GatherArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool user_pool_needed(int dtype, const GatherArgs &a) {
+  if (a.n_seq > 0) return true;
+  const int64_t es = dtype == kF32 ? 4 : 2;
+  return (int64_t)a.n_user * a.Q * a.d * es > kGatherMaxUserValLds;
+}
+
 hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s) {
-  if (a.Q <= 0) return hipSuccess;
+  if (a.Q <= 0 || !user_pool_needed(dtype, a)) return hipSuccess;
   switch (dtype) {
     case kF32: return user_pool_t<float>(hashed, a, s);
     case kBF16: return user_pool_t<__bf16>(hashed, a, s);
@@ -532,11 +570,14 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
                                 sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
   a.meta_lds_bytes = (int32_t)((24 * (size_t)a.M + 15) / 16 * 16);
   a.req_lds_bytes = a.Q + 1 <= kGatherMaxReqLds ? (int32_t)((4 * (a.Q + 1) + 15) / 16 * 16) : 0;
+  a.users_in_lds = user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a) ? 0 : 1;
+  a.urow_lds_bytes = a.users_in_lds ? (int32_t)((4 * (int64_t)a.n_user * a.Q + 15) / 16 * 16) : 0;
+  a.uval_lds_bytes = a.users_in_lds ? (int32_t)((int64_t)a.n_user * a.Q * a.d * sizeof(TS)) : 0;
   const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
   a.se_in_lds = (MODE == kFull || MODE == kWeightsOnly) && se_floats * sizeof(float) <= 24 * 1024;
   a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
-  const size_t shmem = (size_t)a.meta_lds_bytes + a.req_lds_bytes + a.se_lds_bytes +
-                       4 * (size_t)a.wave_lds_bytes;
+  const size_t shmem = (size_t)a.meta_lds_bytes + a.req_lds_bytes + a.urow_lds_bytes +
+                       a.uval_lds_bytes + a.se_lds_bytes + 4 * (size_t)a.wave_lds_bytes;
   if (T * nax > 64 * kGatherMaxIdsPerLane || shmem > 160 * 1024) return hipErrorInvalidValue;
   const int64_t rows_per_block = 4 * (int64_t)T;
   const int64_t blocks = (a.R + rows_per_block - 1) / rows_per_block;

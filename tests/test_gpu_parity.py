@@ -298,6 +298,36 @@ def test_validate_reports_out_of_range_ids():
     compare_scores(cfg, g["scores"], run_oracle(cfg, tables, params, batch)["scores"], "after bad")
 
 
+@pytest.mark.parametrize("n_req", [2, 20])
+def test_validate_reports_bad_user_ids_and_offsets(n_req):
+    """Validate mode flags an out-of-range user id and non-monotone request
+    offsets, whether the gather stages the requests' user rows itself (a
+    few requests) or takes them from the pooling pass (many)."""
+    cfg = mid("serving_bf16")
+    log(f"test_validate_reports_bad_user_ids_and_offsets Q={n_req}")
+    tables, params, batch = problem(cfg, seed=37, cand=[30] * n_req)
+    run = load(cfg, tables, params)
+    try:
+        bad = dict(batch)
+        bad["user_ids"] = batch["user_ids"].copy()
+        bad["user_ids"][2, 1] = cfg.vocab + 5
+        with pytest.raises(binding.ColdError) as ei:
+            run.score(bad, validate=True)
+        assert ei.value.status == binding.COLD_ERR_ID_RANGE and "ids" in str(ei.value)
+        bad = dict(batch)
+        off = batch["req_off"].copy()
+        off[1], off[2] = off[2], off[1]        # still within [0, R], no longer monotone
+        bad["req_off"] = off
+        with pytest.raises(binding.ColdError) as ei:
+            run.score(bad, validate=True)
+        assert ei.value.status == binding.COLD_ERR_ID_RANGE and "offsets" in str(ei.value)
+        g = run.score(batch, validate=True)
+    finally:
+        run.close()
+    compare_scores(cfg, g["scores"], run_oracle(cfg, tables, params, batch)["scores"],
+                   f"after bad, Q={n_req}")
+
+
 def test_empty_batches_are_noops():
     cfg = mid("serving_bf16")
     tables, params, batch = problem(cfg, seed=36, cand=[0, 0])
