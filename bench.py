@@ -435,17 +435,25 @@ def summarize_pmc(fetch_dir, write_dir, probe_mb, command, workload):
             "stages": stages, "sources": _source_hashes()}
 
 
+def _stage_sources(stage):
+    """Source files that define a stage's kernel (with the shared header)."""
+    if stage.startswith("dense") or stage in ("tail", "head", "se_dense"):
+        return ("mlp.hip", "cold_internal.h")
+    return ("gather.hip", "cold_internal.h")
+
+
 def load_traffic(workload):
-    """Measured HBM bytes per stage, or None when the kernel sources changed
-    since the counters were taken."""
+    """Measured HBM bytes per stage, keeping only the stages whose kernel
+    sources are unchanged since the counters were taken (None if none are)."""
     path = TRAFFIC_JSON.format(workload=workload)
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         t = json.load(fh)
-    if t.get("sources") != _source_hashes():
-        return None
-    return t
+    then, now = t.get("sources", {}), _source_hashes()
+    stages = {k: v for k, v in t.get("stages", {}).items()
+              if all(then.get(f) is not None and then.get(f) == now.get(f) for f in _stage_sources(k))}
+    return dict(t, stages=stages) if stages else None
 
 
 def main():
@@ -502,8 +510,8 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the scoring path runs on a single MI355X "
-              f"(rows are independent; see DESIGN.md for how it would shard). Got --gpus {args.gpus}.",
-              file=sys.stderr)
+              f"(rows are independent, so it would shard by requests across GPUs). "
+              f"Got --gpus {args.gpus}.", file=sys.stderr)
         sys.exit(2)
 
     import torch
