@@ -79,12 +79,40 @@ __global__ __launch_bounds__(256) void user_pool_kernel(GatherArgs a) {
     lo = lo < 0 ? 0 : (lo > a.n_seq_ids ? a.n_seq_ids : lo);
     hi = hi < lo ? lo : (hi > a.n_seq_ids ? a.n_seq_ids : hi);
     const TS *tab = static_cast<const TS *>(a.tables[g]);
+    const int64_t rows_g = a.table_rows[g];
+    const uint64_t magic_g = a.table_magic[g];
+    // sum-pooling in sequence order; ids, rows and values are fetched 16 at
+    // a time so that a sequence costs a few memory round trips, not two per id
+    constexpr int kSeqBlock = 16;
     float acc = 0.0f;
-    for (int64_t j = lo; j < hi; ++j) {  // sum-pooling in sequence order
-      const int32_t row = resolve_row<HASHED>(a.seq_ids, j, g, a.table_rows[g],
-                                              a.table_magic[g], a.err);
-      if (row >= 0) acc += Elem<TS>::to_f32(tab[(int64_t)row * d + k]);
+    bool bad = false;
+    for (int64_t j0 = lo; j0 < hi; j0 += kSeqBlock) {
+      int32_t row[kSeqBlock];
+#pragma unroll
+      for (int u = 0; u < kSeqBlock; ++u) {
+        const bool in = j0 + u < hi;
+        const int64_t j = in ? j0 + u : hi - 1;   // loads stay in range; the result is dropped
+        if constexpr (HASHED) {
+          const uint64_t raw = static_cast<const uint64_t *>(a.seq_ids)[j];
+          const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+          const int32_t r = (int32_t)mod_barrett(mix64(raw ^ salt), (uint64_t)rows_g, magic_g);
+          row[u] = in ? r : -1;
+        } else {
+          const int32_t id = static_cast<const int32_t *>(a.seq_ids)[j];
+          const bool ok = id >= 0 && (int64_t)id < rows_g;
+          bad |= in && !ok;
+          row[u] = in && ok ? id : -1;
+        }
+      }
+      float v[kSeqBlock];   // dropped ids read row 0 (always present) and are not added
+#pragma unroll
+      for (int u = 0; u < kSeqBlock; ++u)
+        v[u] = Elem<TS>::to_f32(tab[(int64_t)(row[u] >= 0 ? row[u] : 0) * d + k]);
+#pragma unroll
+      for (int u = 0; u < kSeqBlock; ++u)
+        if (row[u] >= 0) acc += v[u];
     }
+    if (bad) atomicOr(a.err, 1);
     a.U[(q * nus + g) * d + k] = acc;
     s_u[g * d + k] = acc;
   }
@@ -458,6 +486,7 @@ __global__ __launch_bounds__(256) void mask_partial_kernel(const float *s_buf, c
   const int64_t a = lo + p * per, b = (a + per < hi) ? a + per : hi;
   for (int g = threadIdx.x; g < M; g += blockDim.x) {
     float acc = 0.0f;
+#pragma unroll 8
     for (int64_t r = a; r < b; ++r) acc += s_buf[r * M + g];
     partial[(q * P + p) * M + g] = acc;
   }
@@ -474,6 +503,7 @@ __global__ __launch_bounds__(256) void mask_select_kernel(const float *partial, 
   const float n = (float)(hi - lo);
   for (int g = threadIdx.x; g < M; g += blockDim.x) {
     float acc = 0.0f;
+#pragma unroll 16
     for (int p = 0; p < P; ++p) acc += partial[(q * P + p) * M + g];
     imp[g] = n > 0.0f ? acc / n : 0.0f;
   }
