@@ -1,7 +1,7 @@
 // mlp.hip -- the fully connected network of the COLD model (Section 4.1:
 // D_in x 1024 x 512 x 256 x 128 x 64 x 2) on gfx950.
 //
-//  dense_relu_pipe  Y = ReLU(X W^T + b) for bf16/fp16 X, W with fp32
+//  dense_relu_buf   Y = ReLU(X W^T + b) for bf16/fp16 X, W with fp32
 //                   accumulation on the matrix cores
 //                   (v_mfma_f32_16x16x32_{bf16,f16}) and one rounding of the
 //                   output to the storage type.  Operand tiles stream from
@@ -10,8 +10,8 @@
 //                   X the B operand.  Tiles are numbered so that the
 //                   workgroups sharing one row block of X run on the same XCD
 //                   (workgroup i is dispatched to XCD i mod 8) and reuse it
-//                   from that XCD's L2.  256 x 128 tiles for large batches,
-//                   64 x 64 for a single request.
+//                   from that XCD's L2.  256 x 256 tiles (8 waves) for large
+//                   batches, 64 x 64 for a single request.
 //  dense_relu_mfma  the same layer with register-staged, double-buffered LDS
 //                   tiles; used when K is not a multiple of 32.
 //  mlp_tail         the last two hidden layers and the head fused over
@@ -169,15 +169,15 @@ __global__ __launch_bounds__(256, 2) void dense_relu_mfma_kernel(const TS *__res
 }
 
 // ---------------------------------------------------------------------------
-// Pipelined layer: operand tiles stream global -> LDS with the gfx950 direct
-// loads (global_load_lds_dwordx4: each lane's 16 bytes land at
-// base + 16 * lane, no VGPR staging) into an S-stage ring, issued S-1 K steps
-// ahead; each wave waits only for its own loads of the stage it is about to
-// read (vmcnt), then one barrier per K step.  LDS rows are 64 bytes (32
-// elements); chunk c of row r sits in slot c ^ swz(r), which makes the
-// 16-byte fragment reads conflict-free whether the LDS serves 8 or 16 lanes
-// per cycle.  The output tile is staged in LDS after the K loop so every row
-// segment is written with full 16-byte stores.
+// Pipelined layer, dense_relu_buf: operand tiles stream global -> LDS with the
+// gfx950 buffer loads to LDS (each lane's 16 bytes land at base + 16 * lane,
+// no VGPR staging) into an S-stage ring, issued S-1 K steps ahead; each wave
+// waits only for its own loads of the stage it is about to read (vmcnt), then
+// one barrier per K step.  LDS rows are 64 bytes (32 elements); chunk c of
+// row r sits in slot c ^ swz(r), which makes the 16-byte fragment reads
+// conflict-free whether the LDS serves 8 or 16 lanes per cycle.  The output
+// tile is staged in LDS after the K loop so every row segment is written with
+// full 16-byte stores.
 __device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 
 
@@ -195,148 +195,200 @@ __device__ __forceinline__ void wait_stages(int later) {
   }
 }
 
-template <typename TS, int BR, int BN, int S, int MINW = 2>
-__global__ __launch_bounds__(256, MINW) void dense_relu_pipe_kernel(const TS *__restrict__ X,
-                                                                 const TS *__restrict__ W,
-                                                                 const float *__restrict__ bias,
-                                                                 TS *__restrict__ Y, int64_t R, int N,
-                                                                 int K, int tiles_n, int tiles_total) {
-  typedef typename Mfma<TS>::frag frag;
+// The instruction stream of the K loop is kept lean:
+//  * one buffer resource per operand starts at the tile's first row; a lane
+//    has a fixed offset and the K step is a scalar offset, so a K step costs
+//    no vector address arithmetic; rows past the end of the operand read
+//    zeros (the resource's range check);
+//  * the wave index is uniform, so every LDS destination is scalar;
+//  * the K loop is unrolled over the ring, so every LDS read address is a
+//    compile-time offset from one register;
+//  * the accumulators start at the bias;
+//  * the epilogue rounds two outputs per instruction and applies ReLU to the
+//    rounded pair as 16-bit integers (round-to-nearest-even is monotone and
+//    keeps 0, and a negative half-precision value has its sign bit set, so
+//    max(bits, 0) as signed integers is ReLU after rounding).
+// Waves are laid out 2 (rows) x WN (features); each wave owns a
+// (BR/2) x (BN/WN) block of 16 x 16 MFMA tiles.
+template <typename TS> struct Pair;
+template <> struct Pair<__bf16> {
+  typedef __bf16 v2 __attribute__((ext_vector_type(2)));
+};
+template <> struct Pair<_Float16> {
+  typedef _Float16 v2 __attribute__((ext_vector_type(2)));
+};
+
+// 16 bytes per lane from base + voff + soff into LDS at dst + 16 * lane;
+// reads at or past base + bytes return zeros
+__device__ __forceinline__ void buffer_load_lds16(const void *base, int bytes, void *dst, int voff,
+                                                  int soff) {
   typedef __attribute__((address_space(3))) void lds_void;
-  constexpr int NI = BN / 32, RJ = BR / 32;          // 16x16 blocks per wave
+  constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data format
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, kRsrcWord3);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)dst, 16, voff, soff, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t relu_bits2(uint32_t v) {
+  typedef short s2 __attribute__((ext_vector_type(2)));
+  const s2 r = __builtin_elementwise_max(__builtin_bit_cast(s2, v), (s2){0, 0});
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+template <typename TS>
+__device__ __forceinline__ uint32_t round2(float lo, float hi) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  const typename Pair<TS>::v2 h = __builtin_convertvector((f2){lo, hi}, typename Pair<TS>::v2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2>
+__global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
+                                                                     const TS *__restrict__ W,
+                                                                     const float *__restrict__ bias,
+                                                                     TS *__restrict__ Y, int64_t R,
+                                                                     int N, int K, int tiles_n,
+                                                                     int tiles_total) {
+  typedef typename Mfma<TS>::frag frag;
+  constexpr int NT = 128 * WN, NW = 2 * WN;          // threads, waves (2 x WN)
+  constexpr int NI = BN / WN / 16, RJ = BR / 32;     // 16x16 blocks per wave
   constexpr int ROWB = kBK * 2;                      // bytes per LDS row (64)
   constexpr int STAGE = (BN + BR) * ROWB;            // bytes per stage
-  constexpr int LOADS = (BN + BR) / 16 / 4;          // 16-row loads per wave per stage
+  constexpr int LOADS = (BN + BR) / 16 / NW;         // 16-row loads per wave per stage
   constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
-  constexpr int OUT_BYTES = BR * OUT_STRIDE * 2;
+  // the output tile is staged through the ring in one pass, or in two
+  // passes of BR/2 rows when the whole tile does not fit
+  constexpr int OUT_PASSES = BR * OUT_STRIDE * 2 <= S * STAGE ? 1 : 2;
+  constexpr int OUT_BYTES = BR / OUT_PASSES * OUT_STRIDE * 2;
   constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
-  static_assert((BN + BR) % 64 == 0, "loads must split evenly over 4 waves");
-  static_assert(S >= 2 && S <= 8, "stages");
+  static_assert((BN + BR) % (16 * NW) == 0, "loads must split evenly over the waves");
+  static_assert(BN % (16 * WN) == 0 && BR % 32 == 0, "tile shape");
+  static_assert(S >= 2 && S <= 4, "stages");
   __shared__ __align__(16) unsigned char smem[SMEM];
 
   const int tile = xcd_tile(blockIdx.x, tiles_total);
   const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
   const int64_t r0 = (int64_t)tr * BR;
   const int n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave & 1, wr = wave >> 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave % WN, wr = wave / WN;
 
-  // this lane's source rows for each of its wave's loads (clamped in range:
-  // rows past the end are loaded but never stored)
-  const TS *src[LOADS];
-  int dst_off[LOADS];
+  // operand windows: W rows [n0, n0 + min(BN, N - n0)), X rows [r0, r0 + min(BR, R - r0))
+  const int w_rows = N - n0 < BN ? N - n0 : BN;
+  const int x_rows = R - r0 < BR ? (int)(R - r0) : BR;
+  const TS *wbase = W + (int64_t)n0 * K, *xbase = X + r0 * K;
+  const int wbytes = w_rows * K * 2, xbytes = x_rows * K * 2;
+
+  int voff[LOADS];
 #pragma unroll
   for (int u = 0; u < LOADS; ++u) {
     const int ins = wave * LOADS + u;
     const int row16 = lane >> 2, slot = lane & 3;
     const int chunk = slot ^ lds_swz(row16);
-    if (ins < BN / 16) {
-      int n = n0 + ins * 16 + row16;
-      n = n < N ? n : N - 1;
-      src[u] = W + (int64_t)n * K + chunk * 8;
-      dst_off[u] = ins * 16 * ROWB;
-    } else {
-      int64_t r = r0 + (ins - BN / 16) * 16 + row16;
-      r = r < R ? r : R - 1;
-      src[u] = X + r * K + chunk * 8;
-      dst_off[u] = BN * ROWB + (ins - BN / 16) * 16 * ROWB;
-    }
+    const int row = (ins < BN / 16 ? ins : ins - BN / 16) * 16 + row16;
+    voff[u] = (row * K + chunk * 8) * 2;
   }
   auto issue = [&](int ks, int stage) {
 #pragma unroll
-    for (int u = 0; u < LOADS; ++u)
-      __builtin_amdgcn_global_load_lds(static_cast<const void *>(src[u] + ks * kBK),
-                                       (lds_void *)(smem + stage * STAGE + dst_off[u]), 16, 0, 0);
+    for (int u = 0; u < LOADS; ++u) {
+      const int ins = wave * LOADS + u;
+      const int dst = ins < BN / 16 ? ins * 16 * ROWB : BN * ROWB + (ins - BN / 16) * 16 * ROWB;
+      const bool is_w = ins < BN / 16;
+      buffer_load_lds16(is_w ? static_cast<const void *>(wbase) : static_cast<const void *>(xbase),
+                        is_w ? wbytes : xbytes, smem + stage * STAGE + dst, voff[u], ks * (kBK * 2));
+    }
   };
 
+  // bias of this lane's output features (clamped; features past N are not
+  // stored) becomes the accumulators' starting value
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
   f32x4 acc[NI][RJ];
 #pragma unroll
-  for (int i = 0; i < NI; ++i)
+  for (int i = 0; i < NI; ++i) {
+    f32x4 bv;
 #pragma unroll
-    for (int j = 0; j < RJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < 4; ++e) {
+      const int n = n0 + wn * (BN / WN) + i * 16 + dn + e;
+      bv[e] = bias[n < N ? n : N - 1];
+    }
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) acc[i][j] = bv;
+  }
 
   const int ksteps = K / kBK;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < ksteps) issue(st, st);
 
-  // bias of this lane's output features, loaded now so that its latency
-  // hides behind the K loop (indices clamped; features past N are not stored)
-  const int dn = (lane >> 4) * 4, dr = lane & 15;
-  float bv[NI][4];
-#pragma unroll
-  for (int i = 0; i < NI; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int n = n0 + wn * (BN / 2) + i * 16 + dn + e;
-      bv[i][e] = bias[n < N ? n : N - 1];
-    }
-
   const int frow = lane & 15, fc = lane >> 4;
-  const int a_off = (wn * (BN / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
+  const int a_off = (wn * (BN / WN) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
   const int b_off = BN * ROWB + (wr * (BR / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
-  int stage = 0;
-  for (int ks = 0; ks < ksteps; ++ks) {
-    // stage ks must have landed: later stages issued so far = min(S-2, ksteps-1-ks)
-    const int later = ksteps - 1 - ks;
-    wait_stages<LOADS, S - 2>(later);
-    compiler_fence();
-    __builtin_amdgcn_s_barrier();
-    compiler_fence();
-    if (ks + S - 1 < ksteps) {
-      int st = stage + S - 1;
-      st = st >= S ? st - S : st;
-      issue(ks + S - 1, st);
+  for (int kb = 0; kb < ksteps; kb += S) {
+#pragma unroll
+    for (int st = 0; st < S; ++st) {
+      const int ks = kb + st;
+      if (ks < ksteps) {
+        // stage ks must have landed: later stages issued so far = min(S-2, ksteps-1-ks)
+        wait_stages<LOADS, S - 2>(ksteps - 1 - ks);
+        compiler_fence();
+        __builtin_amdgcn_s_barrier();
+        compiler_fence();
+        if (ks + S - 1 < ksteps) issue(ks + S - 1, (st + S - 1) % S);
+        const unsigned char *base = smem + st * STAGE;
+        frag fa[NI];
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+          fa[i] = *reinterpret_cast<const frag *>(base + a_off + i * 16 * ROWB);
+#pragma unroll
+        for (int j = 0; j < RJ; ++j) {
+          const frag fb = *reinterpret_cast<const frag *>(base + b_off + j * 16 * ROWB);
+#pragma unroll
+          for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+        }
+      }
     }
-    const unsigned char *base = smem + stage * STAGE;
-    frag fa[NI];
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-      fa[i] = *reinterpret_cast<const frag *>(base + a_off + i * 16 * ROWB);
-#pragma unroll
-    for (int j = 0; j < RJ; ++j) {
-      const frag fb = *reinterpret_cast<const frag *>(base + b_off + j * 16 * ROWB);
-#pragma unroll
-      for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
-    }
-    stage = stage + 1 == S ? 0 : stage + 1;
   }
 
-  // epilogue: bias + ReLU, round, stage the tile in LDS, write rows with
-  // 16-byte stores.  lane holds D[4*(lane/16) + e][lane % 16] of each block.
+  // epilogue: round, ReLU, stage the tile in LDS, write rows with 16-byte
+  // stores.  lane holds D[4*(lane/16) + e][lane % 16] of each block.
   wait_vm<0>();
   compiler_fence();
   __builtin_amdgcn_s_barrier();
   compiler_fence();
   uint16_t *sout = reinterpret_cast<uint16_t *>(smem);
+  constexpr int PR = BR / OUT_PASSES;   // rows per pass
+  constexpr int CPRW = BN / 8;          // 16-byte chunks per output row
 #pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const int nl = wn * (BN / 2) + i * 16 + dn;
+  for (int pass = 0; pass < OUT_PASSES; ++pass) {
+    if (OUT_PASSES == 1 || wr == pass) {
 #pragma unroll
-    for (int j = 0; j < RJ; ++j) {
-      const int rl = wr * (BR / 2) + j * 16 + dr;
-      float o[4];
+      for (int i = 0; i < NI; ++i) {
+        const int nl = wn * (BN / WN) + i * 16 + dn;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float t = acc[i][j][e] + bv[i][e];
-        o[e] = t > 0.0f ? t : 0.0f;
+        for (int j = 0; j < RJ; ++j) {
+          const int rl = (OUT_PASSES == 1 ? wr * (BR / 2) : 0) + j * 16 + dr;
+          uint2 packed;
+          packed.x = relu_bits2(round2<TS>(acc[i][j][0], acc[i][j][1]));
+          packed.y = relu_bits2(round2<TS>(acc[i][j][2], acc[i][j][3]));
+          *reinterpret_cast<uint2 *>(sout + rl * OUT_STRIDE + nl) = packed;
+        }
       }
-      uint2 packed;
-      packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
-      packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
-      *reinterpret_cast<uint2 *>(sout + rl * OUT_STRIDE + nl) = packed;
     }
-  }
-  compiler_fence();
-  __syncthreads();
-  constexpr int CPRW = BN / 8;  // 16-byte chunks per output row
-  for (int idx = tid; idx < BR * CPRW; idx += 256) {
-    const int rl = idx / CPRW, c = idx - rl * CPRW;
-    const int64_t r = r0 + rl;
-    const int n = n0 + c * 8;
-    if (r < R && n < N)
-      *reinterpret_cast<uint4 *>(Y + r * N + n) =
-          *reinterpret_cast<const uint4 *>(sout + rl * OUT_STRIDE + c * 8);
+    compiler_fence();
+    __syncthreads();
+    for (int idx = tid; idx < PR * CPRW; idx += NT) {
+      const int rl = idx / CPRW, c = idx - rl * CPRW;
+      const int64_t r = r0 + pass * PR + rl;
+      const int n = n0 + c * 8;
+      if (r < R && n < N)
+        *reinterpret_cast<uint4 *>(Y + r * N + n) =
+            *reinterpret_cast<const uint4 *>(sout + rl * OUT_STRIDE + c * 8);
+    }
+    if (pass + 1 < OUT_PASSES) {
+      compiler_fence();
+      __syncthreads();
+    }
   }
 }
 
@@ -653,15 +705,15 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
   return hipGetLastError();
 }
 
-template <typename TS, int BR, int BN, int S>
-static hipError_t dense_pipe_t(const void *x, const void *w, const float *b, void *y, int64_t R,
-                               int N, int K, hipStream_t s) {
+template <typename TS, int BR, int BN, int S, int WN, int MINW>
+static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void *y, int64_t R,
+                              int N, int K, hipStream_t s) {
   const int tiles_n = (N + BN - 1) / BN;
   const int64_t tiles_r = (R + BR - 1) / BR;
   const int64_t total = tiles_r * tiles_n;
   if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_relu_pipe_kernel<TS, BR, BN, S>), dim3((unsigned)total), dim3(256), 0, s,
-                     static_cast<const TS *>(x), static_cast<const TS *>(w), b,
+  hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW>), dim3((unsigned)total),
+                     dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
                      static_cast<TS *>(y), R, N, K, tiles_n, (int)total);
   return hipGetLastError();
 }
@@ -670,12 +722,14 @@ template <typename TS>
 static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, void *y, int64_t R,
                                 int N, int K, hipStream_t s) {
   if (K % kBK == 0 && N % 8 == 0) {
-    // large batches: 256-row tiles; small ones (a single request of a few
-    // thousand ads) would leave most CUs idle, so use 64 x 64 tiles
+    // large batches: 256 x 256 tiles over 8 waves (256 x 128 or 256 x 64
+    // over 4 waves for narrower layers); small ones (a single request of a
+    // few thousand ads) would leave most CUs idle, so use 64 x 64 tiles
     const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
-    if (big_tiles < 256) return dense_pipe_t<TS, 64, 64, 3>(x, w, b, y, R, N, K, s);
-    if (N % 128 == 0) return dense_pipe_t<TS, 256, 128, 3>(x, w, b, y, R, N, K, s);
-    return dense_pipe_t<TS, 256, 64, 3>(x, w, b, y, R, N, K, s);
+    if (big_tiles < 256) return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
+    if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
   }
   if (N % 128 == 0) return dense_mfma_t<TS, 256, 128>(x, w, b, y, R, N, K, s);
   return dense_mfma_t<TS, 256, 64>(x, w, b, y, R, N, K, s);
