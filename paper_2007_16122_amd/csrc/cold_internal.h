@@ -132,8 +132,20 @@ __device__ __forceinline__ int32_t resolve_row(const void *ids, int64_t i, int g
 }
 
 // ------------------------------------------------------------ kernel params
+// floor(n / d) for 0 <= n < 2^16 and 1 <= d < 2^16, from m = div_magic(d):
+// with m = ceil(2^32 / d), n m / 2^32 exceeds n / d by less than n / 2^32,
+// which is below 1 / d while n d < 2^32, so the floor is exact; d = 1 is m = 0
+__host__ __device__ inline uint32_t div_magic(uint32_t d) {
+  return d <= 1 ? 0u : (uint32_t)(0xFFFFFFFFull / d + 1);
+}
+__device__ __forceinline__ int fast_div(int n, uint32_t m) {
+  return m ? (int)__umulhi((uint32_t)n, m) : n;
+}
+
 struct GatherArgs {
   int32_t M, n_user, n_seq, n_ad, n_cross, d, H;
+  int32_t Mp, Hp;                 // M and H rounded up to multiples of 4 (LDS row strides)
+  uint32_t mg_tw, mg_h, mg_m, mg_ns, mg_sd4;   // div_magic of rows_per_tile, H, M, n_seq, n_seq*d/4
   int32_t rows_per_tile;          // rows per wave (set by the launcher)
   int32_t wave_lds_bytes;         // LDS per wave (set by the launcher)
   int32_t se_lds_bytes;           // LDS for SE parameters, 0 if read from global

@@ -148,18 +148,25 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int M = a.M, d = a.d, H = a.H;
+  const int Mp = a.Mp, Hp = a.Hp;          // padded LDS row strides (z, hidden, SE weights)
   const int nus = a.n_user + a.n_seq, nax = a.n_ad + a.n_cross;
   const int Tw = a.rows_per_tile;          // rows per wave
   const int CPG = d / EPC;                 // chunks per group (power of two)
   const int CPR = M * CPG;                 // chunks per row
   const int lcpg = __builtin_ctz(CPG);
+  const float inv_d = 1.0f / (float)d;     // exact: d is a power of two
   const int64_t R = a.R, Q = a.Q;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // (row, chunk) of this lane's first chunk; later chunks step by 64
+  // (row, chunk) of this lane's first chunk; later chunks step by 64 =
+  // q64 rows + r64 chunks, so one step wraps at most once more
   const int t_first = lane / CPR, c_first = lane - t_first * CPR;
+  const int q64 = 64 / CPR, r64 = 64 - q64 * CPR;
   auto advance = [&](int &t, int &c) {
-    c += 64;
-    while (c >= CPR) { c -= CPR; ++t; }
+    c += r64;
+    t += q64;
+    const bool wrap = c >= CPR;
+    c = wrap ? c - CPR : c;
+    t = wrap ? t + 1 : t;
   };
 
   // ---- block-wide: per-group table metadata and (when small) SE parameters in LDS
@@ -217,13 +224,20 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   const float *w1 = a.w1, *b1 = a.b1, *w2 = a.w2, *b2 = a.b2;
   if constexpr ((MODE == kFull || MODE == kWeightsOnly) && SE_LDS) {
     {
+      // W1 [H][Mp], W2 [M][Hp] (rows 16-byte aligned, padding zero), b1 [H], b2 [M]
       float *sw = reinterpret_cast<float *>(cursor);
-      const int nw = H * M;
-      for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[i] = a.w1[i];
-      for (int i = threadIdx.x; i < H; i += kGatherThreads) sw[nw + i] = a.b1[i];
-      for (int i = threadIdx.x; i < nw; i += kGatherThreads) sw[nw + H + i] = a.w2[i];
-      for (int i = threadIdx.x; i < M; i += kGatherThreads) sw[2 * nw + H + i] = a.b2[i];
-      w1 = sw; b1 = sw + nw; w2 = sw + nw + H; b2 = sw + 2 * nw + H;
+      float *sw2 = sw + H * Mp, *sb1 = sw2 + M * Hp, *sb2 = sb1 + H;
+      for (int i = threadIdx.x; i < H * Mp; i += kGatherThreads) {
+        const int j = i / Mp, g = i - j * Mp;
+        sw[i] = g < M ? a.w1[j * M + g] : 0.0f;
+      }
+      for (int i = threadIdx.x; i < M * Hp; i += kGatherThreads) {
+        const int g = i / Hp, j = i - g * Hp;
+        sw2[i] = j < H ? a.w2[g * H + j] : 0.0f;
+      }
+      for (int i = threadIdx.x; i < H; i += kGatherThreads) sb1[i] = a.b1[i];
+      for (int i = threadIdx.x; i < M; i += kGatherThreads) sb2[i] = a.b2[i];
+      w1 = sw; b1 = sb1; w2 = sw2; b2 = sb2;
       cursor += a.se_lds_bytes;
     }
   }
@@ -231,12 +245,13 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
 
   unsigned char *wb = cursor + (size_t)wave * a.wave_lds_bytes;
   const int ns = a.n_seq, nu = a.n_user;
-  float *ust = reinterpret_cast<float *>(wb);              // [Tw][ns*d] pooled sequence rows
-  int32_t *ridx = reinterpret_cast<int32_t *>(ust + Tw * ns * d);  // [Tw][nax]
+  // 16-byte aligned first: z and hid are read as float4 rows
+  float *z = reinterpret_cast<float *>(wb);                // [Tw][Mp] squeeze
+  float *hid = z + Tw * Mp;                                // [Tw][Hp] SE hidden layer
+  float *ust = hid + Tw * Hp;                              // [Tw][ns*d] pooled sequence rows
+  float *sv = ust + Tw * ns * d;                           // [Tw][M] SE weights
+  int32_t *ridx = reinterpret_cast<int32_t *>(sv + Tw * M);  // [Tw][nax]
   int32_t *rq = ridx + Tw * nax;                           // [Tw]
-  float *z = reinterpret_cast<float *>(rq + Tw);           // [Tw][M]
-  float *sv = z + Tw * M;                                  // [Tw][M]
-  float *hid = sv + Tw * M;                                // [Tw][H]
   const TS *Uh = static_cast<const TS *>(a.Uh);
 
   // persistent: each wave walks the row tiles wave_id, wave_id + waves, ...
@@ -259,7 +274,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     const int i = ln + 64 * k;
     idv[k] = 0;
     if (i < Tw * nax) {
-      const int f = i / Tw, t = i - f * Tw;
+      const int f = fast_div(i, a.mg_tw), t = i - f * Tw;
       const int64_t r = r0 + t;
       if (r < R) {
         const bool is_ad = f < a.n_ad;
@@ -282,7 +297,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   for (int k = 0; k < IDMAX; ++k) {
     const int i = ln + 64 * k;
     if (i < Tw * nax) {
-      const int f = i / Tw, t = i - f * Tw;
+      const int f = fast_div(i, a.mg_tw), t = i - f * Tw;
       const int64_t r = r0 + t;
       const int g = nus + f;
       int32_t row = -1;
@@ -324,20 +339,20 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   //      exceed the storage range), squeeze of the user groups
   const int sd4 = ns * d / 4;
   for (int i = ln; i < Tw * sd4; i += 64) {
-    const int t = i / sd4, k4 = i - t * sd4;
+    const int t = fast_div(i, a.mg_sd4), k4 = i - t * sd4;
     reinterpret_cast<float4 *>(ust)[i] =
         reinterpret_cast<const float4 *>(a.U + ((int64_t)rq[t] * nus + nu) * d)[k4];
   }
   if constexpr (MODE == kFull || MODE == kWeightsOnly) {   // squeeze of the pooled sequences
     for (int i = ln; i < Tw * ns; i += 64) {
-      const int t = i / ns, g = nu + (i - t * ns);
-      z[t * M + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
+      const int t = fast_div(i, a.mg_ns), g = nu + (i - t * ns);
+      z[t * Mp + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
     }
   }
   wave_sync();
   if (MODE != kApplyWeights && a.rows_out) {
     for (int i = ln; i < Tw * nus; i += 64) {
-      const int f = i / Tw, t = i - f * Tw;
+      const int f = fast_div(i, a.mg_tw), t = i - f * Tw;
       const int64_t r = r0 + t;
       if (r < R)
         a.rows_out[(int64_t)f * R + r] =
@@ -350,6 +365,8 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   uint4 raw[CPT];
   {
     int t = tf, c = cf;
+  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
+    asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
       const int g = c >> lcpg, p = c & (CPG - 1);
@@ -375,6 +392,8 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   }
   if constexpr (MODE == kFull || MODE == kWeightsOnly) {
     int t = tf, c = cf;
+  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
+    asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
     for (int j = 0; j < CPT; ++j, advance(t, c)) {
       const int g = c >> lcpg, p = c & (CPG - 1);
@@ -383,36 +402,76 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       float part = 0.0f;
 #pragma unroll
       for (int e = 0; e < EPC; ++e) part += v[e];
-      for (int o = 1; o < CPG; o <<= 1) part += __shfl_xor(part, o);
-      if (t < Tw && p == 0 && (g < nu || g >= nus)) z[t * M + g] = r0 + t < R ? part / (float)d : 0.0f;
+      // butterfly over the CPG lanes of the group (offsets are constants;
+      // CPG <= 64 is a power of two)
+      if (CPG > 1) part += __shfl_xor(part, 1);
+      if (CPG > 2) part += __shfl_xor(part, 2);
+      if (CPG > 4) part += __shfl_xor(part, 4);
+      if (CPG > 8) part += __shfl_xor(part, 8);
+      if (CPG > 16) part += __shfl_xor(part, 16);
+      if (CPG > 32) part += __shfl_xor(part, 32);
+      if (t < Tw && p == 0 && (g < nu || g >= nus)) z[t * Mp + g] = r0 + t < R ? part * inv_d : 0.0f;
     }
     wave_sync();
 
     // ---- SE block of the wave's rows (Eq. 2)
+    // sums from the bias in index order; from LDS, weight and input rows are
+    // read four at a time (rows padded to Mp / Hp); from global memory, the
+    // weights keep their unpadded [H][M] / [M][H] layout
     for (int it = ln; it < Tw * H; it += 64) {
-      const int t = it / H, jh = it - t * H;
-      const float *w = w1 + jh * M;
-      const float *zt = z + t * M;
+      const int t = fast_div(it, a.mg_h), jh = it - t * H;
+      const float *zt = z + t * Mp;
       float acc = b1[jh];
+      if constexpr (SE_LDS) {
+        const float *w = w1 + jh * Mp;
+        int g = 0;
+#pragma unroll 1
+        for (; g + 4 <= M; g += 4) {
+          const float4 wv = *reinterpret_cast<const float4 *>(w + g);
+          const float4 zv = *reinterpret_cast<const float4 *>(zt + g);
+          acc += wv.x * zv.x;
+          acc += wv.y * zv.y;
+          acc += wv.z * zv.z;
+          acc += wv.w * zv.w;
+        }
+        for (; g < M; ++g) acc += w[g] * zt[g];
+      } else {
+        const float *w = w1 + jh * M;
 #pragma unroll 8
-      for (int g = 0; g < M; ++g) acc += w[g] * zt[g];
-      hid[it] = acc > 0.0f ? acc : 0.0f;
+        for (int g = 0; g < M; ++g) acc += w[g] * zt[g];
+      }
+      hid[t * Hp + jh] = acc > 0.0f ? acc : 0.0f;
     }
     wave_sync();
     for (int it = ln; it < Tw * M; it += 64) {
-      const int t = it / M, g = it - t * M;
-      const float *w = w2 + g * H;
-      const float *ht = hid + t * H;
+      const int t = fast_div(it, a.mg_m), g = it - t * M;
+      const float *ht = hid + t * Hp;
       float acc = b2[g];
+      if constexpr (SE_LDS) {
+        const float *w = w2 + g * Hp;
+        int jh = 0;
+#pragma unroll 1
+        for (; jh + 4 <= H; jh += 4) {
+          const float4 wv = *reinterpret_cast<const float4 *>(w + jh);
+          const float4 hv = *reinterpret_cast<const float4 *>(ht + jh);
+          acc += wv.x * hv.x;
+          acc += wv.y * hv.y;
+          acc += wv.z * hv.z;
+          acc += wv.w * hv.w;
+        }
+        for (; jh < H; ++jh) acc += w[jh] * ht[jh];
+      } else {
+        const float *w = w2 + g * H;
 #pragma unroll 8
-      for (int jh = 0; jh < H; ++jh) acc += w[jh] * ht[jh];
+        for (int jh = 0; jh < H; ++jh) acc += w[jh] * ht[jh];
+      }
       const float sg = 1.0f / (1.0f + expf(-acc));
       sv[it] = sg;
       if (a.s_buf && r0 + t < R) a.s_buf[r0 * M + it] = sg;
     }
   } else if constexpr (MODE == kApplyWeights) {
     for (int it = ln; it < Tw * M; it += 64) {
-      const int t = it / M, g = it - t * M;
+      const int t = fast_div(it, a.mg_m), g = it - t * M;
       float sg = 0.0f;
       if (r0 + t < R && (!a.mask || a.mask[(int64_t)rq[t] * M + g])) sg = a.s_buf[r0 * M + it];
       sv[it] = sg;
@@ -423,6 +482,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   //      are fp32 sums), for an SE computed by a separate dense layer
   float *E = static_cast<float *>(a.X);
   int t = tf, c = cf;
+  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
   for (int j = 0; j < CPT; ++j, advance(t, c)) {
     const int i = ln + 64 * j;
@@ -448,6 +508,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   // ---- reweight, linear_log, round once, coalesced store
   TS *X = static_cast<TS *>(a.X);
   int t = tf, c = cf;
+  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
   for (int j = 0; j < CPT; ++j, advance(t, c)) {
     const int i = ln + 64 * j;
@@ -598,15 +659,21 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   const int64_t t_fill = (a.R + 1023) / 1024;
   const int T = t_fill < t_max ? (t_fill < 1 ? 1 : (int)t_fill) : t_max;
   a.rows_per_tile = T;
-  a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * a.n_seq * a.d +
-                                sizeof(int32_t) * (size_t)(T * nax + T) +
-                                sizeof(float) * (size_t)(2 * T * a.M + T * a.H) + 15) / 16 * 16);
+  a.Mp = (a.M + 3) & ~3;
+  a.Hp = (a.H + 3) & ~3;
+  a.mg_tw = div_magic((uint32_t)T);
+  a.mg_h = div_magic((uint32_t)a.H);
+  a.mg_m = div_magic((uint32_t)a.M);
+  a.mg_ns = div_magic((uint32_t)(a.n_seq > 0 ? a.n_seq : 1));
+  a.mg_sd4 = div_magic((uint32_t)(a.n_seq > 0 ? a.n_seq * a.d / 4 : 1));
+  a.wave_lds_bytes = (int32_t)((sizeof(float) * (size_t)T * (a.Mp + a.Hp + a.n_seq * a.d + a.M) +
+                                sizeof(int32_t) * (size_t)(T * nax + T) + 15) / 16 * 16);
   a.meta_lds_bytes = (int32_t)((24 * (size_t)a.M + 15) / 16 * 16);
   a.req_lds_bytes = a.Q + 1 <= kGatherMaxReqLds ? (int32_t)((4 * (a.Q + 1) + 15) / 16 * 16) : 0;
   a.users_in_lds = user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a) ? 0 : 1;
   a.urow_lds_bytes = a.users_in_lds ? (int32_t)((4 * (int64_t)a.n_user * a.Q + 15) / 16 * 16) : 0;
   a.uval_lds_bytes = a.users_in_lds ? (int32_t)((int64_t)a.n_user * a.Q * a.d * sizeof(TS)) : 0;
-  const size_t se_floats = 2 * (size_t)a.H * a.M + a.H + a.M;
+  const size_t se_floats = (size_t)a.H * a.Mp + (size_t)a.M * a.Hp + a.H + a.M;
   a.se_in_lds = (MODE == kFull || MODE == kWeightsOnly) && se_floats * sizeof(float) <= 24 * 1024;
   a.se_lds_bytes = a.se_in_lds ? (int32_t)((se_floats * sizeof(float) + 15) / 16 * 16) : 0;
   const size_t shmem = (size_t)a.meta_lds_bytes + a.req_lds_bytes + a.urow_lds_bytes +
