@@ -242,36 +242,34 @@ __device__ __forceinline__ uint32_t round2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2>
-__global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
-                                                                     const TS *__restrict__ W,
-                                                                     const float *__restrict__ bias,
-                                                                     TS *__restrict__ Y, int64_t R,
-                                                                     int N, int K, int tiles_n,
-                                                                     int tiles_total) {
-  typedef typename Mfma<TS>::frag frag;
-  constexpr int NT = 128 * WN, NW = 2 * WN;          // threads, waves (2 x WN)
-  constexpr int NI = BN / WN / 16, RJ = BR / 32;     // 16x16 blocks per wave
-  constexpr int ROWB = kBK * 2;                      // bytes per LDS row (64)
-  constexpr int STAGE = (BN + BR) * ROWB;            // bytes per stage
-  constexpr int LOADS = (BN + BR) / 16 / NW;         // 16-row loads per wave per stage
-  constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
-  // the output tile is staged through the ring in one pass, or in two
-  // passes of BR/2 rows when the whole tile does not fit
-  constexpr int OUT_PASSES = BR * OUT_STRIDE * 2 <= S * STAGE ? 1 : 2;
-  constexpr int OUT_BYTES = BR / OUT_PASSES * OUT_STRIDE * 2;
-  constexpr int SMEM = S * STAGE > OUT_BYTES ? S * STAGE : OUT_BYTES;
+// Tile geometry of the pipelined layer: BR x BN outputs over 2 x WN waves.
+template <int BR, int BN, int S, int WN> struct BufTile {
+  static constexpr int NT = 128 * WN, NW = 2 * WN;          // threads, waves
+  static constexpr int NI = BN / WN / 16, RJ = BR / 32;     // 16x16 blocks per wave
+  static constexpr int ROWB = kBK * 2;                      // bytes per LDS row (64)
+  static constexpr int STAGE = (BN + BR) * ROWB;            // bytes per ring stage
+  static constexpr int LOADS = (BN + BR) / 16 / NW;         // 16-row loads per wave per stage
+  static constexpr int RING = S * STAGE;
   static_assert((BN + BR) % (16 * NW) == 0, "loads must split evenly over the waves");
   static_assert(BN % (16 * WN) == 0 && BR % 32 == 0, "tile shape");
   static_assert(S >= 2 && S <= 4, "stages");
-  __shared__ __align__(16) unsigned char smem[SMEM];
+};
 
-  const int tile = xcd_tile(blockIdx.x, tiles_total);
-  const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
-  const int64_t r0 = (int64_t)tr * BR;
-  const int n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+// The K loop of one tile: acc[i][j] = bias + W X^T over K for the
+// (wn, wr) wave's blocks; lane holds D[4*(lane/16) + e][lane % 16] of block
+// (i, j), i.e. output features n0 + wn*(BN/WN) + 16 i + 4 (lane/16) + e of row
+// r0 + wr*(BR/2) + 16 j + lane % 16.  smem holds the ring (RING bytes); on
+// return the ring is free once the workgroup has passed a barrier.
+template <typename TS, int BR, int BN, int S, int WN>
+__device__ __forceinline__ void buf_tile_kloop(
+    const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
+    int N, int K, int64_t r0, int n0, unsigned char *smem,
+    f32x4 (&acc)[BufTile<BR, BN, S, WN>::NI][BufTile<BR, BN, S, WN>::RJ]) {
+  typedef typename Mfma<TS>::frag frag;
+  typedef BufTile<BR, BN, S, WN> G;
+  constexpr int NI = G::NI, RJ = G::RJ, ROWB = G::ROWB, STAGE = G::STAGE, LOADS = G::LOADS;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave % WN, wr = wave / WN;
 
   // operand windows: W rows [n0, n0 + min(BN, N - n0)), X rows [r0, r0 + min(BR, R - r0))
@@ -302,8 +300,7 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
 
   // bias of this lane's output features (clamped; features past N are not
   // stored) becomes the accumulators' starting value
-  const int dn = (lane >> 4) * 4, dr = lane & 15;
-  f32x4 acc[NI][RJ];
+  const int dn = (lane >> 4) * 4;
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     f32x4 bv;
@@ -349,10 +346,40 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
       }
     }
   }
+  wait_vm<0>();
+}
+
+template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2>
+__global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
+                                                                     const TS *__restrict__ W,
+                                                                     const float *__restrict__ bias,
+                                                                     TS *__restrict__ Y, int64_t R,
+                                                                     int N, int K, int tiles_n,
+                                                                     int tiles_total) {
+  typedef BufTile<BR, BN, S, WN> G;
+  constexpr int NT = G::NT, NI = G::NI, RJ = G::RJ;
+  constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
+  // the output tile is staged through the ring in one pass, or in two
+  // passes of BR/2 rows when the whole tile does not fit
+  constexpr int OUT_PASSES = BR * OUT_STRIDE * 2 <= G::RING ? 1 : 2;
+  constexpr int OUT_BYTES = BR / OUT_PASSES * OUT_STRIDE * 2;
+  constexpr int SMEM = G::RING > OUT_BYTES ? G::RING : OUT_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+
+  const int tile = xcd_tile(blockIdx.x, tiles_total);
+  const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
+  const int64_t r0 = (int64_t)tr * BR;
+  const int n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave % WN, wr = wave / WN;
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+
+  f32x4 acc[NI][RJ];
+  buf_tile_kloop<TS, BR, BN, S, WN>(X, W, bias, R, N, K, r0, n0, smem, acc);
 
   // epilogue: round, ReLU, stage the tile in LDS, write rows with 16-byte
-  // stores.  lane holds D[4*(lane/16) + e][lane % 16] of each block.
-  wait_vm<0>();
+  // stores.
   compiler_fence();
   __builtin_amdgcn_s_barrier();
   compiler_fence();
