@@ -750,9 +750,13 @@ static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, vo
                                 int N, int K, hipStream_t s) {
   if (K % kBK == 0 && N % 8 == 0) {
     // large batches: 256 x 256 tiles over 8 waves (256 x 128 or 256 x 64
-    // over 4 waves for narrower layers); small ones (a single request of a
-    // few thousand ads) would leave most CUs idle, so use 64 x 64 tiles
+    // over 4 waves for narrower layers); batches of a few thousand ads
+    // would leave most CUs idle with those, so 128 x 128 tiles while they
+    // still number at least one per CU, else 64 x 64
     const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
+    const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
+    if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
+      return dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
     if (big_tiles < 256) return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
     if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
     if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
