@@ -654,9 +654,10 @@ static hipError_t gather_se_c(bool hashed, GatherArgs a, hipStream_t s) {
   const int nax = a.n_ad + a.n_cross;
   const int cpr = a.M * (a.d / EPC);
   // rows per wave: as many as the chunk budget allows, fewer for small
-  // batches so that at least ~1024 waves are launched
+  // batches so that about 2048 waves are launched (one 2,000-ad request:
+  // one row per wave)
   const int t_max = (64 * CPT) / cpr;
-  const int64_t t_fill = (a.R + 1023) / 1024;
+  const int64_t t_fill = (a.R + 2047) / 2048;
   const int T = t_fill < t_max ? (t_fill < 1 ? 1 : (int)t_fill) : t_max;
   a.rows_per_tile = T;
   a.Mp = (a.M + 3) & ~3;

@@ -186,6 +186,33 @@ def test_parity_full_size_sampled(name):
     assert np.all(np.isfinite(g["scores"]))
 
 
+@pytest.mark.parametrize("widths,n_req", [((768, 384, 320, 256, 128, 64, 2), 12),
+                                          ((768, 1024, 512, 256, 128, 64, 2), 3)])
+def test_parity_layer_tile_shapes(widths, n_req):
+    """The dense layer's other tile shapes: hidden widths that are multiples
+    of 128 but not 256 (384: 256 x 128 tiles) and of 64 but not 128 (320:
+    256 x 64 tiles) on a batch large enough for 256-row tiles, and a
+    6,000-row batch of the serving widths (128 x 128 tiles for the
+    1,024-wide layer, 64 x 64 for the others); ragged last row tiles;
+    checker on a seeded sample of rows."""
+    cfg = mid("serving_bf16", widths=widths, n_requests=n_req, cand_per_request=2000 - 7)
+    log(f"test_parity_layer_tile_shapes widths={widths} R={cfg.n_rows}")
+    tables, params, batch = problem(cfg, seed=29)
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True)
+    finally:
+        run.close()
+    rng = np.random.default_rng(31)
+    off = batch["req_off"]
+    sample = np.unique(np.concatenate([rng.choice(batch["n_rows"], 1500, replace=False),
+                                       off[:-1], off[1:] - 1]))
+    o = run_oracle(cfg, tables, params, batch, sample=sample, want_rows=True)
+    assert np.array_equal(g["rows"][:, sample], o["rows"].T.astype(np.int32))
+    compare_scores(cfg, g["scores"][sample], o["scores"], f"tile shapes {widths}")
+    assert np.all(np.isfinite(g["scores"]))
+
+
 def test_table_generator_device_matches_numpy():
     cfg = synth.CONFIGS["large_fp16_ll"]
     rows = np.array([0, 1, 12345, cfg.vocab - 1, 7_777_777])
