@@ -124,3 +124,24 @@ def compare_scores(cfg, got, want, label=""):
     assert np.all(np.isfinite(got)), "non-finite GPU score"
     assert stats["max"] <= tol, stats
     return stats
+
+
+def request_slice(cfg, batch, q):
+    """Request q of a host batch as a batch of its own."""
+    off = batch["req_off"]
+    lo, hi = int(off[q]), int(off[q + 1])
+    Q = len(off) - 1
+    out = dict(req_off=np.array([0, hi - lo], np.int32),
+               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q + 1]),
+               ad_ids=np.ascontiguousarray(batch["ad_ids"][:, lo:hi]),
+               cross_ids=np.ascontiguousarray(batch["cross_ids"][:, lo:hi]),
+               n_rows=hi - lo, n_requests=1)
+    if cfg.n_seq:
+        so = batch["seq_off"]
+        segs = [batch["seq_ids"][so[f * Q + q]:so[f * Q + q + 1]] for f in range(cfg.n_seq)]
+        out["seq_off"] = np.concatenate([[0], np.cumsum([len(x) for x in segs])]).astype(np.int32)
+        out["seq_ids"] = np.concatenate(segs)
+    else:
+        out["seq_off"] = np.zeros(1, np.int32)
+        out["seq_ids"] = np.zeros(0, batch["ad_ids"].dtype)
+    return out

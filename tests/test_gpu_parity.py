@@ -10,7 +10,7 @@ import pytest
 from paper_2007_16122_amd import binding, synth
 from tests.common import assert_se_weights_close, problem
 from tests.gpu_common import (GpuRun, compare_scores, device_table_from_numpy, log,
-                              run_oracle, sparse_host_tables)
+                              request_slice, run_oracle, sparse_host_tables)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -263,6 +263,28 @@ def test_user_broadcast_equals_per_row_bitwise():
     finally:
         run.close()
     assert np.array_equal(got, base)
+
+
+@pytest.mark.parametrize("name", ["serving_bf16", "multivalued_fp16_ll"])
+def test_request_alone_equals_batch_bitwise(name):
+    """A 2,000-ad request scored alone (small-batch layer tiles, one row per
+    gather wave, user rows staged by the gather) gives bit-identical scores
+    to the same request inside a 32-request batch (256 x 256 layer tiles,
+    five rows per wave, pooled user rows): every sum runs in the same order
+    whatever the launch shape, so a score does not depend on the batch."""
+    cfg = mid(name, n_requests=32, cand_per_request=2000)
+    log(f"test_request_alone_equals_batch_bitwise {name}: R={cfg.n_rows}")
+    tables, params, batch = problem(cfg, seed=33)
+    qs = [0, 17, 31]
+    run = load(cfg, tables, params)
+    try:
+        full = run.score(batch)["scores"]
+        alone = [run.score(request_slice(cfg, batch, q))["scores"] for q in qs]
+    finally:
+        run.close()
+    off = batch["req_off"]
+    for q, a in zip(qs, alone):
+        assert np.array_equal(a, full[off[q]:off[q + 1]]), f"request {q}"
 
 
 def test_zero_se_gives_exact_half():
