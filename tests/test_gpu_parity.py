@@ -186,6 +186,26 @@ def test_parity_full_size_sampled(name):
     assert np.all(np.isfinite(g["scores"]))
 
 
+@pytest.mark.parametrize("name", ["serving_bf16", "multivalued_fp16_ll"])
+def test_parity_odd_input_width(name):
+    """An odd number of groups (23 ad fields) makes the network input width a
+    multiple of 16 but not of 32, so the first layer runs on the
+    register-staged kernel (K not a multiple of the 32-deep K step);
+    mid-size ragged batch, every row checked."""
+    cfg = mid(name, n_ad=23)
+    assert cfg.d_in % 32 == 16
+    log(f"test_parity_odd_input_width {name}: D_in={cfg.d_in}")
+    tables, params, batch = problem(cfg, seed=35, cand=MID_CANDS[name])
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True)
+    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
+    compare_scores(cfg, g["scores"], o["scores"], f"odd input width {name}")
+
+
 @pytest.mark.parametrize("widths,n_req", [((768, 384, 320, 256, 128, 64, 2), 12),
                                           ((768, 1024, 512, 256, 128, 64, 2), 3)])
 def test_parity_layer_tile_shapes(widths, n_req):
