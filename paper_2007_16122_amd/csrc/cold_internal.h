@@ -45,11 +45,15 @@ template <> struct Elem<__bf16> {
     __bf16 b = static_cast<__bf16>(x);  // round to nearest even
     return __builtin_bit_cast(uint16_t, b);
   }
+  // pairs rounded by one vector conversion each (v_cvt_pk_bf16_f32), the same
+  // round-to-nearest-even as bits()
   __device__ static inline uint4 pack(const float *v) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
     uint32_t w[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      w[i] = (uint32_t)bits(v[2 * i]) | ((uint32_t)bits(v[2 * i + 1]) << 16);
+      w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){v[2 * i], v[2 * i + 1]}, b2));
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static inline float to_f32(__bf16 x) { return static_cast<float>(x); }
@@ -70,10 +74,12 @@ template <> struct Elem<_Float16> {
     return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));  // RNE, overflow -> inf
   }
   __device__ static inline uint4 pack(const float *v) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
     uint32_t w[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      w[i] = (uint32_t)bits(v[2 * i]) | ((uint32_t)bits(v[2 * i + 1]) << 16);
+      w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){v[2 * i], v[2 * i + 1]}, h2));
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static inline float to_f32(_Float16 x) { return static_cast<float>(x); }

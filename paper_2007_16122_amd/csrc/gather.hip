@@ -259,6 +259,8 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   const int64_t stride = (int64_t)gridDim.x * (kGatherThreads / 64);
   for (int64_t wt = (int64_t)blockIdx.x * (kGatherThreads / 64) + wave; wt < n_tiles; wt += stride) {
   const int64_t r0 = wt * Tw;
+  // rows of this tile that exist: t < tv is t < Tw && r0 + t < R
+  const int tv = R - r0 < Tw ? (int)(R - r0) : Tw;
   // chunk coordinates, opaque to the compiler so that nothing derived from
   // them is hoisted out of the tile loop (which would pin registers)
   int tf = t_first, cf = c_first, ln = lane;
@@ -371,7 +373,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     for (int j = 0; j < CPT; ++j) {
       const int g = c >> lcpg, p = c & (CPG - 1);
       raw[j] = make_uint4(0, 0, 0, 0);
-      if (t < Tw && r0 + t < R && (g < nu || g >= nus)) {
+      if (t < tv && (g < nu || g >= nus)) {
         uint64_t addr = 0;
         if (g < nu) {
           bool keep = true;
@@ -410,7 +412,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       if (CPG > 8) part += __shfl_xor(part, 8);
       if (CPG > 16) part += __shfl_xor(part, 16);
       if (CPG > 32) part += __shfl_xor(part, 32);
-      if (t < Tw && p == 0 && (g < nu || g >= nus)) z[t * Mp + g] = r0 + t < R ? part * inv_d : 0.0f;
+      if (t < Tw && p == 0 && (g < nu || g >= nus)) z[t * Mp + g] = t < tv ? part * inv_d : 0.0f;
     }
     wave_sync();
 
@@ -487,7 +489,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   for (int j = 0; j < CPT; ++j, advance(t, c)) {
     const int i = ln + 64 * j;
     const int g = c >> lcpg, p = c & (CPG - 1);
-    if (t < Tw && r0 + t < R) {
+    if (t < tv) {
       float v[EPC];
       if (g >= nu && g < nus) {
         const float *src = ust + t * ns * d + (g - nu) * d + p * EPC;
@@ -513,7 +515,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   for (int j = 0; j < CPT; ++j, advance(t, c)) {
     const int i = ln + 64 * j;
     const int g = c >> lcpg, p = c & (CPG - 1);
-    if (t < Tw && r0 + t < R) {
+    if (t < tv) {
       const float sg = sv[t * M + g];
       float v[EPC];
       if (g >= nu && g < nus) {
