@@ -333,9 +333,15 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
       {al.b1, w->se_b1, sizeof(float) * (m->literal_se ? m->M : m->H), hipMemcpyDeviceToDevice},
       {al.w2, w->se_w2, m->literal_se ? 0 : sizeof(float) * m->M * m->H, hipMemcpyDeviceToDevice},
       {al.b2, w->se_b2, m->literal_se ? 0 : sizeof(float) * m->M, hipMemcpyDeviceToDevice}};
+  // the fused tail's two hidden layers are stored fragment-major; every
+  // other weight matrix is copied as given
+  const bool fuse_tail = L >= 3 && tail_supported(m->dtype, m->widths[L - 3], m->widths[L - 2],
+                                                  m->widths[L - 1], m->widths[L]);
+  auto packed = [&](int l) { return fuse_tail && (l == L - 3 || l == L - 2); };
   for (int l = 0; l < L; ++l) {
-    copies.push_back({al.w[l], w->mlp_w[l], (size_t)m->es * m->widths[l] * m->widths[l + 1],
-                      hipMemcpyDeviceToDevice});
+    if (!packed(l))
+      copies.push_back({al.w[l], w->mlp_w[l], (size_t)m->es * m->widths[l] * m->widths[l + 1],
+                        hipMemcpyDeviceToDevice});
     copies.push_back({al.b[l], w->mlp_b[l], sizeof(float) * m->widths[l + 1], hipMemcpyDeviceToDevice});
   }
   for (const Copy &c : copies) {
@@ -343,6 +349,11 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
     hipError_t e = hipMemcpyAsync(A + c.off, c.src, c.bytes, c.kind, s);
     if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: copy");
   }
+  for (int l = 0; l < L; ++l)
+    if (packed(l)) {
+      hipError_t e = launch_pack_frag(w->mlp_w[l], A + al.w[l], m->widths[l + 1], m->widths[l], s);
+      if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: pack");
+    }
   hipError_t e = hipStreamSynchronize(s);  // host staging must outlive the copies
   if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: synchronize");
   m->arena_ptr = A;

@@ -203,6 +203,9 @@ hipError_t launch_clear_flag(int32_t *err, hipStream_t s);
 hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
                              int64_t R, int32_t N, int32_t K, hipStream_t s);
 bool tail_supported(int dtype, int K0, int N1, int N2, int n_out);
+// the fused tail reads its two hidden layers' weights fragment-major
+// (mlp.hip, frag_offset): [N][K] row-major -> that order (N % 16 == 0, K % 32 == 0)
+hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hipStream_t s);
 hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float *b1,
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s);

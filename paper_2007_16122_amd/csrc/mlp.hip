@@ -419,13 +419,44 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
   }
 }
 
+// Fragment-major weights of the fused tail: a [N][K] matrix (N % 16 == 0,
+// K % 32 == 0) stored as one 1 KB block per (16-feature block fb, 32-deep K
+// step k), in MFMA operand order: lane l holds features fb*16 + l % 16, K
+// elements 32 k + 8 (l / 16) .. + 8.  A wave then loads a fragment as one
+// contiguous 1 KB block instead of 16 half-used cache lines.
+__host__ __device__ inline int64_t frag_offset(int fb, int k, int ksteps, int lane) {
+  return ((int64_t)(fb * ksteps + k) * 64 + lane) * 8;
+}
+
+// one 16-byte chunk per thread: row-major chunk (n, k..k+7) to its fragment-major place
+__global__ __launch_bounds__(256) void pack_frag_kernel(const uint4 *__restrict__ src,
+                                                        uint4 *__restrict__ dst, int64_t N, int32_t K) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t cpr = K / 8;
+  if (c >= N * cpr) return;
+  const int64_t n = c / cpr;
+  const int k = (int)(c - n * cpr) * 8;
+  const int lane = ((k & 31) >> 3) * 16 + (int)(n & 15);
+  dst[frag_offset((int)(n >> 4), k >> 5, K / 32, lane) / 8] = src[c];
+}
+
+hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (N % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  const int64_t chunks = N * (K / 8);
+  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const uint4 *>(src), static_cast<uint4 *>(dst), N, K);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Fused tail: the last two hidden layers and the output head in one kernel,
 // K0 -> N1 -> N2 (ReLU) -> n_out (sigmoid or softmax), for 64-row tiles.  The
 // row tile lives in LDS between layers; the small weight matrices (N1 x K0 and
-// N2 x N1) are read as MFMA fragments straight from global memory, where
-// every workgroup finds them in L2.  Hidden activations are rounded to the
-// storage type between layers, as the separate layers do.
+// N2 x N1, fragment-major, see frag_offset) are read as MFMA fragments
+// straight from global memory, where every workgroup finds them in L2.
+// Hidden activations are rounded to the storage type between layers, as the
+// separate layers do.
 template <typename TS, int K0, int N1, int N2>
 __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
                                                        const TS *__restrict__ W1,
@@ -475,14 +506,12 @@ __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
   for (int k = 0; k < KS1; ++k)
 #pragma unroll
     for (int i = 0; i < NB1; ++i)
-      w1f[k][i] = *reinterpret_cast<const frag *>(W1 + (int64_t)(wave * (N1 / 4) + i * 16 + frow) * K0 +
-                                                 k * 32 + fk);
+      w1f[k][i] = *reinterpret_cast<const frag *>(W1 + frag_offset(wave * NB1 + i, k, KS1, lane));
 #pragma unroll
   for (int k = 0; k < KS2; ++k)
 #pragma unroll
     for (int i = 0; i < NB2; ++i)
-      w2f[k][i] = *reinterpret_cast<const frag *>(W2 + (int64_t)(wave * (N2 / 4) + i * 16 + frow) * N1 +
-                                                 k * 32 + fk);
+      w2f[k][i] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave * NB2 + i, k, KS2, lane));
   static_assert(2 * N2 <= 256, "one head weight per thread");
   const TS whv = Wh[tid < n_out * N2 ? tid : 0];
   const float bhv = bh[tid < n_out ? tid : 0];
