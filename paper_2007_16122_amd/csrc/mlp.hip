@@ -179,6 +179,10 @@ __global__ __launch_bounds__(256, 2) void dense_relu_mfma_kernel(const TS *__res
 // tile is staged in LDS after the K loop so every row segment is written with
 // full 16-byte stores.
 __device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// the same for 128-byte rows (64-deep K steps): rows r and r + 1 are 128 bytes
+// apart, so the eight 16-byte slots of rows r & 7 are permuted by r & 7 and the
+// two halves of a 16-row block by one more bit
+__device__ __forceinline__ int lds_swz64(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 
 // wait until at most min(later, MAXL) stages of LOADS loads each are in flight
@@ -242,16 +246,20 @@ __device__ __forceinline__ uint32_t round2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-// Tile geometry of the pipelined layer: BR x BN outputs over 2 x WN waves.
-template <int BR, int BN, int S, int WN> struct BufTile {
+// Tile geometry of the pipelined layer: BR x BN outputs over 2 x WN waves,
+// KB-deep ring stages (32: 64-byte LDS rows; 64: 128-byte rows).
+template <int BR, int BN, int S, int WN, int KB = 32> struct BufTile {
   static constexpr int NT = 128 * WN, NW = 2 * WN;          // threads, waves
   static constexpr int NI = BN / WN / 16, RJ = BR / 32;     // 16x16 blocks per wave
-  static constexpr int ROWB = kBK * 2;                      // bytes per LDS row (64)
+  static constexpr int ROWB = KB * 2;                       // bytes per LDS row
+  static constexpr int CPRW = KB / 8;                       // 16-byte chunks per LDS row
+  static constexpr int RPI = 64 / CPRW;                     // rows per load instruction
   static constexpr int STAGE = (BN + BR) * ROWB;            // bytes per ring stage
-  static constexpr int LOADS = (BN + BR) / 16 / NW;         // 16-row loads per wave per stage
+  static constexpr int LOADS = (BN + BR) / RPI / NW;        // loads per wave per stage
   static constexpr int RING = S * STAGE;
-  static_assert((BN + BR) % (16 * NW) == 0, "loads must split evenly over the waves");
-  static_assert(BN % (16 * WN) == 0 && BR % 32 == 0, "tile shape");
+  static_assert(KB == 32 || KB == 64, "stage depth");
+  static_assert((BN + BR) % (RPI * NW) == 0, "loads must split evenly over the waves");
+  static_assert(BN % (16 * WN) == 0 && BR % 32 == 0 && BN % RPI == 0, "tile shape");
   static_assert(S >= 2 && S <= 4, "stages");
 };
 
@@ -260,14 +268,16 @@ template <int BR, int BN, int S, int WN> struct BufTile {
 // (i, j), i.e. output features n0 + wn*(BN/WN) + 16 i + 4 (lane/16) + e of row
 // r0 + wr*(BR/2) + 16 j + lane % 16.  smem holds the ring (RING bytes); on
 // return the ring is free once the workgroup has passed a barrier.
-template <typename TS, int BR, int BN, int S, int WN>
+template <typename TS, int BR, int BN, int S, int WN, int KB = 32>
 __device__ __forceinline__ void buf_tile_kloop(
     const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
     int N, int K, int64_t r0, int n0, unsigned char *smem,
-    f32x4 (&acc)[BufTile<BR, BN, S, WN>::NI][BufTile<BR, BN, S, WN>::RJ]) {
+    f32x4 (&acc)[BufTile<BR, BN, S, WN, KB>::NI][BufTile<BR, BN, S, WN, KB>::RJ]) {
   typedef typename Mfma<TS>::frag frag;
-  typedef BufTile<BR, BN, S, WN> G;
+  typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NI = G::NI, RJ = G::RJ, ROWB = G::ROWB, STAGE = G::STAGE, LOADS = G::LOADS;
+  constexpr int CPRW = G::CPRW, RPI = G::RPI;
+  auto swz = [](int r) { return KB == 32 ? lds_swz(r) : lds_swz64(r); };
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave % WN, wr = wave / WN;
@@ -278,23 +288,26 @@ __device__ __forceinline__ void buf_tile_kloop(
   const TS *wbase = W + (int64_t)n0 * K, *xbase = X + r0 * K;
   const int wbytes = w_rows * K * 2, xbytes = x_rows * K * 2;
 
+  // load instruction ins fills RPI consecutive LDS rows (W rows first, then
+  // X rows); lane l writes slot l % CPRW of row l / CPRW, which holds the
+  // row's logical chunk slot ^ swz(row)
   int voff[LOADS];
 #pragma unroll
   for (int u = 0; u < LOADS; ++u) {
     const int ins = wave * LOADS + u;
-    const int row16 = lane >> 2, slot = lane & 3;
-    const int chunk = slot ^ lds_swz(row16);
-    const int row = (ins < BN / 16 ? ins : ins - BN / 16) * 16 + row16;
+    const int rin = lane / CPRW, slot = lane % CPRW;
+    const int row = (ins < BN / RPI ? ins : ins - BN / RPI) * RPI + rin;
+    const int chunk = slot ^ swz(row & 15);
     voff[u] = (row * K + chunk * 8) * 2;
   }
   auto issue = [&](int ks, int stage) {
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int ins = wave * LOADS + u;
-      const int dst = ins < BN / 16 ? ins * 16 * ROWB : BN * ROWB + (ins - BN / 16) * 16 * ROWB;
-      const bool is_w = ins < BN / 16;
+      const bool is_w = ins < BN / RPI;
+      const int dst = is_w ? ins * RPI * ROWB : BN * ROWB + (ins - BN / RPI) * RPI * ROWB;
       buffer_load_lds16(is_w ? static_cast<const void *>(wbase) : static_cast<const void *>(xbase),
-                        is_w ? wbytes : xbytes, smem + stage * STAGE + dst, voff[u], ks * (kBK * 2));
+                        is_w ? wbytes : xbytes, smem + stage * STAGE + dst, voff[u], ks * (KB * 2));
     }
   };
 
@@ -313,14 +326,20 @@ __device__ __forceinline__ void buf_tile_kloop(
     for (int j = 0; j < RJ; ++j) acc[i][j] = bv;
   }
 
-  const int ksteps = K / kBK;
+  const int ksteps = K / KB;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < ksteps) issue(st, st);
 
+  // fragment reads: 32-deep half h of a stage is logical chunks 4 h + lane / 16
   const int frow = lane & 15, fc = lane >> 4;
-  const int a_off = (wn * (BN / WN) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
-  const int b_off = BN * ROWB + (wr * (BR / 2) + frow) * ROWB + ((fc ^ lds_swz(frow)) * 16);
+  int a_off[KB / 32], b_off[KB / 32];
+#pragma unroll
+  for (int h = 0; h < KB / 32; ++h) {
+    const int pc = ((4 * h + fc) ^ swz(frow)) * 16;
+    a_off[h] = (wn * (BN / WN) + frow) * ROWB + pc;
+    b_off[h] = BN * ROWB + (wr * (BR / 2) + frow) * ROWB + pc;
+  }
   for (int kb = 0; kb < ksteps; kb += S) {
 #pragma unroll
     for (int st = 0; st < S; ++st) {
@@ -333,15 +352,18 @@ __device__ __forceinline__ void buf_tile_kloop(
         compiler_fence();
         if (ks + S - 1 < ksteps) issue(ks + S - 1, (st + S - 1) % S);
         const unsigned char *base = smem + st * STAGE;
-        frag fa[NI];
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
-          fa[i] = *reinterpret_cast<const frag *>(base + a_off + i * 16 * ROWB);
+        for (int h = 0; h < KB / 32; ++h) {
+          frag fa[NI];
 #pragma unroll
-        for (int j = 0; j < RJ; ++j) {
-          const frag fb = *reinterpret_cast<const frag *>(base + b_off + j * 16 * ROWB);
+          for (int i = 0; i < NI; ++i)
+            fa[i] = *reinterpret_cast<const frag *>(base + a_off[h] + i * 16 * ROWB);
 #pragma unroll
-          for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+          for (int j = 0; j < RJ; ++j) {
+            const frag fb = *reinterpret_cast<const frag *>(base + b_off[h] + j * 16 * ROWB);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+          }
         }
       }
     }
@@ -349,14 +371,14 @@ __device__ __forceinline__ void buf_tile_kloop(
   wait_vm<0>();
 }
 
-template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2>
+template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2, int KB = 32>
 __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
                                                                      const TS *__restrict__ W,
                                                                      const float *__restrict__ bias,
                                                                      TS *__restrict__ Y, int64_t R,
                                                                      int N, int K, int tiles_n,
                                                                      int tiles_total) {
-  typedef BufTile<BR, BN, S, WN> G;
+  typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NT = G::NT, NI = G::NI, RJ = G::RJ;
   constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
   // the output tile is staged through the ring in one pass, or in two
@@ -376,7 +398,7 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
   const int dn = (lane >> 4) * 4, dr = lane & 15;
 
   f32x4 acc[NI][RJ];
-  buf_tile_kloop<TS, BR, BN, S, WN>(X, W, bias, R, N, K, r0, n0, smem, acc);
+  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, N, K, r0, n0, smem, acc);
 
   // epilogue: round, ReLU, stage the tile in LDS, write rows with 16-byte
   // stores.
@@ -761,14 +783,14 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
   return hipGetLastError();
 }
 
-template <typename TS, int BR, int BN, int S, int WN, int MINW>
+template <typename TS, int BR, int BN, int S, int WN, int MINW, int KB = 32>
 static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void *y, int64_t R,
                               int N, int K, hipStream_t s) {
   const int tiles_n = (N + BN - 1) / BN;
   const int64_t tiles_r = (R + BR - 1) / BR;
   const int64_t total = tiles_r * tiles_n;
   if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW>), dim3((unsigned)total),
+  hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB>), dim3((unsigned)total),
                      dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
                      static_cast<TS *>(y), R, N, K, tiles_n, (int)total);
   return hipGetLastError();
@@ -778,15 +800,18 @@ template <typename TS>
 static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, void *y, int64_t R,
                                 int N, int K, hipStream_t s) {
   if (K % kBK == 0 && N % 8 == 0) {
-    // large batches: 256 x 256 tiles over 8 waves (256 x 128 or 256 x 64
-    // over 4 waves for narrower layers); batches of a few thousand ads
-    // would leave most CUs idle with those, so 128 x 128 tiles while they
-    // still number at least one per CU, else 64 x 64
+    // large batches: 256 x 256 tiles over 8 waves, in 64-deep stages (one
+    // barrier per 64 MFMAs per wave, whole 128-byte rows per load) when K
+    // allows (256 x 128 or 256 x 64 over 4 waves for narrower layers);
+    // batches of a few thousand ads would leave most CUs idle with those,
+    // so 128 x 128 tiles while they still number at least one per CU, else
+    // 64 x 64
     const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
     const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
     if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
       return dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
     if (big_tiles < 256) return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    if (N % 256 == 0 && K % 64 == 0) return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s);
     if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
     if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
     return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
