@@ -808,10 +808,14 @@ static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, vo
     // 64 x 64
     const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
     const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
+    const bool k64 = K % 64 == 0;
     if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
-      return dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    if (big_tiles < 256) return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    if (N % 256 == 0 && K % 64 == 0) return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s);
+      return k64 ? dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
+                 : dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    if (big_tiles < 256)
+      return k64 ? dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
+                 : dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    if (N % 256 == 0 && k64) return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s);
     if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
     if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
     return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
