@@ -367,7 +367,6 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   uint4 raw[CPT];
   {
     int t = tf, c = cf;
-  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
     asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
@@ -394,7 +393,6 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
   }
   if constexpr (MODE == kFull || MODE == kWeightsOnly) {
     int t = tf, c = cf;
-  asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
     asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
     for (int j = 0; j < CPT; ++j, advance(t, c)) {
