@@ -435,6 +435,34 @@ def summarize_pmc(fetch_dir, write_dir, probe_mb, command, workload):
             "stages": stages, "sources": _source_hashes()}
 
 
+def summarize_mfma(pmc_dir, command, workload, simds, xcds):
+    """Matrix-core utilisation per stage from one rocprofv3 run with
+    SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: the first summed over all
+    SIMDs, the second over the XCDs, so busy = (MFMA busy cycles per SIMD) /
+    (active cycles of the dispatch). It does not depend on the clock the
+    chip ran at, unlike the achieved rate against the 2.5 PFLOP/s peak."""
+    import csv
+    import glob
+    path = glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)[0]
+    rows = list(csv.DictReader(open(path)))
+    val = {}
+    for counter in ("SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"):
+        for st, r in _last_call([r for r in rows if r["Counter_Name"] == counter]):
+            val.setdefault(st, {}).setdefault(counter, 0.0)
+            val[st][counter] += float(r["Counter_Value"])
+            val[st]["kernel"] = r["Kernel_Name"]
+    lines = [f"# rocprofv3 matrix-core utilisation, per stage of one cold_score call ({workload})",
+             f"# command: {command}",
+             f"# busy = SQ_VALU_MFMA_BUSY_CYCLES / {simds} SIMDs over GRBM_GUI_ACTIVE / {xcds} XCDs",
+             f"{'stage':12s} {'mfma_busy_per_simd':>18s} {'active_cycles':>13s} {'busy':>6s}  kernel"]
+    for st, v in val.items():
+        busy = v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / simds
+        active = v.get("GRBM_GUI_ACTIVE", 0.0) / xcds
+        frac = busy / active if active else float("nan")
+        lines.append(f"{st:12s} {busy:18.0f} {active:13.0f} {frac:6.3f}  {v['kernel'][:90]}")
+    return "\n".join(lines) + "\n"
+
+
 def _stage_sources(stage):
     """Source files that define a stage's kernel (with the shared header)."""
     if stage.startswith("dense") or stage in ("tail", "head", "se_dense"):
@@ -495,10 +523,19 @@ def main():
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="print matrix-core utilisation per stage from a run with "
+                         "--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE")
+    ap.add_argument("--simds", type=int, default=1024, help="SIMDs on the chip (MI355X: 256 CUs x 4)")
+    ap.add_argument("--xcds", type=int, default=8, help="XCDs on the chip")
     ap.add_argument("--profile-command", default="", help="command recorded in summaries")
     args = ap.parse_args()
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.profile_command), end="")
+        return
+    if args.summarize_mfma:
+        print(summarize_mfma(args.summarize_mfma, args.profile_command, args.workload, args.simds,
+                             args.xcds), end="")
         return
     if args.summarize_pmc:
         t = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_probe_mb or 1024,
