@@ -19,7 +19,10 @@
 //  dense_relu_f32   the layer in fp32 FMA (the fp32 model).
 //  head             last layer (n_out = 1 or 2) in fp32 plus sigmoid or
 //                   two-way softmax; writes the CTR.
+#include <mutex>
 #include <type_traits>
+#include <utility>
+#include <vector>
 
 #include "cold_internal.h"
 
@@ -479,8 +482,15 @@ hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hi
 // straight from global memory, where every workgroup finds them in L2.
 // Hidden activations are rounded to the storage type between layers, as the
 // separate layers do.
-template <typename TS, int K0, int N1, int N2>
-__global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
+// MINB workgroups per CU. At 2 the register budget (256 per lane) holds the
+// input tile and every weight fragment at once, as they are loaded (the
+// shortest chain per tile; batches of a few tiles per CU). At 3 the second
+// hidden layer's output also takes the input tile's LDS, which is dead once
+// the first layer is done, so three workgroups fit per CU, and the compiler
+// reloads some fragments within 168 registers (batches of many tiles per CU).
+// The arithmetic, and so every score, is the same for both.
+template <typename TS, int K0, int N1, int N2, int MINB>
+__global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restrict__ A,
                                                        const TS *__restrict__ W1,
                                                        const float *__restrict__ b1,
                                                        const TS *__restrict__ W2,
@@ -495,7 +505,11 @@ __global__ __launch_bounds__(256) void mlp_tail_kernel(const TS *__restrict__ A,
                 "tail widths");
   __shared__ __align__(16) TS s_in[BR * S0];
   __shared__ __align__(16) TS s_h1[BR * S1];
-  __shared__ __align__(16) TS s_h2[BR * S2];
+  static_assert(MINB == 2 || MINB == 3, "tail occupancy");
+  constexpr bool kAlias = MINB == 3;
+  static_assert(!kAlias || S2 <= S0, "second hidden tile fits in the input tile");
+  __shared__ __align__(16) TS s_h2_own[kAlias ? 8 : BR * S2];
+  TS *s_h2 = kAlias ? s_in : s_h2_own;
   __shared__ float s_wh[2 * N2];
   __shared__ float s_bh[2];
 
@@ -841,21 +855,44 @@ bool tail_supported(int dtype, int K0, int N1, int N2, int n_out) {
   return dtype != kF32 && K0 == 256 && N1 == 128 && N2 == 64 && (n_out == 1 || n_out == 2);
 }
 
+// CUs of the current device (cached per device)
+static int device_cus() {
+  static std::mutex mu;
+  static std::vector<std::pair<int, int>> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const auto &e : cache)
+    if (e.first == dev) return e.second;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  cache.emplace_back(dev, cus);
+  return cus;
+}
+
+template <typename TS, int MINB>
+static void launch_tail_t(const void *a, const void *w1, const float *b1, const void *w2,
+                          const float *b2, const void *wh, const float *bh, int32_t n_out,
+                          float *scores, int64_t R, hipStream_t s) {
+  hipLaunchKernelGGL((mlp_tail_kernel<TS, 256, 128, 64, MINB>), dim3((unsigned)((R + 63) / 64)),
+                     dim3(256), 0, s, static_cast<const TS *>(a), static_cast<const TS *>(w1), b1,
+                     static_cast<const TS *>(w2), b2, static_cast<const TS *>(wh), bh, n_out,
+                     scores, R);
+}
+
 hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float *b1,
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((R + 63) / 64));
-  if (dtype == kBF16)
-    hipLaunchKernelGGL((mlp_tail_kernel<__bf16, 256, 128, 64>), grid, dim3(256), 0, s,
-                       static_cast<const __bf16 *>(a), static_cast<const __bf16 *>(w1), b1,
-                       static_cast<const __bf16 *>(w2), b2, static_cast<const __bf16 *>(wh), bh,
-                       n_out, scores, R);
-  else
-    hipLaunchKernelGGL((mlp_tail_kernel<_Float16, 256, 128, 64>), grid, dim3(256), 0, s,
-                       static_cast<const _Float16 *>(a), static_cast<const _Float16 *>(w1), b1,
-                       static_cast<const _Float16 *>(w2), b2, static_cast<const _Float16 *>(wh), bh,
-                       n_out, scores, R);
+  // more than four 64-row tiles per CU: three workgroups per CU
+  const bool many = (R + 63) / 64 > 4 * (int64_t)device_cus();
+  if (dtype == kBF16) {
+    if (many) launch_tail_t<__bf16, 3>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else launch_tail_t<__bf16, 2>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+  } else {
+    if (many) launch_tail_t<_Float16, 3>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else launch_tail_t<_Float16, 2>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+  }
   return hipGetLastError();
 }
 
