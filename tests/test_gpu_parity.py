@@ -307,6 +307,35 @@ def test_request_alone_equals_batch_bitwise(name):
         assert np.array_equal(a, full[off[q]:off[q + 1]]), f"request {q}"
 
 
+def test_many_tile_batch_equals_smaller_batch_bitwise():
+    """A batch of more than four 64-row tiles per CU runs the fused tail
+    three workgroups per CU, with its second hidden tile in the input tile's
+    LDS; the same requests in a smaller batch run it two per CU. The
+    arithmetic is the same, so the scores are bit-identical."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n_req = 4 * cus * 64 // 2000 + 4
+    cfg = mid("serving_bf16", n_requests=n_req, cand_per_request=2000)
+    assert cfg.n_seq == 0 and (cfg.n_rows + 63) // 64 > 4 * cus
+    log(f"test_many_tile_batch_equals_smaller_batch_bitwise: R={cfg.n_rows}, {cus} CUs")
+    tables, params, batch = problem(cfg, seed=41)
+    q = 8
+    off = batch["req_off"]
+    hi = int(off[q])
+    prefix = dict(req_off=np.ascontiguousarray(off[:q + 1]),
+                  user_ids=np.ascontiguousarray(batch["user_ids"][:, :q]),
+                  ad_ids=np.ascontiguousarray(batch["ad_ids"][:, :hi]),
+                  cross_ids=np.ascontiguousarray(batch["cross_ids"][:, :hi]),
+                  n_rows=hi, n_requests=q, seq_off=np.zeros(1, np.int32),
+                  seq_ids=np.zeros(0, batch["ad_ids"].dtype))
+    run = load(cfg, tables, params)
+    try:
+        full = run.score(batch)["scores"]
+        part = run.score(prefix)["scores"]
+    finally:
+        run.close()
+    assert np.array_equal(part, full[:hi])
+
+
 def test_zero_se_gives_exact_half():
     cfg = mid("serving_bf16")
     tables, params, batch = problem(cfg, seed=33, cand=[100, 29])
