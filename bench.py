@@ -61,6 +61,9 @@ def stage_work(cfg, batch, stage):
         return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * 4 + Q * nus * d * 4
     if stage == "se_dense":
         return "mfma_f32", 2.0 * R * cfg.d_in * m
+    if stage == "dense_tail":     # the last separate layer and the fused tail
+        w = cfg.widths
+        return "mfma", 2.0 * R * (w[-5] * w[-4] + w[-4] * w[-3] + w[-3] * w[-2] + w[-2] * w[-1])
     if stage.startswith("dense"):
         li = int(stage[5:])
         return "mfma", 2.0 * R * cfg.widths[li] * cfg.widths[li + 1]
@@ -337,6 +340,8 @@ def _stage_of(kernel_name, dense_index):
         return {"0": "gather_se", "1": "se_weights", "2": "gather_apply", "3": "gather_raw"}.get(mode, "gather_se")
     if "dense_f32" in kernel_name:
         return "se_dense"
+    if "dense_tail_kernel" in kernel_name:
+        return "dense_tail"
     if "mask_partial" in kernel_name or "mask_select" in kernel_name:
         return "group_mask"
     if "dense_relu" in kernel_name:

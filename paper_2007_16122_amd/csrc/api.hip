@@ -481,9 +481,13 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   const bool fuse_tail = L >= 3 && tail_supported(m->dtype, m->widths[L - 3], m->widths[L - 2],
                                                   m->widths[L - 1], m->widths[L]);
   const int n_separate = fuse_tail ? L - 3 : L - 1;
+  // on large batches the last separate layer runs in the tail's kernel
+  const bool dense_tail = fuse_tail && n_separate >= 1 &&
+                          dense_tail_supported(m->dtype, R, m->widths[n_separate],
+                                               m->widths[n_separate - 1]);
   const void *in = W + wl.X;
   unsigned char *bufs[2] = {W + wl.actA, W + wl.actB};
-  for (int l = 0; l < n_separate; ++l) {
+  for (int l = 0; l < n_separate - (dense_tail ? 1 : 0); ++l) {
     void *outp = bufs[l & 1];
     if ((e = marks.mark(l < 12 ? kDenseNames[l] : "dense")) != hipSuccess)
       return hip_fail(m, e, "profile event");
@@ -492,7 +496,17 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
       return hip_fail(m, e, "dense layer launch");
     in = outp;
   }
-  if (fuse_tail) {
+  if (dense_tail) {
+    const int l = n_separate - 1;
+    if ((e = marks.mark("dense_tail")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_dense_tail(m->dtype, in, A + al.w[l], reinterpret_cast<const float *>(A + al.b[l]),
+                               m->widths[l + 1], m->widths[l], A + al.w[L - 3],
+                               reinterpret_cast<const float *>(A + al.b[L - 3]), A + al.w[L - 2],
+                               reinterpret_cast<const float *>(A + al.b[L - 2]), A + al.w[L - 1],
+                               reinterpret_cast<const float *>(A + al.b[L - 1]), m->widths[L],
+                               scores, R, s)) != hipSuccess)
+      return hip_fail(m, e, "dense + tail launch");
+  } else if (fuse_tail) {
     if ((e = marks.mark("tail")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_mlp_tail(m->dtype, in, A + al.w[L - 3], reinterpret_cast<const float *>(A + al.b[L - 3]),
                              A + al.w[L - 2], reinterpret_cast<const float *>(A + al.b[L - 2]),

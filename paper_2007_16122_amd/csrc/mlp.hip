@@ -482,6 +482,83 @@ hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hi
 // straight from global memory, where every workgroup finds them in L2.
 // Hidden activations are rounded to the storage type between layers, as the
 // separate layers do.
+// One hidden layer of the fused tail on rows held in the LDS:
+// out[r][n] = round(ReLU(b[n] + sum_k W[n][k] in[r][k])) for the 16-row
+// blocks jb0 .. jb0 + JB - 1 and the 16-feature blocks nb0 .. nb0 + NB - 1.
+// The K steps are summed from zero in order and the bias is added last, so
+// every output is the same whichever wave computes it. in_at(row, c) is the
+// LDS address of 16-byte chunk c of an input row; wf[k][i] is the weight
+// fragment of feature block nb0 + i and K step k; out rows are s_out_stride
+// elements apart.
+template <typename TS, int KS, int NB, int JB, typename InAt>
+__device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__restrict__ bg, TS *out,
+                                           int s_out_stride,
+                                           const typename Mfma<TS>::frag (&wf)[KS][NB], int nb0,
+                                           int jb0, int lane) {
+  typedef typename Mfma<TS>::frag frag;
+  const int frow = lane & 15, fq = lane >> 4;
+  const int dn = fq * 4, dr = lane & 15;
+  f32x4 acc[NB][JB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < JB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const frag fb = *reinterpret_cast<const frag *>(in_at((jb0 + j) * 16 + frow, 4 * k + fq));
+#pragma unroll
+      for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int n = (nb0 + i) * 16 + dn;
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = acc[i][j][e] + bg[n + e];
+        o[e] = t > 0.0f ? t : 0.0f;
+      }
+      uint2 packed;
+      packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
+      packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
+      *reinterpret_cast<uint2 *>(&out[((jb0 + j) * 16 + dr) * s_out_stride + n]) = packed;
+    }
+  }
+}
+
+// Output head of the fused tail on 64 rows: 4 threads per row (tid < 256),
+// each summing a quarter of the N2 inputs in order, then two shuffle steps;
+// sigmoid (one logit) or two-way softmax, CTR = class 1. Rows at or past R
+// are not stored.
+template <typename TS, int N2>
+__device__ __forceinline__ void tail_head(const TS *s_h2, int s2, const float *s_wh,
+                                          const float *s_bh, int n_out, float *__restrict__ scores,
+                                          int64_t r0, int64_t R, int tid) {
+  const int row = tid >> 2, q = tid & 3;
+  float z0 = 0.0f, z1 = 0.0f;
+#pragma unroll 4
+  for (int k = q * (N2 / 4); k < (q + 1) * (N2 / 4); ++k) {
+    const float x = Elem<TS>::to_f32(s_h2[row * s2 + k]);
+    z0 += s_wh[k] * x;
+    if (n_out > 1) z1 += s_wh[N2 + k] * x;
+  }
+  z0 += __shfl_xor(z0, 1);
+  z0 += __shfl_xor(z0, 2);
+  z1 += __shfl_xor(z1, 1);
+  z1 += __shfl_xor(z1, 2);
+  const int64_t r = r0 + row;
+  if (q == 0 && r < R) {
+    z0 += s_bh[0];
+    if (n_out > 1) z1 += s_bh[1];
+    scores[r] = n_out == 1 ? 1.0f / (1.0f + expf(-z0)) : 1.0f / (1.0f + expf(z0 - z1));
+  }
+}
+
 // MINB workgroups per CU. At 2 the register budget (256 per lane) holds the
 // input tile and every weight fragment at once, as they are loaded (the
 // shortest chain per tile; batches of a few tiles per CU). At 3 the second
@@ -530,8 +607,6 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
     tile[i] = *reinterpret_cast<const uint4 *>(A + r * K0 + kc * 8);
   }
 
-  const int frow = lane & 15, fk = (lane >> 4) * 8;
-  const int dn = (lane >> 4) * 4, dr = lane & 15;
   // The weight fragments of both layers are loaded once, before the input
   // tile is needed, so their L2 latency overlaps the tile load instead of
   // stalling every K step.
@@ -561,68 +636,101 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
   if (tid < n_out) s_bh[tid] = bhv;
   __syncthreads();   // input tile and head weights in LDS
 
-  // one hidden layer on the tile: wave w owns outputs [w*NOUT/4, (w+1)*NOUT/4)
-  auto layer = [&](const TS *in, int s_in_stride, const float *bg, TS *out, int s_out_stride,
-                   auto &wf, auto nout_tag, auto ks_tag) {
-    constexpr int NOUT = decltype(nout_tag)::value;
-    constexpr int KS = decltype(ks_tag)::value;
-    constexpr int NB = NOUT / 4 / 16;     // 16-wide output blocks per wave
-    f32x4 acc[NB][BR / 16];
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
-#pragma unroll
-      for (int j = 0; j < BR / 16; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int nbase = wave * (NOUT / 4);
-#pragma unroll
-    for (int k = 0; k < KS; ++k) {
-#pragma unroll
-      for (int j = 0; j < BR / 16; ++j) {
-        const frag fb = *reinterpret_cast<const frag *>(&in[(j * 16 + frow) * s_in_stride + k * 32 + fk]);
-#pragma unroll
-        for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int n = nbase + i * 16 + dn;
-#pragma unroll
-      for (int j = 0; j < BR / 16; ++j) {
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float t = acc[i][j][e] + bg[n + e];
-          o[e] = t > 0.0f ? t : 0.0f;
-        }
-        uint2 packed;
-        packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
-        packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
-        *reinterpret_cast<uint2 *>(&out[(j * 16 + dr) * s_out_stride + n]) = packed;
-      }
-    }
-  };
-  layer(s_in, S0, b1, s_h1, S1, w1f, std::integral_constant<int, N1>{}, std::integral_constant<int, KS1>{});
+  // wave w owns the output features [w*N/4, (w+1)*N/4) of each layer
+  auto in0 = [&](int row, int c) { return s_in + row * S0 + c * 8; };
+  tail_layer<TS, KS1, NB1, BR / 16>(in0, b1, s_h1, S1, w1f, wave * NB1, 0, lane);
   __syncthreads();
-  layer(s_h1, S1, b2, s_h2, S2, w2f, std::integral_constant<int, N2>{}, std::integral_constant<int, KS2>{});
+  auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
+  tail_layer<TS, KS2, NB2, BR / 16>(in1, b2, s_h2, S2, w2f, wave * NB2, 0, lane);
   __syncthreads();
+  tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0, R, tid);
+}
 
-  // head: 4 threads per row, each over a quarter of the N2 inputs
-  const int row = tid >> 2, q = tid & 3;
-  float z0 = 0.0f, z1 = 0.0f;
-#pragma unroll 4
-  for (int k = q * (N2 / 4); k < (q + 1) * (N2 / 4); ++k) {
-    const float x = Elem<TS>::to_f32(s_h2[row * S2 + k]);
-    z0 += s_wh[k] * x;
-    if (n_out > 1) z1 += s_wh[N2 + k] * x;
+// The last separate hidden layer and the fused tail in one kernel, for
+// large batches whose last separate layer is 256 wide (the tail's input) and
+// runs on 256 x 256 tiles: a tile then holds whole rows of the tail's input.
+// The layer is the 256 x 256 K loop of dense_relu_buf_kernel with the same
+// rounding; its output tile stays in the LDS (the ring, free after the K
+// loop: 256 rows of 512 bytes, 16-byte chunk c of row r at slot c ^ (r & 7),
+// so the tail's fragment reads of 8 rows hit 8 different slots), and the
+// tail's two layers and head run on it in four 64-row chunks with the
+// device functions of mlp_tail_kernel, 8 waves each taking one 16-feature
+// block of the first layer and half a 16-feature block column of the second.
+// Every score is bit-identical to the separate layer followed by
+// mlp_tail_kernel, and the layer's output never goes to HBM.
+template <typename TS>
+__global__ __launch_bounds__(512, 1) void dense_tail_kernel(
+    const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
+    int K, int tiles_total, const TS *__restrict__ W1, const float *__restrict__ b1,
+    const TS *__restrict__ W2, const float *__restrict__ b2, const TS *__restrict__ Wh,
+    const float *__restrict__ bh, int n_out, float *__restrict__ scores) {
+  typedef typename Mfma<TS>::frag frag;
+  constexpr int BR = 256, BN = 256, S = 2, WN = 4, KB = 64;
+  typedef BufTile<BR, BN, S, WN, KB> G;
+  constexpr int NI = G::NI, RJ = G::RJ;
+  constexpr int N1 = 128, N2 = 64, CH = 64;            // tail widths, rows per tail chunk
+  constexpr int S1 = N1 + 8, S2 = N2 + 8;              // padded LDS rows of the tail
+  constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
+  constexpr int KS1 = BN / 32, KS2 = N1 / 32;
+  static_assert(G::RING == BR * HROW, "the layer's output tile takes the ring");
+  static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "one wave per tail feature block");
+  __shared__ __align__(16) unsigned char smem[G::RING];
+  __shared__ __align__(16) TS s_h1[CH * S1];
+  __shared__ __align__(16) TS s_h2[CH * S2];
+  __shared__ float s_wh[2 * N2];
+  __shared__ float s_bh[2];
+
+  const int tile = xcd_tile(blockIdx.x, tiles_total);
+  const int64_t r0 = (int64_t)tile * BR;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave % WN, wr = wave / WN;
+
+  f32x4 acc[NI][RJ];
+  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, BN, K, r0, 0, smem, acc);
+
+  // the layer's output: round, ReLU (as dense_relu_buf_kernel), into the LDS
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int n = wn * (BN / WN) + i * 16 + dn;
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) {
+      const int rl = wr * (BR / 2) + j * 16 + dr;
+      uint2 packed;
+      packed.x = relu_bits2(round2<TS>(acc[i][j][0], acc[i][j][1]));
+      packed.y = relu_bits2(round2<TS>(acc[i][j][2], acc[i][j][3]));
+      *reinterpret_cast<uint2 *>(smem + rl * HROW + (((n >> 3) ^ (rl & 7)) << 4) + (n & 7) * 2) =
+          packed;
+    }
   }
-  z0 += __shfl_xor(z0, 1);
-  z0 += __shfl_xor(z0, 2);
-  z1 += __shfl_xor(z1, 1);
-  z1 += __shfl_xor(z1, 2);
-  const int64_t r = r0 + row;
-  if (q == 0 && r < R) {
-    z0 += s_bh[0];
-    if (n_out > 1) z1 += s_bh[1];
-    scores[r] = n_out == 1 ? 1.0f / (1.0f + expf(-z0)) : 1.0f / (1.0f + expf(z0 - z1));
+  // tail weights: wave w owns feature block w of the first tail layer and
+  // feature block w % 4, row blocks 2 (w / 4) and 2 (w / 4) + 1 of the second
+  frag w1f[KS1][1], w2f[KS2][1];
+#pragma unroll
+  for (int k = 0; k < KS1; ++k)
+    w1f[k][0] = *reinterpret_cast<const frag *>(W1 + frag_offset(wave, k, KS1, lane));
+#pragma unroll
+  for (int k = 0; k < KS2; ++k)
+    w2f[k][0] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave % 4, k, KS2, lane));
+  if (tid < n_out * N2) s_wh[tid] = Elem<TS>::to_f32(Wh[tid]);
+  if (tid < n_out) s_bh[tid] = bh[tid];
+  __syncthreads();   // the layer's output tile and the head weights are in the LDS
+
+  for (int ch = 0; ch < BR / CH; ++ch) {
+    auto in0 = [&](int row, int c) {
+      const int rr = ch * CH + row;
+      return reinterpret_cast<const TS *>(smem + rr * HROW + ((c ^ (rr & 7)) << 4));
+    };
+    tail_layer<TS, KS1, 1, CH / 16>(in0, b1, s_h1, S1, w1f, wave, 0, lane);
+    __syncthreads();
+    auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
+    tail_layer<TS, KS2, 1, CH / 32>(in1, b2, s_h2, S2, w2f, wave % 4, (wave / 4) * (CH / 32), lane);
+    __syncthreads();
+    if (wave < 4) tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0 + ch * CH, R, tid);
   }
 }
 
@@ -893,6 +1001,34 @@ hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float
     if (many) launch_tail_t<_Float16, 3>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else launch_tail_t<_Float16, 2>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   }
+  return hipGetLastError();
+}
+
+bool dense_tail_supported(int dtype, int64_t R, int32_t N, int32_t K) {
+  // the separate layer would run on 256 x 256 tiles with 64-deep stages
+  // (dense_mfma_dt), and its output is the tail's 256-wide input
+  return dtype != kF32 && N == 256 && K > 0 && K % 64 == 0 && ((R + 255) / 256) * 2 >= 256 &&
+         (R + 255) / 256 <= 0x7FFFFFFF;
+}
+
+hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const float *b, int32_t N,
+                             int32_t K, const void *w1, const float *b1, const void *w2,
+                             const float *b2, const void *wh, const float *bh, int32_t n_out,
+                             float *scores, int64_t R, hipStream_t s) {
+  if (!dense_tail_supported(dtype, R, N, K)) return hipErrorNotSupported;
+  const int tiles = (int)((R + 255) / 256);
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(dense_tail_kernel<__bf16>, dim3(tiles), dim3(512), 0, s,
+                       static_cast<const __bf16 *>(x), static_cast<const __bf16 *>(w), b, R, K,
+                       tiles, static_cast<const __bf16 *>(w1), b1,
+                       static_cast<const __bf16 *>(w2), b2, static_cast<const __bf16 *>(wh), bh,
+                       n_out, scores);
+  else
+    hipLaunchKernelGGL(dense_tail_kernel<_Float16>, dim3(tiles), dim3(512), 0, s,
+                       static_cast<const _Float16 *>(x), static_cast<const _Float16 *>(w), b, R,
+                       K, tiles, static_cast<const _Float16 *>(w1), b1,
+                       static_cast<const _Float16 *>(w2), b2, static_cast<const _Float16 *>(wh),
+                       bh, n_out, scores);
   return hipGetLastError();
 }
 
