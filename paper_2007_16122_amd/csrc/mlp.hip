@@ -486,19 +486,18 @@ hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hi
 // out[r][n] = round(ReLU(b[n] + sum_k W[n][k] in[r][k])) for the 16-row
 // blocks jb0 .. jb0 + JB - 1 and the 16-feature blocks nb0 .. nb0 + NB - 1.
 // The K steps are summed from zero in order and the bias is added last, so
-// every output is the same whichever wave computes it. in_at(row, c) is the
-// LDS address of 16-byte chunk c of an input row; wf[k][i] is the weight
-// fragment of feature block nb0 + i and K step k; out rows are s_out_stride
-// elements apart.
+// every output is the same whichever wave computes it. tail_mma forms the
+// sums (in_at(row, c) is the LDS address of 16-byte chunk c of an input row;
+// wf[k][i] is the weight fragment of feature block nb0 + i and K step k);
+// tail_store adds the bias, applies ReLU, rounds and writes the rows
+// (s_out_stride elements apart). Between the two the caller may pass a
+// barrier and then overwrite the input.
 template <typename TS, int KS, int NB, int JB, typename InAt>
-__device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__restrict__ bg, TS *out,
-                                           int s_out_stride,
-                                           const typename Mfma<TS>::frag (&wf)[KS][NB], int nb0,
-                                           int jb0, int lane) {
+__device__ __forceinline__ void tail_mma(const InAt &in_at,
+                                         const typename Mfma<TS>::frag (&wf)[KS][NB], int jb0,
+                                         int lane, f32x4 (&acc)[NB][JB]) {
   typedef typename Mfma<TS>::frag frag;
   const int frow = lane & 15, fq = lane >> 4;
-  const int dn = fq * 4, dr = lane & 15;
-  f32x4 acc[NB][JB];
 #pragma unroll
   for (int i = 0; i < NB; ++i)
 #pragma unroll
@@ -512,6 +511,12 @@ __device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__res
       for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
     }
   }
+}
+
+template <typename TS, int NB, int JB>
+__device__ __forceinline__ void tail_store(const f32x4 (&acc)[NB][JB], const float *__restrict__ bg,
+                                           TS *out, int s_out_stride, int nb0, int jb0, int lane) {
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int n = (nb0 + i) * 16 + dn;
@@ -531,7 +536,17 @@ __device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__res
   }
 }
 
-// Output head of the fused tail on 64 rows: 4 threads per row (tid < 256),
+template <typename TS, int KS, int NB, int JB, typename InAt>
+__device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__restrict__ bg, TS *out,
+                                           int s_out_stride,
+                                           const typename Mfma<TS>::frag (&wf)[KS][NB], int nb0,
+                                           int jb0, int lane) {
+  f32x4 acc[NB][JB];
+  tail_mma<TS, KS, NB, JB>(in_at, wf, jb0, lane, acc);
+  tail_store<TS, NB, JB>(acc, bg, out, s_out_stride, nb0, jb0, lane);
+}
+
+// Output head of the fused tail: 4 threads per row (row tid / 4),
 // each summing a quarter of the N2 inputs in order, then two shuffle steps;
 // sigmoid (one logit) or two-way softmax, CTR = class 1. Rows at or past R
 // are not stored.
@@ -668,15 +683,14 @@ __global__ __launch_bounds__(512, 1) void dense_tail_kernel(
   constexpr int BR = 256, BN = 256, S = 2, WN = 4, KB = 64;
   typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NI = G::NI, RJ = G::RJ;
-  constexpr int N1 = 128, N2 = 64, CH = 64;            // tail widths, rows per tail chunk
+  constexpr int N1 = 128, N2 = 64;                     // tail widths
   constexpr int S1 = N1 + 8, S2 = N2 + 8;              // padded LDS rows of the tail
   constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
   constexpr int KS1 = BN / 32, KS2 = N1 / 32;
   static_assert(G::RING == BR * HROW, "the layer's output tile takes the ring");
   static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "one wave per tail feature block");
+  static_assert(BR * (S1 + S2) * 2 <= G::RING, "both hidden tiles fit in the ring");
   __shared__ __align__(16) unsigned char smem[G::RING];
-  __shared__ __align__(16) TS s_h1[CH * S1];
-  __shared__ __align__(16) TS s_h2[CH * S2];
   __shared__ float s_wh[2 * N2];
   __shared__ float s_bh[2];
 
@@ -720,18 +734,26 @@ __global__ __launch_bounds__(512, 1) void dense_tail_kernel(
   if (tid < n_out) s_bh[tid] = bh[tid];
   __syncthreads();   // the layer's output tile and the head weights are in the LDS
 
-  for (int ch = 0; ch < BR / CH; ++ch) {
-    auto in0 = [&](int row, int c) {
-      const int rr = ch * CH + row;
-      return reinterpret_cast<const TS *>(smem + rr * HROW + ((c ^ (rr & 7)) << 4));
-    };
-    tail_layer<TS, KS1, 1, CH / 16>(in0, b1, s_h1, S1, w1f, wave, 0, lane);
-    __syncthreads();
-    auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
-    tail_layer<TS, KS2, 1, CH / 32>(in1, b2, s_h2, S2, w2f, wave % 4, (wave / 4) * (CH / 32), lane);
-    __syncthreads();
-    if (wave < 4) tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0 + ch * CH, R, tid);
-  }
+  // first tail layer on all 256 rows (wave w: feature block w); its input
+  // is dead once every wave has its sums, and its output takes its place
+  auto in0 = [&](int row, int c) {
+    return reinterpret_cast<const TS *>(smem + row * HROW + ((c ^ (row & 7)) << 4));
+  };
+  f32x4 a1[1][BR / 16];
+  tail_mma<TS, KS1, 1, BR / 16>(in0, w1f, 0, lane, a1);
+  __syncthreads();
+  TS *s_h1 = reinterpret_cast<TS *>(smem);
+  TS *s_h2 = reinterpret_cast<TS *>(smem + BR * S1 * 2);
+  tail_store<TS, 1, BR / 16>(a1, b1, s_h1, S1, wave, 0, lane);
+  __syncthreads();
+  // second tail layer (wave w: feature block w % 4, rows 128 (w / 4) ..)
+  auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
+  tail_layer<TS, KS2, 1, BR / 32>(in1, b2, s_h2, S2, w2f, wave % 4, (wave / 4) * (BR / 32), lane);
+  __syncthreads();
+  // head, 128 rows per pass
+#pragma unroll
+  for (int p = 0; p < BR / 128; ++p)
+    tail_head<TS, N2>(s_h2 + p * 128 * S2, S2, s_wh, s_bh, n_out, scores, r0 + p * 128, R, tid);
 }
 
 // fp32 layer: 64 x 64 output tile, 4 x 4 per thread, K in steps of 16.
