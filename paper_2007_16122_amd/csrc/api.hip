@@ -19,7 +19,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct ArenaLayout {
-  size_t tables, rows, magic, pairs, w1, b1, w2, b2;
+  size_t tables, rows, magic, pairs, w1, b1, w2, b2, w1t, w2t;
   std::vector<size_t> w, b;
   size_t total;
 };
@@ -88,11 +88,15 @@ ArenaLayout arena_layout(const cold_model &m) {
     a.b1 = take(sizeof(float) * m.M);
     a.w2 = take(0);
     a.b2 = take(0);
+    a.w1t = take(0);
+    a.w2t = take(0);
   } else {
     a.w1 = take(sizeof(float) * m.H * m.M);
     a.b1 = take(sizeof(float) * m.H);
     a.w2 = take(sizeof(float) * m.M * m.H);
     a.b2 = take(sizeof(float) * m.M);
+    a.w1t = take(sizeof(float) * m.M * m.H);   // W1 as [M][H]
+    a.w2t = take(sizeof(float) * m.H * m.M);   // W2 as [H][M]
   }
   const int L = m.desc.n_layers;
   for (int l = 0; l < L; ++l) {
@@ -349,6 +353,15 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
     hipError_t e = hipMemcpyAsync(A + c.off, c.src, c.bytes, c.kind, s);
     if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: copy");
   }
+  if (!m->literal_se) {
+    // transposed SE weights for the gathers that read them from global memory
+    hipError_t e = launch_transpose_f32(reinterpret_cast<const float *>(A + al.w1),
+                                        reinterpret_cast<float *>(A + al.w1t), m->H, m->M, s);
+    if (e == hipSuccess)
+      e = launch_transpose_f32(reinterpret_cast<const float *>(A + al.w2),
+                               reinterpret_cast<float *>(A + al.w2t), m->M, m->H, s);
+    if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: transpose");
+  }
   for (int l = 0; l < L; ++l)
     if (packed(l)) {
       hipError_t e = launch_pack_frag(w->mlp_w[l], A + al.w[l], m->widths[l + 1], m->widths[l], s);
@@ -405,6 +418,8 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   g.b1 = reinterpret_cast<const float *>(A + al.b1);
   g.w2 = reinterpret_cast<const float *>(A + al.w2);
   g.b2 = reinterpret_cast<const float *>(A + al.b2);
+  g.w1t = reinterpret_cast<const float *>(A + al.w1t);
+  g.w2t = reinterpret_cast<const float *>(A + al.w2t);
   g.U = reinterpret_cast<float *>(W + wl.U);
   g.zU = reinterpret_cast<float *>(W + wl.zU);
   g.Uh = W + wl.Uh;

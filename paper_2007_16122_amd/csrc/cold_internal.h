@@ -173,6 +173,7 @@ struct GatherArgs {
   const uint64_t *table_magic;    // device [M]
   const int32_t *cross_pairs;     // device [n_cross][2] (user field, ad field) or null
   const float *w1, *b1, *w2, *b2; // SE parameters
+  const float *w1t, *w2t;         // W1 as [M][H], W2 as [H][M] (read when they are not in LDS)
   float *U;                       // [Q][n_user+n_seq][d] pooled user side
   float *zU;                      // [Q][n_user+n_seq] squeeze of the user groups
   void *Uh;                       // [Q][n_user][d] single-valued user rows, storage type
@@ -199,6 +200,9 @@ hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t
                              int32_t M, int32_t k, float *partial, int32_t n_parts,
                              uint8_t *mask, uint8_t *mask_out, hipStream_t s);
 hipError_t launch_clear_flag(int32_t *err, hipStream_t s);
+// dst[c][r] = src[r][c] for a [rows][cols] fp32 matrix
+hipError_t launch_transpose_f32(const float *src, float *dst, int32_t rows, int32_t cols,
+                                hipStream_t s);
 
 hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
                              int64_t R, int32_t N, int32_t K, hipStream_t s);

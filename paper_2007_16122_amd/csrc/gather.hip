@@ -417,7 +417,8 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     // ---- SE block of the wave's rows (Eq. 2)
     // sums from the bias in index order; from LDS, weight and input rows are
     // read four at a time (rows padded to Mp / Hp); from global memory, the
-    // weights keep their unpadded [H][M] / [M][H] layout
+    // weights are read transposed, so that the lanes (one output each) of a
+    // step read consecutive words
     for (int it = ln; it < Tw * H; it += 64) {
       const int t = fast_div(it, a.mg_h), jh = it - t * H;
       const float *zt = z + t * Mp;
@@ -436,9 +437,10 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
         }
         for (; g < M; ++g) acc += w[g] * zt[g];
       } else {
-        const float *w = w1 + jh * M;
+        // W1 transposed ([M][H]): the lanes of a step read consecutive words
+        const float *w = a.w1t + jh;
 #pragma unroll 8
-        for (int g = 0; g < M; ++g) acc += w[g] * zt[g];
+        for (int g = 0; g < M; ++g) acc += w[g * H] * zt[g];
       }
       hid[t * Hp + jh] = acc > 0.0f ? acc : 0.0f;
     }
@@ -461,9 +463,10 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
         }
         for (; jh < H; ++jh) acc += w[jh] * ht[jh];
       } else {
-        const float *w = w2 + g * H;
+        // W2 transposed ([H][M]): the lanes of a step read consecutive words
+        const float *w = a.w2t + g;
 #pragma unroll 8
-        for (int jh = 0; jh < H; ++jh) acc += w[jh] * ht[jh];
+        for (int jh = 0; jh < H; ++jh) acc += w[jh * M] * ht[jh];
       }
       const float sg = 1.0f / (1.0f + expf(-acc));
       sv[it] = sg;
@@ -725,6 +728,24 @@ hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(mask_select_kernel, dim3((unsigned)Q), dim3(256), sizeof(float) * M, s,
                      partial, req_off, R, M, n_parts, k, mask, mask_out);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void transpose_f32_kernel(const float *__restrict__ src,
+                                                            float *__restrict__ dst, int32_t rows,
+                                                            int32_t cols) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)rows * cols) return;
+  const int32_t r = (int32_t)(i / cols), c = (int32_t)(i - (int64_t)r * cols);
+  dst[(int64_t)c * rows + r] = src[i];
+}
+
+hipError_t launch_transpose_f32(const float *src, float *dst, int32_t rows, int32_t cols,
+                                hipStream_t s) {
+  const int64_t n = (int64_t)rows * cols;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
+                     dst, rows, cols);
   return hipGetLastError();
 }
 
