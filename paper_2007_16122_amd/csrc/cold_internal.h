@@ -231,7 +231,7 @@ hipError_t launch_head(int dtype, const void *a, const void *w, const float *b, 
 constexpr int kGatherThreads = 256;
 constexpr int kGatherMaxChunksPerRow = 1024;  // 64 lanes x 16 chunks
 constexpr int kGatherMaxIdsPerLane = 8;       // rows per wave x (ad + cross fields) <= 512
-constexpr int kMaskParts = 64;
+constexpr int kMaskParts = 256;   // row parts per request in the importance reduction
 constexpr int kGatherMaxReqLds = 1024;        // request offsets held in LDS up to this count
 constexpr int kGatherMaxUserValLds = 4096;    // user row bytes the gather stages in LDS itself
 

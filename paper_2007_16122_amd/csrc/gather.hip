@@ -559,19 +559,35 @@ __global__ __launch_bounds__(256) void mask_partial_kernel(const float *s_buf, c
   }
 }
 
-__global__ __launch_bounds__(256) void mask_select_kernel(const float *partial, const int32_t *req_off,
-                                                          int64_t R, int32_t M, int32_t P, int32_t k,
-                                                          uint8_t *mask, uint8_t *mask_out) {
-  extern __shared__ float imp[];  // [M]
+// Per request: importance I_g = (sum of the P partial sums of group g) / n,
+// then the top-k mask. The partial sums are added by kSelQuarters threads per
+// group, each over a contiguous quarter of the parts, and the quarters are
+// added in order, so the result does not depend on the launch.
+constexpr int kSelQuarters = 4;
+__global__ __launch_bounds__(1024) void mask_select_kernel(const float *partial, const int32_t *req_off,
+                                                           int64_t R, int32_t M, int32_t P, int32_t k,
+                                                           uint8_t *mask, uint8_t *mask_out) {
+  extern __shared__ float lds[];  // [kSelQuarters][M] quarter sums, then [M] importance
+  float *imp = lds + kSelQuarters * M;
   const int64_t q = blockIdx.x;
   int64_t lo = req_off[q], hi = req_off[q + 1];
   lo = lo < 0 ? 0 : (lo > R ? R : lo);
   hi = hi < lo ? lo : (hi > R ? R : hi);
   const float n = (float)(hi - lo);
-  for (int g = threadIdx.x; g < M; g += blockDim.x) {
+  const int per = P / kSelQuarters;
+  for (int idx = threadIdx.x; idx < kSelQuarters * M; idx += blockDim.x) {
+    const int c = idx / M, g = idx - c * M;
+    const float *src = partial + (q * P + c * per) * M + g;
     float acc = 0.0f;
 #pragma unroll 16
-    for (int p = 0; p < P; ++p) acc += partial[(q * P + p) * M + g];
+    for (int p = 0; p < per; ++p) acc += src[(int64_t)p * M];
+    lds[idx] = acc;
+  }
+  __syncthreads();
+  for (int g = threadIdx.x; g < M; g += blockDim.x) {
+    float acc = lds[g];
+#pragma unroll
+    for (int c = 1; c < kSelQuarters; ++c) acc += lds[c * M + g];
     imp[g] = n > 0.0f ? acc / n : 0.0f;
   }
   __syncthreads();
@@ -726,8 +742,10 @@ hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t
                      req_off, R, M, n_parts, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(mask_select_kernel, dim3((unsigned)Q), dim3(256), sizeof(float) * M, s,
-                     partial, req_off, R, M, n_parts, k, mask, mask_out);
+  if (n_parts % kSelQuarters != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(mask_select_kernel, dim3((unsigned)Q), dim3(1024),
+                     sizeof(float) * (kSelQuarters + 1) * M, s, partial, req_off, R, M, n_parts, k,
+                     mask, mask_out);
   return hipGetLastError();
 }
 
