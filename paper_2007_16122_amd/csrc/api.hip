@@ -496,7 +496,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
   const bool fuse_tail = L >= 3 && tail_supported(m->dtype, m->widths[L - 3], m->widths[L - 2],
                                                   m->widths[L - 1], m->widths[L]);
   const int n_separate = fuse_tail ? L - 3 : L - 1;
-  // on large batches the last separate layer runs in the tail's kernel
+  // the last separate layer runs in the tail's kernel when it is 256 wide
   const bool dense_tail = fuse_tail && n_separate >= 1 &&
                           dense_tail_supported(m->dtype, R, m->widths[n_separate],
                                                m->widths[n_separate - 1]);

@@ -214,8 +214,8 @@ hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s);
 // the last separate hidden layer (N = 256, the tail's input) and the fused
-// tail in one kernel; hipErrorNotSupported unless that layer would run on
-// 256 x 256 tiles (large batches, K % 64 == 0, half precision)
+// tail in one kernel; hipErrorNotSupported unless N == 256, K % 64 == 0 and
+// the model is in half precision
 bool dense_tail_supported(int dtype, int64_t R, int32_t N, int32_t K);
 hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const float *b, int32_t N,
                              int32_t K, const void *w1, const float *b1, const void *w2,

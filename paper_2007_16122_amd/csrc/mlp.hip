@@ -661,9 +661,10 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
   tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0, R, tid);
 }
 
-// The last separate hidden layer and the fused tail in one kernel, for
-// large batches whose last separate layer is 256 wide (the tail's input) and
-// runs on 256 x 256 tiles: a tile then holds whole rows of the tail's input.
+// The last separate hidden layer and the fused tail in one kernel, when that
+// layer is 256 wide (the tail's input): a BR x 256 output tile holds whole
+// rows of the tail's input. BR = 256 for large batches (the tiles of the
+// separate layer), 64 for batches of fewer than one 256-row tile per CU.
 // The layer is the 256 x 256 K loop of dense_relu_buf_kernel with the same
 // rounding; its output tile stays in the LDS (the ring, free after the K
 // loop: 256 rows of 512 bytes, 16-byte chunk c of row r at slot c ^ (r & 7),
@@ -673,21 +674,22 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
 // block of the first layer and half a 16-feature block column of the second.
 // Every score is bit-identical to the separate layer followed by
 // mlp_tail_kernel, and the layer's output never goes to HBM.
-template <typename TS>
-__global__ __launch_bounds__(512, 1) void dense_tail_kernel(
+template <typename TS, int BR, int MINB>
+__global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
     const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
     int K, int tiles_total, const TS *__restrict__ W1, const float *__restrict__ b1,
     const TS *__restrict__ W2, const float *__restrict__ b2, const TS *__restrict__ Wh,
     const float *__restrict__ bh, int n_out, float *__restrict__ scores) {
   typedef typename Mfma<TS>::frag frag;
-  constexpr int BR = 256, BN = 256, S = 2, WN = 4, KB = 64;
+  constexpr int BN = 256, S = 2, WN = 4, KB = 64;
+  static_assert(BR == 256 || BR == 64, "tile rows");
   typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NI = G::NI, RJ = G::RJ;
   constexpr int N1 = 128, N2 = 64;                     // tail widths
   constexpr int S1 = N1 + 8, S2 = N2 + 8;              // padded LDS rows of the tail
   constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
   constexpr int KS1 = BN / 32, KS2 = N1 / 32;
-  static_assert(G::RING == BR * HROW, "the layer's output tile takes the ring");
+  static_assert(G::RING >= BR * HROW, "the layer's output tile takes the ring");
   static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "one wave per tail feature block");
   static_assert(BR * (S1 + S2) * 2 <= G::RING, "both hidden tiles fit in the ring");
   __shared__ __align__(16) unsigned char smem[G::RING];
@@ -746,14 +748,18 @@ __global__ __launch_bounds__(512, 1) void dense_tail_kernel(
   TS *s_h2 = reinterpret_cast<TS *>(smem + BR * S1 * 2);
   tail_store<TS, 1, BR / 16>(a1, b1, s_h1, S1, wave, 0, lane);
   __syncthreads();
-  // second tail layer (wave w: feature block w % 4, rows 128 (w / 4) ..)
+  // second tail layer (wave w: feature block w % 4, rows BR/2 (w / 4) ..)
   auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
   tail_layer<TS, KS2, 1, BR / 32>(in1, b2, s_h2, S2, w2f, wave % 4, (wave / 4) * (BR / 32), lane);
   __syncthreads();
-  // head, 128 rows per pass
+  // head, 128 rows per pass (a 64-row tile: waves 0-3)
+  if constexpr (BR >= 128) {
 #pragma unroll
-  for (int p = 0; p < BR / 128; ++p)
-    tail_head<TS, N2>(s_h2 + p * 128 * S2, S2, s_wh, s_bh, n_out, scores, r0 + p * 128, R, tid);
+    for (int p = 0; p < BR / 128; ++p)
+      tail_head<TS, N2>(s_h2 + p * 128 * S2, S2, s_wh, s_bh, n_out, scores, r0 + p * 128, R, tid);
+  } else {
+    if (wave < BR / 16) tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0, R, tid);
+  }
 }
 
 // fp32 layer: 64 x 64 output tile, 4 x 4 per thread, K in steps of 16.
@@ -1027,10 +1033,20 @@ hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float
 }
 
 bool dense_tail_supported(int dtype, int64_t R, int32_t N, int32_t K) {
-  // the separate layer would run on 256 x 256 tiles with 64-deep stages
-  // (dense_mfma_dt), and its output is the tail's 256-wide input
-  return dtype != kF32 && N == 256 && K > 0 && K % 64 == 0 && ((R + 255) / 256) * 2 >= 256 &&
-         (R + 255) / 256 <= 0x7FFFFFFF;
+  // the layer's output is the tail's 256-wide input, in 64-deep K steps
+  return dtype != kF32 && N == 256 && K > 0 && K % 64 == 0 && R > 0 && (R + 63) / 64 <= 0x7FFFFFFF;
+}
+
+template <typename TS, int BR, int MINB>
+static void launch_dense_tail_t(const void *x, const void *w, const float *b, int32_t K,
+                                const void *w1, const float *b1, const void *w2, const float *b2,
+                                const void *wh, const float *bh, int32_t n_out, float *scores,
+                                int64_t R, hipStream_t s) {
+  const int tiles = (int)((R + BR - 1) / BR);
+  hipLaunchKernelGGL((dense_tail_kernel<TS, BR, MINB>), dim3(tiles), dim3(512), 0, s,
+                     static_cast<const TS *>(x), static_cast<const TS *>(w), b, R, K, tiles,
+                     static_cast<const TS *>(w1), b1, static_cast<const TS *>(w2), b2,
+                     static_cast<const TS *>(wh), bh, n_out, scores);
 }
 
 hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const float *b, int32_t N,
@@ -1038,19 +1054,16 @@ hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const floa
                              const float *b2, const void *wh, const float *bh, int32_t n_out,
                              float *scores, int64_t R, hipStream_t s) {
   if (!dense_tail_supported(dtype, R, N, K)) return hipErrorNotSupported;
-  const int tiles = (int)((R + 255) / 256);
-  if (dtype == kBF16)
-    hipLaunchKernelGGL(dense_tail_kernel<__bf16>, dim3(tiles), dim3(512), 0, s,
-                       static_cast<const __bf16 *>(x), static_cast<const __bf16 *>(w), b, R, K,
-                       tiles, static_cast<const __bf16 *>(w1), b1,
-                       static_cast<const __bf16 *>(w2), b2, static_cast<const __bf16 *>(wh), bh,
-                       n_out, scores);
-  else
-    hipLaunchKernelGGL(dense_tail_kernel<_Float16>, dim3(tiles), dim3(512), 0, s,
-                       static_cast<const _Float16 *>(x), static_cast<const _Float16 *>(w), b, R,
-                       K, tiles, static_cast<const _Float16 *>(w1), b1,
-                       static_cast<const _Float16 *>(w2), b2, static_cast<const _Float16 *>(wh),
-                       bh, n_out, scores);
+  // 256-row tiles where the separate layer would use 256 x 256 tiles (at
+  // least one tile per CU), 64-row tiles for smaller batches
+  const bool big = ((R + 255) / 256) * 2 >= 256;
+  if (dtype == kBF16) {
+    if (big) launch_dense_tail_t<__bf16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else launch_dense_tail_t<__bf16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+  } else {
+    if (big) launch_dense_tail_t<_Float16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else launch_dense_tail_t<_Float16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+  }
   return hipGetLastError();
 }
 
