@@ -207,14 +207,18 @@ def test_parity_odd_input_width(name):
 
 
 @pytest.mark.parametrize("widths,n_req", [((768, 384, 320, 256, 128, 64, 2), 12),
-                                          ((768, 1024, 512, 256, 128, 64, 2), 3)])
+                                          ((768, 1024, 512, 256, 128, 64, 2), 3),
+                                          ((768, 1024, 544, 256, 128, 64, 2), 3),
+                                          ((768, 1024, 544, 256, 128, 64, 2), 36)])
 def test_parity_layer_tile_shapes(widths, n_req):
     """The dense layer's other tile shapes: hidden widths that are multiples
     of 128 but not 256 (384: 256 x 128 tiles) and of 64 but not 128 (320:
     256 x 64 tiles) on a batch large enough for 256-row tiles, and a
     6,000-row batch of the serving widths (128 x 128 tiles for the
-    1,024-wide layer, 64 x 64 for the others); ragged last row tiles;
-    checker on a seeded sample of rows."""
+    1,024-wide layer, 64-row tiles of the fused last layers). A 544-wide
+    layer (256 x 64 tiles; 32-deep K steps into the 256-wide layer) keeps
+    the tail in its own kernel: two workgroups per CU on 6,000 rows, three
+    on 72,000. Ragged last row tiles; checker on a seeded sample of rows."""
     cfg = mid("serving_bf16", widths=widths, n_requests=n_req, cand_per_request=2000 - 7)
     log(f"test_parity_layer_tile_shapes widths={widths} R={cfg.n_rows}")
     tables, params, batch = problem(cfg, seed=29)
@@ -308,13 +312,16 @@ def test_request_alone_equals_batch_bitwise(name):
 
 
 def test_many_tile_batch_equals_smaller_batch_bitwise():
-    """A batch of more than four 64-row tiles per CU runs the fused tail
-    three workgroups per CU, with its second hidden tile in the input tile's
-    LDS; the same requests in a smaller batch run it two per CU. The
-    arithmetic is the same, so the scores are bit-identical."""
+    """With a layer before the tail that keeps the tail in its own kernel
+    (544 -> 256 in 32-deep K steps), a batch of more than four 64-row tiles
+    per CU runs the tail three workgroups per CU, with its second hidden
+    tile in the input tile's LDS; the same requests in a smaller batch run
+    it two per CU. The arithmetic is the same, so the scores are
+    bit-identical."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     n_req = 4 * cus * 64 // 2000 + 4
-    cfg = mid("serving_bf16", n_requests=n_req, cand_per_request=2000)
+    cfg = mid("serving_bf16", n_requests=n_req, cand_per_request=2000,
+              widths=(768, 1024, 544, 256, 128, 64, 2))
     assert cfg.n_seq == 0 and (cfg.n_rows + 63) // 64 > 4 * cus
     log(f"test_many_tile_batch_equals_smaller_batch_bitwise: R={cfg.n_rows}, {cus} CUs")
     tables, params, batch = problem(cfg, seed=41)
