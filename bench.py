@@ -353,6 +353,32 @@ def _stage_of(kernel_name, dense_index):
     return None
 
 
+def _ours(rows):
+    """Dispatches of libcold kernels in launch order. rocprofv3 prints some
+    kernel names mangled and some demangled, so both forms are matched."""
+    ours = [r for r in rows if ("4cold" in r["Kernel_Name"] or "cold::" in r["Kernel_Name"])
+            and "clear_flag" not in r["Kernel_Name"] and "transpose_f32" not in r["Kernel_Name"]
+            and "pack_frag" not in r["Kernel_Name"]]
+    ours.sort(key=lambda r: int(r["Start_Timestamp"]))
+    return ours
+
+
+def _label_call(call):
+    """(stage, row) pairs of one scoring call. A demangled gather name does
+    not carry its pass; the gather right before the group mask is the
+    importance pass."""
+    out, di = [], 0
+    for r in call:
+        st = _stage_of(r["Kernel_Name"], di)
+        if st and st.startswith("dense"):
+            di += 1
+        out.append([st, r])
+    for i in range(len(out) - 1):
+        if out[i][0] == "gather_se" and out[i + 1][0] == "group_mask":
+            out[i][0] = "se_weights"
+    return [tuple(x) for x in out]
+
+
 def _call_starts(ours):
     """Indices of the first kernel of each scoring call: the per-request
     user pooling, or, in a call without one, the first gather after the
@@ -370,19 +396,11 @@ def _call_starts(ours):
 def _last_call(rows, key_start="Start_Timestamp"):
     """Dispatches of libcold kernels in the last complete scoring call,
     as (stage, row) pairs in launch order."""
-    ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
-    ours.sort(key=lambda r: int(r[key_start]))
+    ours = _ours(rows)
     starts = _call_starts(ours)
     if not starts:
         return []
-    call = ours[starts[-1]:]
-    out, di = [], 0
-    for r in call:
-        st = _stage_of(r["Kernel_Name"], di)
-        if st and st.startswith("dense"):
-            di += 1
-        out.append((st, r))
-    return out
+    return _label_call(ours[starts[-1]:])
 
 
 def summarize_trace(trace_dir, command):
@@ -392,16 +410,12 @@ def summarize_trace(trace_dir, command):
     import glob
     path = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
     rows = list(csv.DictReader(open(path)))
-    ours = [r for r in rows if "4cold" in r["Kernel_Name"] and "clear_flag" not in r["Kernel_Name"]]
-    ours.sort(key=lambda r: int(r["Start_Timestamp"]))
+    ours = _ours(rows)
     starts = _call_starts(ours)
     per_stage = {}
     for a, b in zip(starts, starts[1:] + [len(ours)]):
-        di = 0
-        for r in ours[a:b]:
-            st = _stage_of(r["Kernel_Name"], di) or "other"
-            if st.startswith("dense"):
-                di += 1
+        for st, r in _label_call(ours[a:b]):
+            st = st or "other"
             d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
             per_stage.setdefault(st, {"us": [], "kernel": r["Kernel_Name"], "grid": r.get("Grid_Size_X", r.get("Grid_Size", "?"))})["us"].append(d)
     lines = [f"# rocprofv3 kernel trace, per stage of one cold_score call", f"# command: {command}",
