@@ -690,7 +690,7 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
   constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
   constexpr int KS1 = BN / 32, KS2 = N1 / 32;
   static_assert(G::RING >= BR * HROW, "the layer's output tile takes the ring");
-  static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "one wave per tail feature block");
+  static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "8 waves: the tail layers split 4 (features) x 2 (rows)");
   static_assert(BR * (S1 + S2) * 2 <= G::RING, "both hidden tiles fit in the ring");
   __shared__ __align__(16) unsigned char smem[G::RING];
   __shared__ float s_wh[2 * N2];
@@ -723,12 +723,15 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
           packed;
     }
   }
-  // tail weights: wave w owns feature block w of the first tail layer and
-  // feature block w % 4, row blocks 2 (w / 4) and 2 (w / 4) + 1 of the second
-  frag w1f[KS1][1], w2f[KS2][1];
+  // tail weights: wave w owns feature blocks 2 (w % 4) and 2 (w % 4) + 1 of
+  // the first tail layer, and feature block w % 4 of the second, each on
+  // the rows BR/2 (w / 4) .. BR/2 (w / 4 + 1)
+  frag w1f[KS1][2], w2f[KS2][1];
 #pragma unroll
   for (int k = 0; k < KS1; ++k)
-    w1f[k][0] = *reinterpret_cast<const frag *>(W1 + frag_offset(wave, k, KS1, lane));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      w1f[k][i] = *reinterpret_cast<const frag *>(W1 + frag_offset(2 * (wave % 4) + i, k, KS1, lane));
 #pragma unroll
   for (int k = 0; k < KS2; ++k)
     w2f[k][0] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave % 4, k, KS2, lane));
@@ -736,17 +739,18 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
   if (tid < n_out) s_bh[tid] = bh[tid];
   __syncthreads();   // the layer's output tile and the head weights are in the LDS
 
-  // first tail layer on all 256 rows (wave w: feature block w); its input
-  // is dead once every wave has its sums, and its output takes its place
+  // first tail layer (each wave reads half of the tile's rows once for its
+  // two feature blocks); the tile is dead once every wave has its sums, and
+  // the layer's output takes its place
   auto in0 = [&](int row, int c) {
     return reinterpret_cast<const TS *>(smem + row * HROW + ((c ^ (row & 7)) << 4));
   };
-  f32x4 a1[1][BR / 16];
-  tail_mma<TS, KS1, 1, BR / 16>(in0, w1f, 0, lane, a1);
+  f32x4 a1[2][BR / 32];
+  tail_mma<TS, KS1, 2, BR / 32>(in0, w1f, (wave / 4) * (BR / 32), lane, a1);
   __syncthreads();
   TS *s_h1 = reinterpret_cast<TS *>(smem);
   TS *s_h2 = reinterpret_cast<TS *>(smem + BR * S1 * 2);
-  tail_store<TS, 1, BR / 16>(a1, b1, s_h1, S1, wave, 0, lane);
+  tail_store<TS, 2, BR / 32>(a1, b1, s_h1, S1, 2 * (wave % 4), (wave / 4) * (BR / 32), lane);
   __syncthreads();
   // second tail layer (wave w: feature block w % 4, rows BR/2 (w / 4) ..)
   auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
