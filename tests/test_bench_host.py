@@ -1,0 +1,81 @@
+"""Host-side logic of bench.py (no GPU): the algorithmic work of each stage
+and the splitting of a rocprofv3 kernel trace into scoring calls and stages."""
+import csv
+import os
+
+import numpy as np
+
+import bench
+from paper_2007_16122_amd import synth
+
+
+def _batch(cfg, R, Q):
+    return {"n_rows": R, "req_off": np.linspace(0, R, Q + 1).astype(np.int32),
+            "seq_off": np.zeros(1, np.int32)}
+
+
+def test_fused_stage_work_is_layer_plus_tail():
+    cfg = synth.CONFIGS["serving_bf16"]
+    b = _batch(cfg, 64_000, 32)
+    kind, fused = bench.stage_work(cfg, b, "dense_tail")
+    _, layer = bench.stage_work(cfg, b, "dense2")
+    _, tail = bench.stage_work(cfg, b, "tail")
+    assert kind == "mfma"
+    assert fused == layer + tail
+    # 2 * R * (512*256 + 256*128 + 128*64 + 64*2) for the serving widths
+    assert fused == 2.0 * 64_000 * (512 * 256 + 256 * 128 + 128 * 64 + 64 * 2)
+
+
+def test_mlp_flops_of_the_staged_path_cover_the_network():
+    cfg = synth.CONFIGS["serving_bf16"]
+    b = _batch(cfg, 64_000, 32)
+    staged = sum(bench.stage_work(cfg, b, st)[1] for st in ("dense0", "dense1", "dense_tail"))
+    w = cfg.widths
+    assert staged == 2.0 * 64_000 * sum(w[i] * w[i + 1] for i in range(len(w) - 1))
+
+
+MANGLED = {
+    "gather": "_ZN4cold16gather_se_kernelIDF16bLi{m}ELb0ELb0ELi8ELb0EEEvNS_10GatherArgsE",
+    "dense": "_ZN4cold21dense_relu_buf_kernelIDF16bLi128ELi128ELi2ELi2ELi2ELi64EEEvPKT_S3_PKfPS1_liiii",
+    "fused": "_ZN4cold17dense_tail_kernelIDF16bLi64ELi2EEEvPKT_S3_PKfliiS3_S5_S3_S5_S3_S5_iPf",
+}
+DEMANGLED_GATHER = "void cold::gather_se_kernel<bool _Accum, int, E, false, false, 8, false>(cold::GatherArgs)"
+MASK = ["cold::mask_partial_kernel(float const*, int const*, long, int, int, float*)",
+        "cold::mask_select_kernel(float const*, int const*, long, int, int, int, unsigned char*, unsigned char*)"]
+
+
+def _wide_call():
+    """Kernel names of one scoring call of a model with a group mask, with
+    the importance pass and the mask kernels printed demangled."""
+    return [DEMANGLED_GATHER, *MASK, MANGLED["gather"].format(m=2), MANGLED["dense"],
+            MANGLED["dense"], MANGLED["fused"]]
+
+
+def _write_trace(path, calls):
+    t = 1000
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, ["Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"])
+        w.writeheader()
+        w.writerow({"Kernel_Name": "void at::native::fill_kernel", "Start_Timestamp": t,
+                    "End_Timestamp": t + 5, "Grid_Size_X": 1})
+        for call in calls:
+            for name in call:
+                t += 1000
+                w.writerow({"Kernel_Name": name, "Start_Timestamp": t, "End_Timestamp": t + 500,
+                            "Grid_Size_X": 256})
+
+
+def test_trace_split_handles_demangled_names(tmp_path):
+    d = tmp_path / "trace"
+    d.mkdir()
+    _write_trace(os.path.join(d, "bench_kernel_trace.csv"), [_wide_call(), _wide_call()])
+    rows = list(csv.DictReader(open(os.path.join(d, "bench_kernel_trace.csv"))))
+    stages = [st for st, _ in bench._last_call(rows)]
+    assert stages == ["se_weights", "group_mask", "group_mask", "gather_apply", "dense0",
+                      "dense1", "dense_tail"]
+    text = bench.summarize_trace(str(d), "cmd")
+    assert "# 2 calls profiled" in text
+    lines = {l.split()[0]: l.split() for l in text.splitlines() if l and not l.startswith(("#", "stage"))}
+    assert int(lines["se_weights"][1]) == 2
+    assert int(lines["group_mask"][1]) == 4      # two kernels per call
+    assert float(lines["dense_tail"][2]) == 0.5  # mean duration in us
