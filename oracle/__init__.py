@@ -76,6 +76,9 @@ def lib():
         L.orc_hash_row.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint64]
         L.orc_cross_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         L.orc_cross_key.restype = ctypes.c_uint64
+        L.orc_decode_stored.restype = ctypes.c_int
+        L.orc_decode_stored.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -106,6 +109,17 @@ def hash_row(raw: int, g: int, rows: int) -> int:
 def cross_key(user_id: int, ad_id: int) -> int:
     """64-bit key of a user x ad cross value (see orc_cross_key)."""
     return int(lib().orc_cross_key(user_id & 0xFFFFFFFFFFFFFFFF, ad_id & 0xFFFFFFFFFFFFFFFF))
+
+
+def decode_stored(dtype: str, values: np.ndarray) -> np.ndarray:
+    """The checker's decoder of stored parameters (fp32, bf16 bit patterns
+    as uint16, or fp16) to float64."""
+    src = np.ascontiguousarray(values)
+    out = np.zeros(src.size, np.float64)
+    st = lib().orc_decode_stored(DTYPES[dtype], src.ctypes.data, src.size, out.ctypes.data)
+    if st != 0:
+        raise OracleError(_ERRORS.get(st, f"status {st}"))
+    return out
 
 
 def score(dims: dict, tables, params: dict, batch: dict, sample=None, *,

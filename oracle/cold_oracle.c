@@ -107,6 +107,15 @@ static double load_stored(int dtype, const void *p, int64_t i) {
   return from_f32(p, i);
 }
 
+/* The decoder above on n stored values (for the tests that pin it against
+ * an independent widening of every 16-bit pattern). */
+int orc_decode_stored(int32_t dtype, const void *p, int64_t n, double *out) {
+  if ((dtype != ORC_F32 && dtype != ORC_BF16 && dtype != ORC_F16) || n < 0 || (n > 0 && (!p || !out)))
+    return ORC_BAD_ARG;
+  for (int64_t i = 0; i < n; ++i) out[i] = load_stored(dtype, p, i);
+  return ORC_OK;
+}
+
 /* --------------------------------------------------------- id resolution */
 /* SplitMix64 output function (Steele, Lea, Flood, "Fast splittable
  * pseudorandom number generators", OOPSLA 2014). */

@@ -45,6 +45,41 @@ def run_brute(cfg, tables, params, batch):
                               [np.asarray(b, np.float64) for b in params["mlp_b"]], batch)
 
 
+# ------------------------------------------------- stored-value decoding
+def _same_f64(got, want):
+    """Equal as float64 bit patterns, except that any NaN matches any NaN."""
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan].view(np.uint64), want[~nan].view(np.uint64))
+
+
+def test_decode_f16_every_pattern():
+    """The checker's binary16 decoder on all 65,536 bit patterns (normals,
+    subnormals, signed zeros, infinities, NaNs) against numpy's own
+    float16 -> float64 widening."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    want = bits.view(np.float16).astype(np.float64)
+    got = oracle.decode_stored("f16", bits.view(np.float16))
+    _same_f64(got, want)
+    # the classes the synthetic inputs never produce are really covered
+    assert np.sum(np.isnan(want)) == 2 * 1023 and np.sum(np.isinf(want)) == 2
+    assert np.sum((want != 0) & (np.abs(want) < 2.0 ** -14)) == 2 * 1023
+
+
+def test_decode_bf16_every_pattern():
+    """bfloat16 patterns against the upper half of a binary32 pattern
+    widened by numpy."""
+    bits = np.arange(1 << 16, dtype=np.uint32)
+    want = (bits << 16).astype(np.uint32).view(np.float32).astype(np.float64)
+    got = oracle.decode_stored("bf16", bits.astype(np.uint16))
+    _same_f64(got, want)
+
+
+def test_decode_f32_passthrough():
+    v = np.array([0.0, -0.0, 1.5, -3.25e-41, np.inf, -np.inf, 3.4e38], np.float32)
+    _same_f64(oracle.decode_stored("f32", v), v.astype(np.float64))
+
+
 # --------------------------------------------------------------- Eq. 3
 def test_linear_log_golden():
     for x_tok, want in _read_golden("linear_log.txt"):
