@@ -252,8 +252,12 @@ def groups_sweep(base, counts, steps, warmup, torch, binding, synth, dev):
     return out
 
 
-def cpu_baseline(cfg, batch, params, target_s):
-    """The CPU checker, as it stands, on a bounded sample of the workload."""
+def cpu_baseline(cfg, batch, params, target_s, gpu_scores=None, one_core_s=0.0):
+    """The CPU checker, as it stands, on a bounded sample of the workload;
+    with `gpu_scores` (the GPU's scores of the whole batch) also the
+    |GPU - checker| CTR statistics over the sampled rows, and with
+    `one_core_s` > 0 the checker's rate on one thread over a smaller
+    sample."""
     import oracle
     from paper_2007_16122_amd import synth
     dims = dict(n_user=cfg.n_user, n_seq=cfg.n_seq, n_ad=cfg.n_ad, n_cross=cfg.n_cross,
@@ -310,10 +314,27 @@ def cpu_baseline(cfg, batch, params, target_s):
     t0 = time.perf_counter()
     o = oracle.score(dims, tabs, stored, batch, sample=sample, n_threads=threads)
     dt = time.perf_counter() - t0
-    return {"value": round(n / dt, 1), "unit": "ads/s", "cores": int(o["n_threads"]),
-            "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"first {n} rows (requests 0..{int(np.searchsorted(batch['req_off'], n - 1, side='right')) - 1}) "
-                      f"of the {cfg.name} batch, fp64 checker, {o['n_threads']} threads"}
+    out = {"value": round(n / dt, 1), "unit": "ads/s", "cores": int(o["n_threads"]),
+           "kind": "oracle", "seconds": round(dt, 2),
+           "sample": f"first {n} rows (requests 0..{int(np.searchsorted(batch['req_off'], n - 1, side='right')) - 1}) "
+                     f"of the {cfg.name} batch, fp64 checker, {o['n_threads']} threads"}
+    parity = None
+    if gpu_scores is not None:
+        d = np.abs(np.asarray(gpu_scores, np.float64)[sample] - o["scores"])
+        tol = 1e-5 if cfg.dtype == "f32" else 2e-3
+        parity = {"rows": int(n), "max_abs_dctr": float(d.max()),
+                  "p99_abs_dctr": float(np.quantile(d, 0.99)), "mean_abs_dctr": float(d.mean()),
+                  "tol": tol, "within_tol": bool(d.max() <= tol),
+                  "ctr_mean": float(o["scores"].mean()), "ctr_std": float(o["scores"].std())}
+    one = None
+    if one_core_s > 0:
+        n1 = int(min(n, max(len(probe), one_core_s / max(per_row * threads, 1e-9))))
+        t0 = time.perf_counter()
+        oracle.score(dims, tabs, stored, batch, sample=np.arange(n1), n_threads=1)
+        dt1 = time.perf_counter() - t0
+        one = {"value": round(n1 / dt1, 1), "unit": "ads/s", "cores": 1, "kind": "oracle",
+               "seconds": round(dt1, 2), "sample": f"first {n1} rows, one thread"}
+    return out, parity, one
 
 
 # ---------------------------------------------------------------------------
@@ -512,6 +533,8 @@ def main():
     ap.add_argument("--latency-iters", type=int, default=300)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-one-core-seconds", type=float, default=3.0,
+                    help="also time the checker on one thread for about this long (0 = skip)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain "
                          "copy of known size, to calibrate HBM byte counters)")
@@ -737,10 +760,13 @@ def main():
         log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
         del src, dst
 
-    cpu = None
+    cpu = parity = cpu1 = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, batch, params, args.cpu_seconds)
-        log(f"cpu baseline {cpu}")
+        cpu, parity, cpu1 = cpu_baseline(cfg, batch, params, args.cpu_seconds,
+                                         gpu_scores=scores.cpu().numpy(),
+                                         one_core_s=args.cpu_one_core_seconds)
+        log(f"cpu baseline {cpu}; one core {cpu1}")
+        log(f"parity over the checked rows: {parity}")
 
     out = {
         "metric": "candidate ads scored/sec on 1 GPU; p50 latency of a 2,000-ad request",
@@ -770,6 +796,8 @@ def main():
                         traffic=(traffic["stages"].get(e["name"]) if traffic else None))
                    for e in stage_rows],
         "cpu_baseline": cpu,
+        "cpu_baseline_one_core": cpu1,
+        "parity": parity,
         "topn": topn,
         "groups_sweep": sweep,
         "serving_streams": serving,

@@ -181,13 +181,18 @@ int cold_load_weights(cold_model *model, const cold_weights *w, void *arena,
  *   group_mask  device uint8 [Q][M] or NULL: kept groups per request (topk_k > 0)
  *   rows_out    device int32 [M][R] or NULL: table row each single-valued group
  *               of each row resolved to (-1 for sequence groups)
+ *   x_out       device [R][D_in] in the model dtype, or NULL: the network input
+ *               of each row, v_g = s_g e_g for every group (Section 3.2),
+ *               after the top-k mask and linear_log (Section 3.3, Eq. 3) and
+ *               the one rounding to the model dtype (a debug copy; the
+ *               scores do not depend on it)
  *   flags       0 or COLD_SCORE_VALIDATE (then the call synchronises the stream
  *               and returns COLD_ERR_ID_RANGE if any id or offset was out of range;
  *               without it such ids read a zero embedding)
  * Asynchronous on `stream` unless validating.  Q = 0 or R = 0 is a no-op. */
 int cold_score(cold_model *model, const cold_batch *b, void *workspace, size_t ws_bytes,
                float *scores, float *importance, uint8_t *group_mask, int32_t *rows_out,
-               int32_t flags, void *stream);
+               void *x_out, int32_t flags, void *stream);
 
 /* Stage timing, for measurement tools.  While enabled, every cold_score
  * call on this model records a HIP event on its stream before each kernel

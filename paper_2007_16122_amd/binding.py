@@ -94,7 +94,7 @@ def lib():
         L.cold_workspace_bytes.restype = sz
         L.cold_load_weights.argtypes = [vp, ctypes.POINTER(cold_weights), vp, sz, vp]
         L.cold_load_weights.restype = ctypes.c_int
-        L.cold_score.argtypes = [vp, ctypes.POINTER(cold_batch), vp, sz, vp, vp, vp, vp, i32, vp]
+        L.cold_score.argtypes = [vp, ctypes.POINTER(cold_batch), vp, sz, vp, vp, vp, vp, vp, i32, vp]
         L.cold_score.restype = ctypes.c_int
         L.cold_status_string.argtypes = [ctypes.c_int]
         L.cold_status_string.restype = ctypes.c_char_p
@@ -137,9 +137,9 @@ def cold_load_weights(h, w: cold_weights, arena: int, arena_bytes: int, stream: 
 
 def cold_score(h, b: cold_batch, workspace: int, ws_bytes: int, scores: int,
                importance: Optional[int], group_mask: Optional[int], rows_out: Optional[int],
-               flags: int, stream: int) -> int:
+               x_out: Optional[int], flags: int, stream: int) -> int:
     return lib().cold_score(h, ctypes.byref(b), workspace, ws_bytes, scores, importance,
-                            group_mask, rows_out, flags, stream)
+                            group_mask, rows_out, x_out, flags, stream)
 
 
 def cold_status_string(st: int) -> str:
@@ -288,7 +288,7 @@ class ColdModel:
                           seq_off=_ptr(batch.get("seq_off")), seq_ids=_ptr(batch.get("seq_ids")))
 
     def score(self, batch: dict, scores=None, importance=None, group_mask=None, rows_out=None,
-              validate=False, workspace=None):
+              validate=False, workspace=None, x_out=None):
         """Score every row; returns the fp32 score tensor (asynchronous on
         the current stream unless validate).  Concurrent calls on different
         streams pass distinct `workspace` tensors (uint8, device, at least
@@ -299,7 +299,7 @@ class ColdModel:
         if scores is None:
             scores = torch.empty(b.n_rows, dtype=torch.float32, device=self.device)
         st = cold_score(self.h, b, _ptr(ws), ws.numel(), _ptr(scores), _ptr(importance),
-                        _ptr(group_mask), _ptr(rows_out),
+                        _ptr(group_mask), _ptr(rows_out), _ptr(x_out),
                         COLD_SCORE_VALIDATE if validate else 0, self._stream())
         if st != COLD_OK:
             raise ColdError(st, "cold_score: " + cold_last_error(self.h))

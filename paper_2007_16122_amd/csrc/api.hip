@@ -375,8 +375,8 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
 }
 
 int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_bytes, float *scores,
-               float *importance, uint8_t *group_mask, int32_t *rows_out, int32_t flags,
-               void *stream) {
+               float *importance, uint8_t *group_mask, int32_t *rows_out, void *x_out,
+               int32_t flags, void *stream) {
   if (!m) return COLD_ERR_INVALID_ARG;
   if (!b) return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null batch");
   if (flags & ~COLD_SCORE_VALIDATE) return fail(m, COLD_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
@@ -490,17 +490,21 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
     if ((e = launch_gather_se(m->dtype, kApplyWeights, D.linear_log, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se (apply) launch");
   }
+  if (x_out) {   // debug copy of the network input
+    if ((e = hipMemcpyAsync(x_out, W + wl.X, (size_t)m->es * R * m->D_in, hipMemcpyDeviceToDevice,
+                            s)) != hipSuccess)
+      return hip_fail(m, e, "network input copy");
+  }
   // network: hidden layers ping-pong between two activation buffers; the
   // last two hidden layers and the head run fused when their widths allow
   const int L = D.n_layers;
   const bool fuse_tail = L >= 3 && tail_supported(m->dtype, m->widths[L - 3], m->widths[L - 2],
                                                   m->widths[L - 1], m->widths[L]);
   const int n_separate = fuse_tail ? L - 3 : L - 1;
-  // the last separate layer runs in the tail's kernel when it is 256 wide,
-  // from 4,096 rows up: a single 2,000-ad request scores sooner with the two
-  // kernels (p50 0.0598 against 0.0606 ms on one box)
-  constexpr int64_t kDenseTailMinRows = 4096;
-  const bool dense_tail = fuse_tail && n_separate >= 1 && R >= kDenseTailMinRows &&
+  // the last separate layer runs in the tail's kernel when it is 256 wide
+  // with K in 64-deep steps, for every batch size (the choice depends on the
+  // model alone, so a score does not depend on the batch it is scored in)
+  const bool dense_tail = fuse_tail && n_separate >= 1 &&
                           dense_tail_supported(m->dtype, R, m->widths[n_separate],
                                                m->widths[n_separate - 1]);
   const void *in = W + wl.X;

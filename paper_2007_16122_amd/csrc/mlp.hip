@@ -14,15 +14,15 @@
 //                   batches, 64 x 64 for a single request.
 //  dense_relu_mfma  the same layer with register-staged, double-buffered LDS
 //                   tiles; used when K is not a multiple of 32.
-//  mlp_tail         the last two hidden layers and the head fused over
-//                   64-row tiles held in LDS.
+//  dense_tail       the last separate hidden layer (512 -> 256) fused with
+//                   the tail: the last two hidden layers and the head, with
+//                   the tail's activations carried at about twice the
+//                   storage precision (hi/lo pairs, see the tail section).
+//  mlp_tail         the tail alone over 64-row tiles held in LDS.
 //  dense_relu_f32   the layer in fp32 FMA (the fp32 model).
 //  head             last layer (n_out = 1 or 2) in fp32 plus sigmoid or
 //                   two-way softmax; writes the CTR.
-#include <mutex>
 #include <type_traits>
-#include <utility>
-#include <vector>
 
 #include "cold_internal.h"
 
@@ -475,25 +475,55 @@ hipError_t launch_pack_frag(const void *src, void *dst, int64_t N, int32_t K, hi
 }
 
 // ---------------------------------------------------------------------------
-// Fused tail: the last two hidden layers and the output head in one kernel,
-// K0 -> N1 -> N2 (ReLU) -> n_out (sigmoid or softmax), for 64-row tiles.  The
-// row tile lives in LDS between layers; the small weight matrices (N1 x K0 and
-// N2 x N1, fragment-major, see frag_offset) are read as MFMA fragments
-// straight from global memory, where every workgroup finds them in L2.
-// Hidden activations are rounded to the storage type between layers, as the
-// separate layers do.
-// One hidden layer of the fused tail on rows held in the LDS:
-// out[r][n] = round(ReLU(b[n] + sum_k W[n][k] in[r][k])) for the 16-row
-// blocks jb0 .. jb0 + JB - 1 and the 16-feature blocks nb0 .. nb0 + NB - 1.
-// The K steps are summed from zero in order and the bias is added last, so
-// every output is the same whichever wave computes it. tail_mma forms the
-// sums (in_at(row, c) is the LDS address of 16-byte chunk c of an input row;
-// wf[k][i] is the weight fragment of feature block nb0 + i and K step k);
-// tail_store adds the bias, applies ReLU, rounds and writes the rows
-// (s_out_stride elements apart). Between the two the caller may pass a
-// barrier and then overwrite the input.
-template <typename TS, int KS, int NB, int JB, typename InAt>
-__device__ __forceinline__ void tail_mma(const InAt &in_at,
+// Fused tail: the last two hidden layers and the output head, K0 -> N1 -> N2
+// (ReLU) -> n_out (sigmoid or softmax), on row tiles held in LDS; the small
+// weight matrices (N1 x K0 and N2 x N1, fragment-major, see frag_offset) are
+// read as MFMA fragments straight from global memory, where every workgroup
+// finds them in L2.
+//
+// Precision of the tail. Its layers are narrow (the last one feeds the 64
+// inputs of the head directly), so rounding their activations to the storage
+// type moves the CTR more than the rounding of every wider layer before them.
+// The tail therefore carries each hidden activation v (fp32, after bias and
+// ReLU) as a pair hi = RNE(v), lo = RNE(v - hi) of storage-type values (v - hi
+// is exact in fp32), about twice the storage precision, and a layer takes
+// both halves through the matrix cores: W hi + W lo, two MFMAs per product,
+// summed in fp32. The last hidden layer's output stays in fp32 and the head
+// reads it as such. Every sum of the tail runs in the same order whichever
+// kernel, tile shape or wave computes it.
+
+// the two storage-type values packed in one 32-bit word, widened to fp32
+template <typename TS> __device__ __forceinline__ void unpack2(uint32_t w, float &a, float &b);
+template <> __device__ __forceinline__ void unpack2<__bf16>(uint32_t w, float &a, float &b) {
+  a = __uint_as_float(w << 16);
+  b = __uint_as_float(w & 0xFFFF0000u);
+}
+template <> __device__ __forceinline__ void unpack2<_Float16>(uint32_t w, float &a, float &b) {
+  a = static_cast<float>(__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu)));
+  b = static_cast<float>(__builtin_bit_cast(_Float16, (uint16_t)(w >> 16)));
+}
+
+// hi/lo pairs of two fp32 values (see above); a value whose hi is not finite
+// (beyond the storage range) gets lo = 0
+template <typename TS>
+__device__ __forceinline__ void split2(float v0, float v1, uint32_t &hi, uint32_t &lo) {
+  hi = round2<TS>(v0, v1);
+  float h0, h1;
+  unpack2<TS>(hi, h0, h1);
+  const float d0 = __builtin_isfinite(h0) ? v0 - h0 : 0.0f;
+  const float d1 = __builtin_isfinite(h1) ? v1 - h1 : 0.0f;
+  lo = round2<TS>(d0, d1);
+}
+
+// MFMA sums of one tail layer on rows held in LDS: acc[i][j] = sum over K of
+// W[n][k] in[r][k] for the 16-row blocks jb0 .. jb0 + JB - 1 and the
+// NB 16-feature blocks of wf, from zero, K steps in order. in_at(row, c) is
+// the LDS address of 16-byte chunk c of an input row; with EXT the low halves
+// of the input sit lo_bytes after the high halves, and each K step adds
+// W hi, then W lo. wf[k][i] is the weight fragment of feature block i and K
+// step k.
+template <typename TS, int KS, int NB, int JB, bool EXT, typename InAt>
+__device__ __forceinline__ void tail_mma(const InAt &in_at, int lo_bytes,
                                          const typename Mfma<TS>::frag (&wf)[KS][NB], int jb0,
                                          int lane, f32x4 (&acc)[NB][JB]) {
   typedef typename Mfma<TS>::frag frag;
@@ -506,59 +536,91 @@ __device__ __forceinline__ void tail_mma(const InAt &in_at,
   for (int k = 0; k < KS; ++k) {
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
-      const frag fb = *reinterpret_cast<const frag *>(in_at((jb0 + j) * 16 + frow, 4 * k + fq));
+      const TS *p = in_at((jb0 + j) * 16 + frow, 4 * k + fq);
+      const frag fb = *reinterpret_cast<const frag *>(p);
+      frag fl;
+      if constexpr (EXT) fl = *reinterpret_cast<const frag *>(reinterpret_cast<const char *>(p) + lo_bytes);
 #pragma unroll
-      for (int i = 0; i < NB; ++i) acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
+      for (int i = 0; i < NB; ++i) {
+        acc[i][j] = Mfma<TS>::mac(wf[k][i], fb, acc[i][j]);
+        if constexpr (EXT) acc[i][j] = Mfma<TS>::mac(wf[k][i], fl, acc[i][j]);
+      }
     }
   }
 }
 
+// bias, ReLU, then the hi/lo pair of every output: row (jb0 + j) * 16 + lane % 16,
+// features (nb0 + i) * 16 + 4 (lane / 16) .. + 3; the low halves go lo_elems
+// elements after the high halves
 template <typename TS, int NB, int JB>
-__device__ __forceinline__ void tail_store(const f32x4 (&acc)[NB][JB], const float *__restrict__ bg,
-                                           TS *out, int s_out_stride, int nb0, int jb0, int lane) {
+__device__ __forceinline__ void tail_store_ext(const f32x4 (&acc)[NB][JB], const float *__restrict__ bg,
+                                               TS *out, int stride, int lo_elems, int nb0, int jb0,
+                                               int lane) {
   const int dn = (lane >> 4) * 4, dr = lane & 15;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int n = (nb0 + i) * 16 + dn;
+    float bv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bv[e] = bg[n + e];
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
-      float o[4];
+      float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float t = acc[i][j][e] + bg[n + e];
-        o[e] = t > 0.0f ? t : 0.0f;
+        const float t = acc[i][j][e] + bv[e];
+        v[e] = t > 0.0f ? t : 0.0f;
       }
-      uint2 packed;
-      packed.x = (uint32_t)Elem<TS>::bits(o[0]) | ((uint32_t)Elem<TS>::bits(o[1]) << 16);
-      packed.y = (uint32_t)Elem<TS>::bits(o[2]) | ((uint32_t)Elem<TS>::bits(o[3]) << 16);
-      *reinterpret_cast<uint2 *>(&out[((jb0 + j) * 16 + dr) * s_out_stride + n]) = packed;
+      uint2 hi, lo;
+      split2<TS>(v[0], v[1], hi.x, lo.x);
+      split2<TS>(v[2], v[3], hi.y, lo.y);
+      TS *o = out + ((jb0 + j) * 16 + dr) * stride + n;
+      *reinterpret_cast<uint2 *>(o) = hi;
+      *reinterpret_cast<uint2 *>(o + lo_elems) = lo;
     }
   }
 }
 
-template <typename TS, int KS, int NB, int JB, typename InAt>
-__device__ __forceinline__ void tail_layer(const InAt &in_at, const float *__restrict__ bg, TS *out,
-                                           int s_out_stride,
-                                           const typename Mfma<TS>::frag (&wf)[KS][NB], int nb0,
-                                           int jb0, int lane) {
-  f32x4 acc[NB][JB];
-  tail_mma<TS, KS, NB, JB>(in_at, wf, jb0, lane, acc);
-  tail_store<TS, NB, JB>(acc, bg, out, s_out_stride, nb0, jb0, lane);
+// bias and ReLU in fp32, stored as fp32 (the last hidden layer)
+template <int NB, int JB>
+__device__ __forceinline__ void tail_store_f32(const f32x4 (&acc)[NB][JB], const float *__restrict__ bg,
+                                               float *out, int stride, int nb0, int jb0, int lane) {
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int n = (nb0 + i) * 16 + dn;
+    float bv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bv[e] = bg[n + e];
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      float4 v;
+      v.x = acc[i][j][0] + bv[0];
+      v.y = acc[i][j][1] + bv[1];
+      v.z = acc[i][j][2] + bv[2];
+      v.w = acc[i][j][3] + bv[3];
+      v.x = v.x > 0.0f ? v.x : 0.0f;
+      v.y = v.y > 0.0f ? v.y : 0.0f;
+      v.z = v.z > 0.0f ? v.z : 0.0f;
+      v.w = v.w > 0.0f ? v.w : 0.0f;
+      *reinterpret_cast<float4 *>(out + ((jb0 + j) * 16 + dr) * stride + n) = v;
+    }
+  }
 }
 
-// Output head of the fused tail: 4 threads per row (row tid / 4),
+// Output head of the fused tail on fp32 rows: 4 threads per row (row tid / 4),
 // each summing a quarter of the N2 inputs in order, then two shuffle steps;
-// sigmoid (one logit) or two-way softmax, CTR = class 1. Rows at or past R
-// are not stored.
-template <typename TS, int N2>
-__device__ __forceinline__ void tail_head(const TS *s_h2, int s2, const float *s_wh,
+// sigmoid (one logit) or two-way softmax, CTR = class 1. row_of maps the
+// LDS row to the batch row; rows at or past R are not stored.
+template <int N2, typename RowOf>
+__device__ __forceinline__ void tail_head(const float *h2, int s2, const float *s_wh,
                                           const float *s_bh, int n_out, float *__restrict__ scores,
-                                          int64_t r0, int64_t R, int tid) {
+                                          const RowOf &row_of, int64_t R, int tid) {
   const int row = tid >> 2, q = tid & 3;
   float z0 = 0.0f, z1 = 0.0f;
 #pragma unroll 4
   for (int k = q * (N2 / 4); k < (q + 1) * (N2 / 4); ++k) {
-    const float x = Elem<TS>::to_f32(s_h2[row * s2 + k]);
+    const float x = h2[row * s2 + k];
     z0 += s_wh[k] * x;
     if (n_out > 1) z1 += s_wh[N2 + k] * x;
   }
@@ -566,7 +628,7 @@ __device__ __forceinline__ void tail_head(const TS *s_h2, int s2, const float *s
   z0 += __shfl_xor(z0, 2);
   z1 += __shfl_xor(z1, 1);
   z1 += __shfl_xor(z1, 2);
-  const int64_t r = r0 + row;
+  const int64_t r = row_of(row);
   if (q == 0 && r < R) {
     z0 += s_bh[0];
     if (n_out > 1) z1 += s_bh[1];
@@ -574,15 +636,13 @@ __device__ __forceinline__ void tail_head(const TS *s_h2, int s2, const float *s
   }
 }
 
-// MINB workgroups per CU. At 2 the register budget (256 per lane) holds the
-// input tile and every weight fragment at once, as they are loaded (the
-// shortest chain per tile; batches of a few tiles per CU). At 3 the second
-// hidden layer's output also takes the input tile's LDS, which is dead once
-// the first layer is done, so three workgroups fit per CU, and the compiler
-// reloads some fragments within 168 registers (batches of many tiles per CU).
-// The arithmetic, and so every score, is the same for both.
-template <typename TS, int K0, int N1, int N2, int MINB>
-__global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restrict__ A,
+// The tail as a kernel of its own (the layer before it is not fused with
+// it: its K is not a multiple of 64, or there is none): 64-row tiles, input
+// tile in the storage type from global memory, first layer on it, then the
+// extended-precision second layer and head. Two workgroups per CU (the
+// second hidden tile takes the input tile's LDS once the first layer is done).
+template <typename TS, int K0, int N1, int N2>
+__global__ __launch_bounds__(256, 2) void mlp_tail_kernel(const TS *__restrict__ A,
                                                        const TS *__restrict__ W1,
                                                        const float *__restrict__ b1,
                                                        const TS *__restrict__ W2,
@@ -592,16 +652,13 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
                                                        float *__restrict__ scores, int64_t R) {
   typedef typename Mfma<TS>::frag frag;
   constexpr int BR = 64;
-  constexpr int S0 = K0 + 8, S1 = N1 + 8, S2 = N2 + 8;   // padded LDS rows
+  constexpr int S0 = K0 + 8, S1 = N1 + 8, S2 = N2 + 4;   // padded LDS rows
   static_assert(K0 % 32 == 0 && N1 % 32 == 0 && N2 % 32 == 0 && N1 % 64 == 0 && N2 % 64 == 0,
                 "tail widths");
+  static_assert(BR * S2 * 4 <= BR * S0 * 2, "the last hidden tile fits in the input tile");
   __shared__ __align__(16) TS s_in[BR * S0];
-  __shared__ __align__(16) TS s_h1[BR * S1];
-  static_assert(MINB == 2 || MINB == 3, "tail occupancy");
-  constexpr bool kAlias = MINB == 3;
-  static_assert(!kAlias || S2 <= S0, "second hidden tile fits in the input tile");
-  __shared__ __align__(16) TS s_h2_own[kAlias ? 8 : BR * S2];
-  TS *s_h2 = kAlias ? s_in : s_h2_own;
+  __shared__ __align__(16) TS s_h1[2 * BR * S1];       // hi, then lo
+  float *s_h2 = reinterpret_cast<float *>(s_in);        // after the first layer
   __shared__ float s_wh[2 * N2];
   __shared__ float s_bh[2];
 
@@ -653,27 +710,32 @@ __global__ __launch_bounds__(256, MINB) void mlp_tail_kernel(const TS *__restric
 
   // wave w owns the output features [w*N/4, (w+1)*N/4) of each layer
   auto in0 = [&](int row, int c) { return s_in + row * S0 + c * 8; };
-  tail_layer<TS, KS1, NB1, BR / 16>(in0, b1, s_h1, S1, w1f, wave * NB1, 0, lane);
-  __syncthreads();
+  f32x4 a1[NB1][BR / 16];
+  tail_mma<TS, KS1, NB1, BR / 16, false>(in0, 0, w1f, 0, lane, a1);
+  tail_store_ext<TS, NB1, BR / 16>(a1, b1, s_h1, S1, BR * S1, wave * NB1, 0, lane);
+  __syncthreads();   // the input tile is dead: the last hidden tile takes its place
   auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
-  tail_layer<TS, KS2, NB2, BR / 16>(in1, b2, s_h2, S2, w2f, wave * NB2, 0, lane);
+  f32x4 a2[NB2][BR / 16];
+  tail_mma<TS, KS2, NB2, BR / 16, true>(in1, BR * S1 * 2, w2f, 0, lane, a2);
+  tail_store_f32<NB2, BR / 16>(a2, b2, s_h2, S2, wave * NB2, 0, lane);
   __syncthreads();
-  tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0, R, tid);
+  tail_head<N2>(s_h2, S2, s_wh, s_bh, n_out, scores, [&](int row) { return r0 + row; }, R, tid);
 }
 
 // The last separate hidden layer and the fused tail in one kernel, when that
 // layer is 256 wide (the tail's input): a BR x 256 output tile holds whole
 // rows of the tail's input. BR = 256 for large batches (the tiles of the
 // separate layer), 64 for batches of fewer than one 256-row tile per CU.
-// The layer is the 256 x 256 K loop of dense_relu_buf_kernel with the same
-// rounding; its output tile stays in the LDS (the ring, free after the K
-// loop: 256 rows of 512 bytes, 16-byte chunk c of row r at slot c ^ (r & 7),
-// so the tail's fragment reads of 8 rows hit 8 different slots), and the
-// tail's two layers and head run on it in four 64-row chunks with the
-// device functions of mlp_tail_kernel, 8 waves each taking one 16-feature
-// block of the first layer and half a 16-feature block column of the second.
-// Every score is bit-identical to the separate layer followed by
-// mlp_tail_kernel, and the layer's output never goes to HBM.
+// The layer is the 256 x 256 K loop of dense_relu_buf_kernel; its output
+// (bias and ReLU in fp32) becomes hi/lo pairs in the LDS ring, which is free
+// after the K loop (PR-row passes: 128 rows of hi, then of lo, 512 bytes a
+// row, 16-byte chunk c of row r at slot c ^ (r & 7), so the tail's fragment
+// reads of 8 rows hit 8 different slots), and the tail's two layers and head
+// run on each pass, 8 waves each taking two 16-feature blocks of the first
+// layer and one of the second over half of the pass's rows. A 256-row tile
+// takes two passes: pass p holds row blocks 4p .. 4p + 3 of every wave's
+// 128 rows, so each wave frees half of its accumulators per pass. The
+// layer's output never goes to HBM.
 template <typename TS, int BR, int MINB>
 __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
     const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
@@ -686,15 +748,24 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
   typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NI = G::NI, RJ = G::RJ;
   constexpr int N1 = 128, N2 = 64;                     // tail widths
-  constexpr int S1 = N1 + 8, S2 = N2 + 8;              // padded LDS rows of the tail
+  constexpr int S1 = N1 + 8, S2 = N2 + 4;              // padded LDS rows of the tail
   constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
   constexpr int KS1 = BN / 32, KS2 = N1 / 32;
-  static_assert(G::RING >= BR * HROW, "the layer's output tile takes the ring");
+  constexpr int PR = BR < 128 ? BR : 128;              // rows per pass
+  constexpr int NP = BR / PR, JP = RJ / NP;            // passes; row blocks of a wave per pass
+  constexpr int JB = PR / 32;                          // row blocks of a wave in the tail layers
+  constexpr int H3_BYTES = 2 * PR * HROW;              // hi and lo of the layer's output
+  constexpr int H1_BYTES = 2 * PR * S1 * 2, H2_BYTES = PR * S2 * 4;
+  // head weights in the ring when it has room past the layer's output
+  constexpr bool WH_IN_RING = G::RING >= H3_BYTES + 2 * N2 * 4 + 16;
+  static_assert(G::RING >= H3_BYTES, "a pass of the layer's output takes the ring");
   static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "8 waves: the tail layers split 4 (features) x 2 (rows)");
-  static_assert(BR * (S1 + S2) * 2 <= G::RING, "both hidden tiles fit in the ring");
+  static_assert(H1_BYTES + H2_BYTES <= H3_BYTES, "both hidden tiles fit where the layer's output was");
+  static_assert(RJ % NP == 0 && PR * 4 <= 512, "passes");
   __shared__ __align__(16) unsigned char smem[G::RING];
-  __shared__ float s_wh[2 * N2];
-  __shared__ float s_bh[2];
+  __shared__ float s_whb_own[WH_IN_RING ? 1 : 2 * N2 + 4];
+  float *s_wh = WH_IN_RING ? reinterpret_cast<float *>(smem + H3_BYTES) : s_whb_own;
+  float *s_bh = s_wh + 2 * N2;
 
   const int tile = xcd_tile(blockIdx.x, tiles_total);
   const int64_t r0 = (int64_t)tile * BR;
@@ -705,27 +776,9 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
   f32x4 acc[NI][RJ];
   buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, BN, K, r0, 0, smem, acc);
 
-  // the layer's output: round, ReLU (as dense_relu_buf_kernel), into the LDS
-  compiler_fence();
-  __builtin_amdgcn_s_barrier();
-  compiler_fence();
-  const int dn = (lane >> 4) * 4, dr = lane & 15;
-#pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const int n = wn * (BN / WN) + i * 16 + dn;
-#pragma unroll
-    for (int j = 0; j < RJ; ++j) {
-      const int rl = wr * (BR / 2) + j * 16 + dr;
-      uint2 packed;
-      packed.x = relu_bits2(round2<TS>(acc[i][j][0], acc[i][j][1]));
-      packed.y = relu_bits2(round2<TS>(acc[i][j][2], acc[i][j][3]));
-      *reinterpret_cast<uint2 *>(smem + rl * HROW + (((n >> 3) ^ (rl & 7)) << 4) + (n & 7) * 2) =
-          packed;
-    }
-  }
   // tail weights: wave w owns feature blocks 2 (w % 4) and 2 (w % 4) + 1 of
   // the first tail layer, and feature block w % 4 of the second, each on
-  // the rows BR/2 (w / 4) .. BR/2 (w / 4 + 1)
+  // the rows PR/2 (w / 4) .. PR/2 (w / 4 + 1) of a pass
   frag w1f[KS1][2], w2f[KS2][1];
 #pragma unroll
   for (int k = 0; k < KS1; ++k)
@@ -735,34 +788,68 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
 #pragma unroll
   for (int k = 0; k < KS2; ++k)
     w2f[k][0] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave % 4, k, KS2, lane));
-  if (tid < n_out * N2) s_wh[tid] = Elem<TS>::to_f32(Wh[tid]);
-  if (tid < n_out) s_bh[tid] = bh[tid];
-  __syncthreads();   // the layer's output tile and the head weights are in the LDS
+  const float whv = Elem<TS>::to_f32(Wh[tid < n_out * N2 ? tid : 0]);
+  const float bhv = bh[tid < n_out ? tid : 0];
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();   // every wave is past the K loop: the ring is free
+  compiler_fence();
+  if (tid < n_out * N2) s_wh[tid] = whv;
+  if (tid < n_out) s_bh[tid] = bhv;
 
-  // first tail layer (each wave reads half of the tile's rows once for its
-  // two feature blocks); the tile is dead once every wave has its sums, and
-  // the layer's output takes its place
-  auto in0 = [&](int row, int c) {
-    return reinterpret_cast<const TS *>(smem + row * HROW + ((c ^ (row & 7)) << 4));
-  };
-  f32x4 a1[2][BR / 32];
-  tail_mma<TS, KS1, 2, BR / 32>(in0, w1f, (wave / 4) * (BR / 32), lane, a1);
-  __syncthreads();
+  const int dn = (lane >> 4) * 4, dr = lane & 15;
   TS *s_h1 = reinterpret_cast<TS *>(smem);
-  TS *s_h2 = reinterpret_cast<TS *>(smem + BR * S1 * 2);
-  tail_store<TS, 2, BR / 32>(a1, b1, s_h1, S1, 2 * (wave % 4), (wave / 4) * (BR / 32), lane);
-  __syncthreads();
-  // second tail layer (wave w: feature block w % 4, rows BR/2 (w / 4) ..)
-  auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
-  tail_layer<TS, KS2, 1, BR / 32>(in1, b2, s_h2, S2, w2f, wave % 4, (wave / 4) * (BR / 32), lane);
-  __syncthreads();
-  // head, 128 rows per pass (a 64-row tile: waves 0-3)
-  if constexpr (BR >= 128) {
+  float *s_h2 = reinterpret_cast<float *>(smem + H1_BYTES);
 #pragma unroll
-    for (int p = 0; p < BR / 128; ++p)
-      tail_head<TS, N2>(s_h2 + p * 128 * S2, S2, s_wh, s_bh, n_out, scores, r0 + p * 128, R, tid);
-  } else {
-    if (wave < BR / 16) tail_head<TS, N2>(s_h2, S2, s_wh, s_bh, n_out, scores, r0, R, tid);
+  for (int p = 0; p < NP; ++p) {
+    // this pass's rows of the layer's output: bias (in the accumulators),
+    // ReLU, hi/lo pairs into the LDS
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int n = wn * (BN / WN) + i * 16 + dn;
+#pragma unroll
+      for (int jj = 0; jj < JP; ++jj) {
+        const int j = p * JP + jj;
+        const int rl = wr * (PR / 2) + jj * 16 + dr;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e] > 0.0f ? acc[i][j][e] : 0.0f;
+        uint2 hi, lo;
+        split2<TS>(v[0], v[1], hi.x, lo.x);
+        split2<TS>(v[2], v[3], hi.y, lo.y);
+        unsigned char *o = smem + rl * HROW + (((n >> 3) ^ (rl & 7)) << 4) + (n & 7) * 2;
+        *reinterpret_cast<uint2 *>(o) = hi;
+        *reinterpret_cast<uint2 *>(o + PR * HROW) = lo;
+      }
+    }
+    __syncthreads();   // the pass's tile (and the head weights) are in the LDS
+
+    // first tail layer (each wave reads half of the pass's rows once for its
+    // two feature blocks); the tile is dead once every wave has its sums, and
+    // the layer's output takes its place
+    auto in0 = [&](int row, int c) {
+      return reinterpret_cast<const TS *>(smem + row * HROW + ((c ^ (row & 7)) << 4));
+    };
+    f32x4 a1[2][JB];
+    tail_mma<TS, KS1, 2, JB, true>(in0, PR * HROW, w1f, (wave / 4) * JB, lane, a1);
+    __syncthreads();
+    tail_store_ext<TS, 2, JB>(a1, b1, s_h1, S1, PR * S1, 2 * (wave % 4), (wave / 4) * JB, lane);
+    __syncthreads();
+    // second tail layer (wave w: feature block w % 4, rows PR/2 (w / 4) ..),
+    // output in fp32 after the first layer's
+    auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
+    f32x4 a2[1][JB];
+    tail_mma<TS, KS2, 1, JB, true>(in1, PR * S1 * 2, w2f, (wave / 4) * JB, lane, a2);
+    tail_store_f32<1, JB>(a2, b2, s_h2, S2, wave % 4, (wave / 4) * JB, lane);
+    __syncthreads();
+    // head: LDS row lr of the pass is row (lr / (PR/2)) * (BR/2) + p * (PR/2)
+    // + lr % (PR/2) of the tile
+    if (tid < PR * 4)
+      tail_head<N2>(s_h2, S2, s_wh, s_bh, n_out, scores,
+                    [&](int lr) {
+                      return r0 + (lr / (PR / 2)) * (BR / 2) + p * (PR / 2) + lr % (PR / 2);
+                    },
+                    R, tid);
+    if (p + 1 < NP) __syncthreads();   // the next pass overwrites the tail's tiles
   }
 }
 
@@ -995,26 +1082,11 @@ bool tail_supported(int dtype, int K0, int N1, int N2, int n_out) {
   return dtype != kF32 && K0 == 256 && N1 == 128 && N2 == 64 && (n_out == 1 || n_out == 2);
 }
 
-// CUs of the current device (cached per device)
-static int device_cus() {
-  static std::mutex mu;
-  static std::vector<std::pair<int, int>> cache;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  std::lock_guard<std::mutex> lk(mu);
-  for (const auto &e : cache)
-    if (e.first == dev) return e.second;
-  int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  cache.emplace_back(dev, cus);
-  return cus;
-}
-
-template <typename TS, int MINB>
+template <typename TS>
 static void launch_tail_t(const void *a, const void *w1, const float *b1, const void *w2,
                           const float *b2, const void *wh, const float *bh, int32_t n_out,
                           float *scores, int64_t R, hipStream_t s) {
-  hipLaunchKernelGGL((mlp_tail_kernel<TS, 256, 128, 64, MINB>), dim3((unsigned)((R + 63) / 64)),
+  hipLaunchKernelGGL((mlp_tail_kernel<TS, 256, 128, 64>), dim3((unsigned)((R + 63) / 64)),
                      dim3(256), 0, s, static_cast<const TS *>(a), static_cast<const TS *>(w1), b1,
                      static_cast<const TS *>(w2), b2, static_cast<const TS *>(wh), bh, n_out,
                      scores, R);
@@ -1024,15 +1096,8 @@ hipError_t launch_mlp_tail(int dtype, const void *a, const void *w1, const float
                            const void *w2, const float *b2, const void *wh, const float *bh,
                            int32_t n_out, float *scores, int64_t R, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  // more than four 64-row tiles per CU: three workgroups per CU
-  const bool many = (R + 63) / 64 > 4 * (int64_t)device_cus();
-  if (dtype == kBF16) {
-    if (many) launch_tail_t<__bf16, 3>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
-    else launch_tail_t<__bf16, 2>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
-  } else {
-    if (many) launch_tail_t<_Float16, 3>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
-    else launch_tail_t<_Float16, 2>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
-  }
+  if (dtype == kBF16) launch_tail_t<__bf16>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+  else launch_tail_t<_Float16>(a, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   return hipGetLastError();
 }
 

@@ -67,7 +67,7 @@ class ColdConfig:
     seq_len_max: int = 50
     init: str = "he"           # "normal005" | "he"
     seq_table: str = "tri"     # value scheme of the sequence tables
-    out_gain: float = 6.0      # output-layer scale relative to He init ("he" init)
+    out_gain: float = 15.0     # output-layer scale relative to He init ("he" init)
     out_bias: float = -2.0     # output-layer bias of the click class ("he" init)
     seed: int = 2007_16122
     # () : cross ids come with the batch; else ((user field, ad field), ...)
@@ -122,28 +122,27 @@ CONFIGS = {
         name="serving_bf16", n_requests=32, cand_per_request=2000,
         n_user=12, n_seq=0, n_ad=24, n_cross=12, emb_dim=16, vocab=1_000_000,
         zipf_s=1.05, dtype="bf16", se_reduction=4, widths=_mlp(48 * 16),
-        head="softmax2", out_gain=5.5, out_bias=-2.0, seed=2007_16122 + 1),
+        head="softmax2", seed=2007_16122 + 1),
     # as serving, plus 6 sum-pooled behaviour sequences; fp16 + linear_log.
     "multivalued_fp16_ll": ColdConfig(
         name="multivalued_fp16_ll", n_requests=32, cand_per_request=2000,
         n_user=12, n_seq=6, n_ad=24, n_cross=12, emb_dim=16, vocab=1_000_000,
         zipf_s=1.05, dtype="f16", se_reduction=4, widths=_mlp(54 * 16),
-        head="softmax2", linear_log=True, seq_table="big", out_gain=0.27,
-        out_bias=-3.0, seed=2007_16122 + 2),
+        head="softmax2", linear_log=True, seq_table="big", out_gain=0.19,
+        seed=2007_16122 + 2),
     # 128 requests x 10k ads, 64 fields with 10M-row hashed tables, fp16.
     "large_fp16_ll": ColdConfig(
         name="large_fp16_ll", n_requests=128, cand_per_request=10_000,
         n_user=16, n_seq=0, n_ad=32, n_cross=16, emb_dim=16, vocab=10_000_000,
         zipf_s=1.0, dtype="f16", se_reduction=4, widths=_mlp(64 * 16),
-        head="softmax2", linear_log=True, hashed=True, out_gain=11.0, out_bias=-3.5,
-        seed=2007_16122 + 3),
+        head="softmax2", linear_log=True, hashed=True, seed=2007_16122 + 3),
     # 1 request x 5000 ads, 200 fields; SE importance + top-k group mask.
     "wide_prune_bf16": ColdConfig(
         name="wide_prune_bf16", n_requests=1, cand_per_request=5000,
         n_user=50, n_seq=0, n_ad=100, n_cross=50, emb_dim=16,
         vocab=1_000_000, zipf_s=1.05, dtype="bf16", se_reduction=4,
         widths=_mlp(200 * 16), head="softmax2", topk_k=100,
-        emit_importance=True, out_gain=6.0, out_bias=-2.0, seed=2007_16122 + 4),
+        emit_importance=True, seed=2007_16122 + 4),
 }
 
 
@@ -407,10 +406,11 @@ def make_params(cfg: ColdConfig, seed: Optional[int] = None) -> dict:
     ``he``: SE W1 ~ N(0, 10/sqrt(M)), b1 ~ N(0, 0.1), W2 ~ N(0, 1/sqrt(H)),
     b2 ~ N(0, 1) (so groups differ in importance); hidden MLP layers
     N(0, sqrt(2/fan_in)) with biases N(0, 0.01); the output layer at
-    ``out_gain`` times that scale with bias ``out_bias`` on the click class.
-    The two are set per workload so that, on its inputs, the logit spreads by
-    about 0.1 (bf16) or 0.4 (fp16) around a mean CTR of 5-15%: a trained
-    model's logit scale, not one a random network happens to produce.
+    ``out_gain`` (15) times that scale with bias ``out_bias`` (-2) on the
+    click class.  The behaviour-sequence workload, whose linear_log'd pooled
+    groups are about 300 times larger than an embedding, takes the gain that
+    gives its logit the spread of the serving workload's at 15 (0.19).
+    Its SE W1 columns of the pooled groups are scaled by 2^-20 (see below).
     """
     seed = cfg.seed if seed is None else seed
     rng = np.random.default_rng(np.random.SeedSequence([seed, 0x5E, 0x3A]))
@@ -426,6 +426,13 @@ def make_params(cfg: ColdConfig, seed: Optional[int] = None) -> dict:
         se_b1 = rng.normal(0, 0.1, h).astype(f32)
         se_w2 = rng.normal(0, 1.0 / math.sqrt(h), (m, h)).astype(f32)
         se_b2 = rng.normal(0, 1.0, m).astype(f32)
+        if cfg.n_seq and cfg.seq_table == "big":
+            # the squeeze of a pooled large-value sequence group is about
+            # 2^20 times that of an embedding group (std ~1.2e4 against
+            # ~0.013); its W1 columns are scaled by 2^-20 so that it moves
+            # the SE logits as much as any other group, instead of driving
+            # every weight to 0 or 1
+            se_w1[:, cfg.n_user:cfg.n_user + cfg.n_seq] *= f32(2.0 ** -20)
     if cfg.se_form == "literal":
         # se_w1 [M][D_in], se_b1 [M]; drawn from a stream of their own so the
         # network weights are those of the squeeze form of the same workload

@@ -42,9 +42,13 @@ def stored_params(cfg, params: dict) -> dict:
     return out
 
 
-def problem(cfg, seed=None, cand=None, scheme=None, params=None):
-    tables = [synth.table_numpy(cfg, g, seed=seed, scheme=scheme) for g in range(cfg.n_groups)]
-    params = synth.make_params(cfg, seed) if params is None else params
+def problem(cfg, seed=None, cand=None, scheme=None, params=None, model_seed=None):
+    """Tables, parameters and a batch of a configuration.  The batch comes
+    from `seed`; the model (tables and parameters) from `model_seed` when it
+    is given (cfg.seed: the configured model itself), else from `seed`."""
+    ms = seed if model_seed is None else model_seed
+    tables = [synth.table_numpy(cfg, g, seed=ms, scheme=scheme) for g in range(cfg.n_groups)]
+    params = synth.make_params(cfg, ms) if params is None else params
     batch = synth.make_batch(cfg, seed, cand)
     return tables, params, batch
 

@@ -2,6 +2,8 @@
 the CPU checker on the same seeded inputs, and compare."""
 from __future__ import annotations
 
+import json
+import os
 import sys
 import time
 
@@ -82,7 +84,8 @@ class GpuRun:
         self.tables_dev = tables_dev
         self.model.load(tables_dev, self.params_dev)
 
-    def score(self, batch_np, want_rows=False, want_s=False, want_mask=False, validate=True):
+    def score(self, batch_np, want_rows=False, want_s=False, want_mask=False, want_x=False,
+              validate=True):
         torch = self.torch
         cfg = self.cfg
         b = binding.batch_to_device(batch_np, self.device)
@@ -91,7 +94,11 @@ class GpuRun:
         rows = torch.full((m, max(r_n, 1)), -7, dtype=torch.int32, device=self.device) if want_rows else None
         imp = torch.zeros((max(r_n, 1), m), dtype=torch.float32, device=self.device) if want_s else None
         mask = torch.zeros((max(q_n, 1), m), dtype=torch.uint8, device=self.device) if want_mask else None
-        scores = self.model.score(b, importance=imp, group_mask=mask, rows_out=rows, validate=validate)
+        xdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype]
+        x = torch.full((max(r_n, 1), cfg.d_in), float("nan"), dtype=xdt, device=self.device) \
+            if want_x else None
+        scores = self.model.score(b, importance=imp, group_mask=mask, rows_out=rows, x_out=x,
+                                  validate=validate)
         torch.cuda.synchronize(self.device)
         out = {"scores": scores.cpu().numpy().astype(np.float64)}
         if want_rows:
@@ -100,6 +107,8 @@ class GpuRun:
             out["s"] = imp.cpu().numpy()[:r_n]
         if want_mask:
             out["mask"] = mask.cpu().numpy()[:q_n]
+        if want_x:
+            out["x"] = x[:r_n].to(torch.float32).cpu().numpy().astype(np.float64)
         return out
 
     def close(self):
@@ -113,7 +122,18 @@ def run_oracle(cfg, tables, params, batch, sample=None, **kw):
     return o
 
 
+def record(entry: dict) -> None:
+    """Append one JSON line to the file COLD_PARITY_LOG names (if set)."""
+    path = os.environ.get("COLD_PARITY_LOG")
+    if path:
+        with open(path, "a") as fh:
+            fh.write(json.dumps(entry) + "\n")
+
+
 def compare_scores(cfg, got, want, label=""):
+    """|GPU - checker| CTR statistics, asserted within the tolerance of the
+    model's dtype.  With COLD_PARITY_LOG set, each comparison is also
+    appended to that file as one JSON line."""
     d = np.abs(got - want)
     tol = TOL[cfg.dtype]
     stats = dict(max=float(d.max()) if d.size else 0.0,
@@ -121,6 +141,9 @@ def compare_scores(cfg, got, want, label=""):
                  mean=float(d.mean()) if d.size else 0.0, n=int(d.size))
     log(f"[{label}] |dCTR| max {stats['max']:.3e} p99 {stats['p99']:.3e} "
         f"mean {stats['mean']:.3e} over {stats['n']} rows (tol {tol:g})")
+    record(dict(stats, label=label, workload=cfg.name, dtype=cfg.dtype, tol=tol,
+                ctr_mean=float(np.mean(want)) if d.size else 0.0,
+                ctr_std=float(np.std(want)) if d.size else 0.0))
     assert np.all(np.isfinite(got)), "non-finite GPU score"
     assert stats["max"] <= tol, stats
     return stats
@@ -145,3 +168,34 @@ def request_slice(cfg, batch, q):
         out["seq_off"] = np.zeros(1, np.int32)
         out["seq_ids"] = np.zeros(0, batch["ad_ids"].dtype)
     return out
+
+
+def with_empty_sequences(cfg, batch, empties):
+    """The batch with the behaviour sequences (field f, request q) in
+    `empties` emptied (Section 3.3: an empty sequence pools to zero)."""
+    q_n = len(batch["req_off"]) - 1
+    so, ids = batch["seq_off"], batch["seq_ids"]
+    segs = []
+    for f in range(cfg.n_seq):
+        for q in range(q_n):
+            seg = ids[so[f * q_n + q]:so[f * q_n + q + 1]]
+            segs.append(seg[:0] if (f, q) in empties else seg)
+    out = dict(batch)
+    out["seq_off"] = np.concatenate([[0], np.cumsum([len(x) for x in segs])]).astype(np.int32)
+    out["seq_ids"] = np.concatenate(segs) if segs else ids[:0]
+    return out
+
+
+def half_ulp(x, dtype):
+    """The spacing of the model dtype's values at |x| (the unit in the last
+    place of the rounded network input): fp16 10 fraction bits with
+    subnormals below 2^-14, bf16 7 fraction bits."""
+    ax = np.abs(np.asarray(x, np.float64))
+    if dtype == "f16":
+        e = np.floor(np.log2(np.maximum(ax, 2.0 ** -14)))
+        return 2.0 ** (e - 10)
+    if dtype == "bf16":
+        e = np.floor(np.log2(np.maximum(ax, 2.0 ** -126)))
+        return 2.0 ** (e - 7)
+    e = np.floor(np.log2(np.maximum(ax, 2.0 ** -126)))
+    return 2.0 ** (e - 23)

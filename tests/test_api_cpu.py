@@ -109,14 +109,14 @@ def test_score_before_load_and_bad_calls():
     h = B.cold_create_model(d)
     try:
         b = B.cold_batch(n_requests=1, n_rows=10)
-        st = B.cold_score(h, b, None, 0, None, None, None, None, 0, None)
+        st = B.cold_score(h, b, None, 0, None, None, None, None, None, 0, None)
         assert st == B.COLD_ERR_NOT_LOADED
         assert "before cold_load_weights" in B.cold_last_error(h)
-        st = B.lib().cold_score(h, None, None, 0, None, None, None, None, 0, None)
+        st = B.lib().cold_score(h, None, None, 0, None, None, None, None, None, 0, None)
         assert st == B.COLD_ERR_INVALID_ARG
-        st = B.cold_score(h, b, None, 0, None, None, None, None, 0x10, None)
+        st = B.cold_score(h, b, None, 0, None, None, None, None, None, 0x10, None)
         assert st == B.COLD_ERR_INVALID_ARG
-        assert B.lib().cold_score(None, ctypes.byref(b), None, 0, None, None, None, None, 0,
+        assert B.lib().cold_score(None, ctypes.byref(b), None, 0, None, None, None, None, None, 0,
                                   None) == B.COLD_ERR_INVALID_ARG
         w = B.cold_weights()
         assert B.cold_load_weights(h, w, None, 0, None) == B.COLD_ERR_INVALID_ARG

@@ -85,7 +85,7 @@ def test_recall_of_gpu_scores_against_checker_scores():
     batch against the top-200 of the checker-scored one (same bids)."""
     base = synth.CONFIGS["serving_bf16"]
     cfg = synth.config("serving_bf16", vocab=20_000)
-    tables, params, batch = problem(cfg, seed=31, cand=[2000] * 4)
+    tables, params, batch = problem(cfg, seed=31, cand=[2000] * 4, model_seed=cfg.seed)
     run = GpuRun(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
     try:
         g = run.score(batch)

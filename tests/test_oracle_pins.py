@@ -302,6 +302,28 @@ def test_linear_log_inside_path():
                 assert o["x"][r, g * d + k] == pytest.approx(want, abs=1e-15)
 
 
+def test_sequence_workload_inputs_exercise_se_and_linear_log():
+    """The behaviour-sequence workload's inputs are shaped so that its
+    parity checks reach both parts of the method they exist for: the SE
+    weights (Section 3.2, Eq. 2) of every group, pooled ones included, stay
+    fractional rather than saturating at 0 or 1, and pooled values still
+    pass the fp16 range before linear_log (Section 3.3, Eq. 3)."""
+    cfg = synth.config("multivalued_fp16_ll", vocab=4000)
+    tables, params, batch = problem(cfg, seed=5, cand=[300, 200, 1, 250])
+    o = run_oracle(cfg, tables, params, batch, want_s=True, want_x=True)
+    s = o["s"]
+    saturated = (s < 1e-6) | (s > 1.0 - 1e-6)
+    seq = slice(cfg.n_user, cfg.n_user + cfg.n_seq)
+    assert saturated.mean() < 0.01 and saturated[:, seq].mean() < 0.01, saturated.mean()
+    # every pooled group's weight varies across rows (requests)
+    assert np.all(s[:, seq].std(axis=0) > 1e-3)
+    # |s e| > 65504 for some pooled coordinates: x = LL(s e) > 1 + ln 65504
+    d = cfg.emb_dim
+    xs = o["x"][:, cfg.n_user * d:(cfg.n_user + cfg.n_seq) * d]
+    frac = np.mean(np.abs(xs) > 1.0 + math.log(65504.0))
+    assert frac > 0.001, frac
+
+
 # ----------------------------------------------------------- invariants
 @pytest.mark.parametrize("name", ["tiny_fp32", "serving_bf16", "multivalued_fp16_ll",
                                   "large_fp16_ll"])

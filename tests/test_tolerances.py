@@ -26,26 +26,40 @@ def fp32_se(params, z):
     return expit(logit.astype(np.float64))
 
 
-def _fixture(name, cand, seed):
+def _fixture(name, cand, seed, w1_seq_scale=1.0):
     base = synth.CONFIGS[name]
     cfg = synth.config(name, vocab=20_000, seq_len_max=base.seq_len_max)
-    tables, params, batch = problem(cfg, seed=seed, cand=cand)
+    params = synth.make_params(cfg, seed)
+    if w1_seq_scale != 1.0:
+        params["se_w1"] = params["se_w1"].copy()
+        params["se_w1"][:, cfg.n_user:cfg.n_user + cfg.n_seq] *= np.float32(w1_seq_scale)
+    tables, params, batch = problem(cfg, seed=seed, cand=cand, params=params)
     o = run_oracle(cfg, tables, params, batch, want_s=True, want_z=True)
     assert np.array_equal(o["z"].astype(np.float32).astype(np.float64), o["z"])
     return params, o["z"], o["s"]
 
 
 def test_se_bound_covers_fp32_on_large_pooled_sums():
-    """Pooled sequences of the large-value table reach |z| ~ 1e5, where fp32
-    SE weights drift by up to ~1e-3 on a few dozen of 124,200 weights; the
-    bound must cover that drift and stay at its 2e-6 floor elsewhere."""
+    """Pooled sequences of the large-value table reach |z| ~ 1e5.  With the
+    pooled groups' W1 columns at the scale of the others (2^20 times the
+    workload's own), their SE logits reach ~1e4 and fp32 SE weights drift by
+    up to ~1e-3 on a few dozen of 124,200 weights; the bound must cover that
+    drift and stay at its 2e-6 floor elsewhere."""
     cand = [int(c) for c in np.random.default_rng(7).integers(0, 4, size=1500)]
-    params, z, s = _fixture("multivalued_fp16_ll", cand, 27)
+    params, z, s = _fixture("multivalued_fp16_ll", cand, 27, w1_seq_scale=2.0 ** 20)
     bound = se_weight_bound(params, z, s)
     err = np.abs(fp32_se(params, z) - s)
     assert err.max() > 1e-4          # the stress case really stresses fp32
     assert np.all(err <= bound)
     assert np.median(bound) <= 2.0001e-6 and np.mean(bound > 1e-4) < 1e-3
+
+
+def test_se_bound_on_the_sequence_workload():
+    """The sequence workload as drawn (pooled groups' W1 columns scaled to
+    the others' logit spread): fp32 stays inside the bound."""
+    params, z, s = _fixture("multivalued_fp16_ll", [257, 0, 1, 500], 21)
+    bound = se_weight_bound(params, z, s)
+    assert np.all(np.abs(fp32_se(params, z) - s) <= bound)
 
 
 def test_se_bound_is_tight_on_ordinary_rows():
