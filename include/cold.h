@@ -194,6 +194,23 @@ int cold_score(cold_model *model, const cold_batch *b, void *workspace, size_t w
                float *scores, float *importance, uint8_t *group_mask, int32_t *rows_out,
                void *x_out, int32_t flags, void *stream);
 
+/* Scoring for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * cold_score with its workspace in a device array that the library holds,
+ * COLD_NOALLOC_WORKSPACE_BYTES on each GPU it runs on, until the process
+ * ends; the other arguments as for cold_score.  The stream (NULL: the null
+ * stream) must belong to the current device.  A batch whose
+ * cold_workspace_bytes(R, Q) exceeds the array (the serving model: more
+ * than five 2,000-ad requests) returns COLD_ERR_WORKSPACE with nothing
+ * enqueued.  Every call on one GPU uses that GPU's one array, which keeps
+ * the last call's contents: calls that overlap on one GPU (other streams,
+ * other threads) race, so the caller serialises them.  Calls no allocating
+ * routine; stage profiling does not record these calls. */
+#define COLD_NOALLOC_WORKSPACE_BYTES (64ull * 1024 * 1024)
+int cold_score_noalloc(cold_model *model, const cold_batch *b, float *scores, float *importance,
+                       uint8_t *group_mask, int32_t *rows_out, void *x_out, int32_t flags,
+                       void *stream);
+
 /* Stage timing, for measurement tools.  While enabled, every cold_score
  * call on this model records a HIP event on its stream before each kernel
  * stage and one after the last; cold_profile_read synchronises those events

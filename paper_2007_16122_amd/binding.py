@@ -32,7 +32,8 @@ DTYPES = {"f32": COLD_F32, "bf16": COLD_BF16, "f16": COLD_F16}
 EXPORTS = ("cold_create_model", "cold_destroy_model", "cold_weight_arena_bytes",
            "cold_workspace_bytes", "cold_load_weights", "cold_score",
            "cold_status_string", "cold_last_error", "cold_profile_enable",
-           "cold_profile_read", "cold_select_topn")
+           "cold_profile_read", "cold_select_topn", "cold_score_noalloc")
+COLD_NOALLOC_WORKSPACE_BYTES = 64 * 1024 * 1024
 COLD_TOPN_MAX = 1024
 COLD_SE_SQUEEZE, COLD_SE_LITERAL = 0, 1
 
@@ -96,6 +97,8 @@ def lib():
         L.cold_load_weights.restype = ctypes.c_int
         L.cold_score.argtypes = [vp, ctypes.POINTER(cold_batch), vp, sz, vp, vp, vp, vp, vp, i32, vp]
         L.cold_score.restype = ctypes.c_int
+        L.cold_score_noalloc.argtypes = [vp, ctypes.POINTER(cold_batch), vp, vp, vp, vp, vp, i32, vp]
+        L.cold_score_noalloc.restype = ctypes.c_int
         L.cold_status_string.argtypes = [ctypes.c_int]
         L.cold_status_string.restype = ctypes.c_char_p
         L.cold_last_error.argtypes = [vp]
@@ -140,6 +143,13 @@ def cold_score(h, b: cold_batch, workspace: int, ws_bytes: int, scores: int,
                x_out: Optional[int], flags: int, stream: int) -> int:
     return lib().cold_score(h, ctypes.byref(b), workspace, ws_bytes, scores, importance,
                             group_mask, rows_out, x_out, flags, stream)
+
+
+def cold_score_noalloc(h, b: cold_batch, scores: int, importance: Optional[int],
+                       group_mask: Optional[int], rows_out: Optional[int], x_out: Optional[int],
+                       flags: int, stream: int) -> int:
+    return lib().cold_score_noalloc(h, ctypes.byref(b), scores, importance, group_mask, rows_out,
+                                    x_out, flags, stream)
 
 
 def cold_status_string(st: int) -> str:

@@ -6,6 +6,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "cold.h"
@@ -139,8 +140,8 @@ struct StageMarks {
   hipStream_t s;
   ProfSet *set = nullptr;
   size_t n = 0;
-  StageMarks(cold_model *m_, hipStream_t s_) : m(m_), s(s_) {
-    if (!m->prof_on || m->prof_used >= kMaxProfiledCalls) return;
+  StageMarks(cold_model *m_, hipStream_t s_, bool enabled) : m(m_), s(s_) {
+    if (!enabled || !m->prof_on || m->prof_used >= kMaxProfiledCalls) return;
     if (m->prof_used == m->prof.size()) m->prof.emplace_back();
     set = &m->prof[m->prof_used++];
     set->names.clear();
@@ -374,32 +375,42 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
   return COLD_OK;
 }
 
-int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_bytes, float *scores,
-               float *importance, uint8_t *group_mask, int32_t *rows_out, void *x_out,
-               int32_t flags, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks of a scoring call that do not involve the workspace.
+// Returns COLD_OK, a negative status (recorded on the model), or 1 for a
+// valid empty batch (nothing to do).
+int check_call(cold_model *m, const cold_batch *b, const float *scores, int32_t flags,
+               const char *who) {
   if (!m) return COLD_ERR_INVALID_ARG;
-  if (!b) return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null batch");
+  if (!b) return fail(m, COLD_ERR_INVALID_ARG, "%s: null batch", who);
   if (flags & ~COLD_SCORE_VALIDATE) return fail(m, COLD_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
-  if (!m->loaded) return fail(m, COLD_ERR_NOT_LOADED, "cold_score before cold_load_weights");
+  if (!m->loaded) return fail(m, COLD_ERR_NOT_LOADED, "%s before cold_load_weights", who);
   const int64_t Q = b->n_requests, R = b->n_rows;
   if (Q < 0 || R < 0 || b->n_seq_ids < 0) return fail(m, COLD_ERR_INVALID_ARG, "negative size");
   if (Q == 0 && R > 0) return fail(m, COLD_ERR_SHAPE, "rows without requests");
   if (R > 0x7FFFFFFFll * 16 || Q > 0x7FFFFFFF) return fail(m, COLD_ERR_SHAPE, "batch too large");
-  if (Q == 0 || R == 0) return COLD_OK;
+  if (Q == 0 || R == 0) return 1;
   const cold_model_desc &D = m->desc;
-  if (!b->req_off || !scores || !workspace ||
+  if (!b->req_off || !scores ||
       (D.n_user > 0 && !b->user_ids) || (D.n_ad > 0 && !b->ad_ids) ||
       (D.n_cross > 0 && !D.cross_pairs && !b->cross_ids) || (D.n_seq > 0 && !b->seq_off) ||
       (D.n_seq > 0 && b->n_seq_ids > 0 && !b->seq_ids))
-    return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null pointer");
-  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
-    return fail(m, COLD_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
-  const WorkLayout wl = work_layout(*m, R, Q);
-  if (ws_bytes < wl.total)
-    return fail(m, COLD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, wl.total);
+    return fail(m, COLD_ERR_INVALID_ARG, "%s: null pointer", who);
+  return COLD_OK;
+}
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  unsigned char *W = static_cast<unsigned char *>(workspace);
+// The launch sequence of one scoring call on a checked batch, with the
+// workspace regions at W (work_layout(R, Q) bytes, 256-byte aligned).  With
+// profile, stage events are recorded when the model's profiling is on.
+int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *scores,
+                 float *importance, uint8_t *group_mask, int32_t *rows_out, void *x_out,
+                 int32_t flags, hipStream_t s, bool profile) {
+  const int64_t Q = b->n_requests, R = b->n_rows;
+  const cold_model_desc &D = m->desc;
+  const WorkLayout wl = work_layout(*m, R, Q);
   unsigned char *A = m->arena_ptr;
   const ArenaLayout &al = m->arena;
   const bool topk = D.topk_k > 0;
@@ -430,7 +441,7 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
 
   hipError_t e;
   const bool validate = flags & COLD_SCORE_VALIDATE;
-  StageMarks marks(m, s);
+  StageMarks marks(m, s, profile);
   static const char *kDenseNames[] = {"dense0", "dense1", "dense2", "dense3", "dense4", "dense5",
                                       "dense6", "dense7", "dense8", "dense9", "dense10", "dense11"};
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
@@ -551,6 +562,89 @@ int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_by
                           (flag & 2) ? "offsets" : "");
   }
   return COLD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cold_score(cold_model *m, const cold_batch *b, void *workspace, size_t ws_bytes, float *scores,
+               float *importance, uint8_t *group_mask, int32_t *rows_out, void *x_out,
+               int32_t flags, void *stream) {
+  const int st = check_call(m, b, scores, flags, "cold_score");
+  if (st != COLD_OK) return st == 1 ? COLD_OK : st;
+  if (!workspace) return fail(m, COLD_ERR_INVALID_ARG, "cold_score: null pointer");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(m, COLD_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
+  const size_t need = work_layout(*m, b->n_rows, b->n_requests).total;
+  if (ws_bytes < need)
+    return fail(m, COLD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  return score_launch(m, b, static_cast<unsigned char *>(workspace), scores, importance, group_mask,
+                      rows_out, x_out, flags, static_cast<hipStream_t>(stream), true);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------- scoring without allocation
+// The workspace of cold_score_noalloc: a device array the library holds,
+// one copy per GPU it runs on, until the process ends.  In host code this
+// name is not a device address; hipGetSymbolAddress gives each device's copy.
+static __device__ __align__(256) unsigned char scratch[COLD_NOALLOC_WORKSPACE_BYTES];
+
+static_assert(COLD_NOALLOC_WORKSPACE_BYTES % 256 == 0, "workspace regions are 256-byte aligned");
+
+namespace {
+
+// Device address of `scratch` on device dev (the current device), looked up
+// once per device and kept.
+hipError_t scratch_address(int dev, unsigned char **out) {
+  static std::mutex mu;
+  static std::vector<std::pair<int, unsigned char *>> known;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const auto &e : known)
+    if (e.first == dev) {
+      *out = e.second;
+      return hipSuccess;
+    }
+  void *p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!p) return hipErrorInvalidSymbol;
+  known.emplace_back(dev, static_cast<unsigned char *>(p));
+  *out = static_cast<unsigned char *>(p);
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cold_score_noalloc(cold_model *m, const cold_batch *b, float *scores, float *importance,
+                       uint8_t *group_mask, int32_t *rows_out, void *x_out, int32_t flags,
+                       void *stream) {
+  const int st = check_call(m, b, scores, flags, "cold_score_noalloc");
+  if (st != COLD_OK) return st == 1 ? COLD_OK : st;
+  const size_t need = work_layout(*m, b->n_rows, b->n_requests).total;
+  if (need > COLD_NOALLOC_WORKSPACE_BYTES)
+    return fail(m, COLD_ERR_WORKSPACE,
+                "cold_score_noalloc: the batch needs %zu bytes of workspace, more than the "
+                "library's %llu-byte array; score it with cold_score and a workspace",
+                need, (unsigned long long)COLD_NOALLOC_WORKSPACE_BYTES);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int cur = -1, dev = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return hip_fail(m, e, "cold_score_noalloc: current device");
+  dev = cur;
+  if (s && (e = hipStreamGetDevice(s, &dev)) != hipSuccess)
+    return hip_fail(m, e, "cold_score_noalloc: stream device");
+  if (dev != cur)
+    return fail(m, COLD_ERR_INVALID_ARG,
+                "cold_score_noalloc: the stream is on device %d, the current device is %d", dev,
+                cur);
+  unsigned char *W = nullptr;
+  if ((e = scratch_address(dev, &W)) != hipSuccess)
+    return hip_fail(m, e, "cold_score_noalloc: workspace address");
+  return score_launch(m, b, W, scores, importance, group_mask, rows_out, x_out, flags, s, false);
 }
 
 }  // extern "C"
