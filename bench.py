@@ -503,6 +503,51 @@ def summarize_mfma(pmc_dir, command, workload, simds, xcds):
     return "\n".join(lines) + "\n"
 
 
+def summarize_parity(run_dir, command):
+    """profiles/parity_<workload>.txt from one GPU run: the |GPU - checker|
+    CTR statistics of every parity test (the JSON lines the tests append to
+    COLD_PARITY_LOG) and of the bench's checked sample (bench_<workload>.json)."""
+    tests = {}
+    path = os.path.join(run_dir, "parity.jsonl")
+    if os.path.exists(path):
+        for line in open(path):
+            e = json.loads(line)
+            if "max" in e:
+                tests.setdefault(e["workload"], []).append(e)
+    written = []
+    names = sorted(set(tests) | {f[6:-5] for f in os.listdir(run_dir)
+                                 if f.startswith("bench_") and f.endswith(".json")})
+    for w in names:
+        lines = [f"# |GPU - checker| CTR per parity check, workload {w}",
+                 f"# command: {command}"]
+        bj = os.path.join(run_dir, f"bench_{w}.json")
+        if os.path.exists(bj):
+            rows = [l for l in open(bj).read().splitlines() if l.startswith("{")]
+            if rows:
+                b = json.loads(rows[-1])
+                p = b.get("parity")
+                if p:
+                    lines.append(f"# bench.py --workload {w}: full-size batch, the checked sample of "
+                                 f"the CPU baseline leg ({b['cpu_baseline']['sample']})")
+                    lines.append(f"{'check':52s} {'rows':>7s} {'max':>9s} {'p99':>9s} {'mean':>9s} "
+                                 f"{'tol':>7s} {'ctr_mean':>8s} {'ctr_std':>8s}")
+                    lines.append(f"{'bench full-size sample':52s} {p['rows']:7d} {p['max_abs_dctr']:9.2e} "
+                                 f"{p['p99_abs_dctr']:9.2e} {p['mean_abs_dctr']:9.2e} {p['tol']:7.0e} "
+                                 f"{p['ctr_mean']:8.4f} {p['ctr_std']:8.4f}")
+        if w in tests:
+            if len(lines) == 2:
+                lines.append(f"{'check':52s} {'rows':>7s} {'max':>9s} {'p99':>9s} {'mean':>9s} "
+                             f"{'tol':>7s} {'ctr_mean':>8s} {'ctr_std':>8s}")
+            for e in tests[w]:
+                lines.append(f"{e['label'][:52]:52s} {e['n']:7d} {e['max']:9.2e} {e['p99']:9.2e} "
+                             f"{e['mean']:9.2e} {e['tol']:7.0e} {e['ctr_mean']:8.4f} {e['ctr_std']:8.4f}")
+        out = os.path.join(ROOT, "profiles", f"parity_{w}.txt")
+        with open(out, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        written.append(out)
+    return written
+
+
 def _stage_sources(stage):
     """Source files that define a stage's kernel (with the shared header)."""
     if stage.startswith("dense") or stage in ("tail", "head", "se_dense"):
@@ -565,6 +610,9 @@ def main():
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--summarize-parity", metavar="DIR",
+                    help="write profiles/parity_<workload>.txt from a GPU run's parity.jsonl "
+                         "(tests with COLD_PARITY_LOG) and bench_<workload>.json files, and exit")
     ap.add_argument("--summarize-mfma", metavar="DIR",
                     help="print matrix-core utilisation per stage from a run with "
                          "--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE")
@@ -572,6 +620,10 @@ def main():
     ap.add_argument("--xcds", type=int, default=8, help="XCDs on the chip")
     ap.add_argument("--profile-command", default="", help="command recorded in summaries")
     args = ap.parse_args()
+    if args.summarize_parity:
+        for path in summarize_parity(args.summarize_parity, args.profile_command):
+            print(path)
+        return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.profile_command), end="")
         return

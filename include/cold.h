@@ -152,24 +152,39 @@ typedef struct cold_batch {
   const void *seq_ids;
 } cold_batch;
 
-/* Validate a model description and create the host-side model.  CPU only.
- * *out receives a library-owned handle (free with cold_destroy_model). */
+/* Validate a model description and create the host-side model: one deep
+ * CTR model that scores every candidate ad of a request (Section 2, the
+ * pre-ranking problem; Section 3.1, the network over concatenated
+ * group-wise embeddings; Section 4.1, its widths).  CPU only.  *out
+ * receives a library-owned handle (free with cold_destroy_model).  Returns
+ * COLD_ERR_INVALID_ARG / _SHAPE / _DTYPE for a description outside the
+ * supported shapes above, with *out set to NULL. */
 int cold_create_model(const cold_model_desc *desc, cold_model **out);
 
-/* Free the host-side model (never device memory).  NULL is a no-op. */
+/* Free the host-side model made by cold_create_model (never device
+ * memory: the arena, tables and workspaces stay the caller's).  NULL is a
+ * no-op. */
 void cold_destroy_model(cold_model *model);
 
-/* Bytes of device memory the caller must provide as the weight arena. */
+/* Bytes of device memory the caller must provide as the weight arena: the
+ * SE parameters (Section 3.2, Eq. 2) and the network's weights and biases
+ * (Section 4.1), plus per-table metadata.  0 for a NULL model. */
 size_t cold_weight_arena_bytes(const cold_model *model);
 
-/* Bytes of device workspace cold_score needs for up to max_rows rows and
- * max_requests requests (0 if the model is NULL or a size is negative). */
+/* Bytes of device workspace cold_score needs for up to max_rows rows (ads)
+ * and max_requests requests (the batch of Section 2: the candidate ads of a
+ * request, Section 3.3: requests scored together): pooled user rows, the
+ * network input and two hidden-layer buffers.  0 if the model is NULL or a
+ * size is negative. */
 size_t cold_workspace_bytes(const cold_model *model, int64_t max_rows, int64_t max_requests);
 
 /* Register the tables and copy SE and MLP parameters into `arena` (device,
- * 256-byte aligned, >= cold_weight_arena_bytes).  Callable repeatedly (an
- * online model update); ordered on `stream`, and returns after the copies
- * have completed.  The arena must stay alive while the model scores. */
+ * 256-byte aligned, >= cold_weight_arena_bytes).  Callable repeatedly: the
+ * online model update of Section 3.4 (the model is retrained and updated
+ * continuously) swaps parameters in place; ordered on `stream`, and returns
+ * after the copies have completed.  The arena must stay alive while the
+ * model scores.  Returns COLD_ERR_INVALID_ARG for a NULL or misaligned
+ * pointer and COLD_ERR_WORKSPACE for a short arena, before any copy. */
 int cold_load_weights(cold_model *model, const cold_weights *w, void *arena,
                       size_t arena_bytes, void *stream);
 
@@ -211,7 +226,8 @@ int cold_score_noalloc(cold_model *model, const cold_batch *b, float *scores, fl
                        uint8_t *group_mask, int32_t *rows_out, void *x_out, int32_t flags,
                        void *stream);
 
-/* Stage timing, for measurement tools.  While enabled, every cold_score
+/* Stage timing: measurement only, not part of scoring (the paper defines
+ * no such call).  While enabled, every cold_score
  * call on this model records a HIP event on its stream before each kernel
  * stage and one after the last; cold_profile_read synchronises those events
  * and returns, per stage, its name and the summed elapsed milliseconds over
