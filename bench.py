@@ -215,6 +215,105 @@ def serving_curve(model, batch, cfg, streams, iters, torch, binding):
     return out
 
 
+def serving_worker(args):
+    """One serving process of the multi-process measurement: builds the
+    serving model on cuda:0, captures one 2,000-ad request's scoring call in
+    a HIP graph, prints 'ready', waits for the start file, then replays the
+    request back to back (one request in flight, host-side latency from
+    replay to stream synchronisation) for the given time and prints one JSON
+    line of latencies."""
+    import torch
+    from paper_2007_16122_amd import binding, synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.workload]
+    batch = synth.make_batch(cfg, device=dev)
+    params = synth.make_params(cfg)
+    tables = [synth.table_torch(cfg, g, device=dev) for g in range(cfg.n_groups)]
+    model = binding.ColdModel(cfg, device=dev)
+    model.load(tables, binding.params_to_device(params, cfg.dtype, dev))
+    q = args.worker_id % (len(batch["req_off"]) - 1)
+    req = binding.batch_to_device(request_slice(batch, q, cfg), dev)
+    sc = torch.empty(req["n_rows"], dtype=torch.float32, device=dev)
+    ws = model.ensure_workspace(req["n_rows"], 1)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            model.score(req, scores=sc, workspace=ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        model.score(req, scores=sc, workspace=ws)
+    lat = []
+    with torch.cuda.stream(stream):   # replays go to the current stream
+        for _ in range(20):
+            g.replay()
+        torch.cuda.synchronize()
+        print("ready", flush=True)
+        while not os.path.exists(args.start_file):
+            time.sleep(0.0005)
+        t_end = time.perf_counter() + args.duration
+        while True:
+            t0 = time.perf_counter()
+            if t0 >= t_end:
+                break
+            g.replay()
+            stream.synchronize()
+            lat.append(time.perf_counter() - t0)
+    torch.cuda.synchronize()
+    print(json.dumps({"worker": args.worker_id, "requests": len(lat), "seconds": args.duration,
+                      "lat_ms": [round(v * 1e3, 4) for v in lat]}), flush=True)
+    del g
+    model.close()
+
+
+def serving_processes(args):
+    """Concurrent serving from several processes on the one GPU (the analogue
+    of the paper's CUDA MPS setup, Section 3.3, and of its usable-QPS
+    measurement, Table 5): for each process count P, P workers each replay a
+    graph of one 2,000-ad request back to back for the same interval; the
+    aggregate request rate and the latency percentiles over all requests.
+    The coordinating process never touches the GPU."""
+    import subprocess
+    import tempfile
+    out = []
+    for n_proc in [int(v) for v in args.serving_processes.split(",") if v]:
+        start = os.path.join(tempfile.mkdtemp(prefix="cold_serve_"), "start")
+        procs = [subprocess.Popen([sys.executable, os.path.abspath(__file__), "--serving-worker",
+                                   "--worker-id", str(i), "--workload", args.workload,
+                                   "--duration", str(args.duration), "--start-file", start],
+                                  stdout=subprocess.PIPE, text=True)
+                 for i in range(n_proc)]
+        for p in procs:
+            line = p.stdout.readline().strip()
+            if line != "ready":
+                for q in procs:
+                    q.kill()
+                raise RuntimeError(f"serving worker did not start: {line!r}")
+        open(start, "w").close()
+        results = []
+        for p in procs:
+            text, _ = p.communicate(timeout=args.duration + 120)
+            if p.returncode != 0:
+                raise RuntimeError(f"serving worker failed ({p.returncode})")
+            results.append(json.loads(text.strip().splitlines()[-1]))
+        lat = np.concatenate([np.asarray(r["lat_ms"]) for r in results])
+        n_req = int(sum(r["requests"] for r in results))
+        e = {"processes": n_proc, "requests_per_s": round(n_req / args.duration, 1),
+             "ads_per_s": round(n_req * 2000 / args.duration, 1),
+             "p50_ms": round(float(np.median(lat)), 4),
+             "p99_ms": round(float(np.quantile(lat, 0.99)), 4),
+             "requests": n_req}
+        out.append(e)
+        log(f"serving {n_proc:2d} processes: {e['requests_per_s']:9.1f} req/s, p50 {e['p50_ms']:.4f} ms, "
+            f"p99 {e['p99_ms']:.4f} ms")
+    usable = {f"p99<={lim}ms": max([e["requests_per_s"] for e in out if e["p99_ms"] <= lim],
+                                   default=None) for lim in (0.1, 0.25, 0.5, 1.0)}
+    print(json.dumps({"workload": args.workload, "duration_s": args.duration,
+                      "serving_processes": out, "usable_requests_per_s": usable}), flush=True)
+
+
 def groups_sweep(base, counts, steps, warmup, torch, binding, synth, dev):
     """Throughput of lightweight models that keep K feature groups (Section
     3.2, feature group selection: the offline tests weigh a model with the
@@ -606,6 +705,14 @@ def main():
                     help="skip every measurement after the timed steps: the 2,000-ad latency, "
                          "the serving curves and the top-n selection (kernel-trace profiles of "
                          "the step only)")
+    ap.add_argument("--serving-processes", default="",
+                    help="only measure concurrent serving from this many processes (comma list), "
+                         "each replaying a 2,000-ad request back to back, and print one JSON line")
+    ap.add_argument("--duration", type=float, default=2.0,
+                    help="seconds of back-to-back requests per process count")
+    ap.add_argument("--serving-worker", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--worker-id", type=int, default=0, help=argparse.SUPPRESS)
+    ap.add_argument("--start-file", default="", help=argparse.SUPPRESS)
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -620,6 +727,12 @@ def main():
     ap.add_argument("--xcds", type=int, default=8, help="XCDs on the chip")
     ap.add_argument("--profile-command", default="", help="command recorded in summaries")
     args = ap.parse_args()
+    if args.serving_worker:
+        serving_worker(args)
+        return
+    if args.serving_processes:
+        serving_processes(args)
+        return
     if args.summarize_parity:
         for path in summarize_parity(args.summarize_parity, args.profile_command):
             print(path)
