@@ -56,6 +56,13 @@ def stage_work(cfg, batch, stage):
         # ids + gathered ad/cross rows + network input written + pooled user rows
         out = R * cfg.d_in * es if stage != "se_weights" else R * m * 4
         return "hbm", R * nax * (idb + d * es) + out + Q * nus * d * 4
+    if stage == "gather_sq":
+        # ids + gathered rows + the rows written exact (the input's place) + squeeze written
+        return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * es + R * m * 4 + Q * nus * d * 4
+    if stage == "se_rows":      # squeeze read, SE weights written
+        return "hbm", 2 * R * m * 4
+    if stage == "apply":        # rows read and written in place, SE weights read
+        return "hbm", 2 * R * cfg.d_in * es + R * m * 4
     if stage == "gather_raw":
         # ids + gathered ad/cross rows + the fp32 concatenated embedding written
         return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * 4 + Q * nus * d * 4
@@ -457,7 +464,12 @@ def _stage_of(kernel_name, dense_index):
         # full, weights, apply, raw
         mt = re.search(r"gather_se_kernelI\w*?Li(\d+)E", kernel_name)
         mode = mt.group(1) if mt else "0"
-        return {"0": "gather_se", "1": "se_weights", "2": "gather_apply", "3": "gather_raw"}.get(mode, "gather_se")
+        return {"0": "gather_se", "1": "se_weights", "2": "gather_apply", "3": "gather_raw",
+                "4": "gather_sq"}.get(mode, "gather_se")
+    if "se_rows_kernel" in kernel_name:
+        return "se_rows"
+    if "apply_weights_kernel" in kernel_name:
+        return "apply"
     if "dense_f32" in kernel_name:
         return "se_dense"
     if "dense_tail_kernel" in kernel_name:
@@ -496,6 +508,8 @@ def _label_call(call):
     for i in range(len(out) - 1):
         if out[i][0] == "gather_se" and out[i + 1][0] == "group_mask":
             out[i][0] = "se_weights"
+        if out[i][0] == "gather_se" and out[i + 1][0] == "se_rows":
+            out[i][0] = "gather_sq"
     return [tuple(x) for x in out]
 
 
@@ -506,7 +520,8 @@ def _call_starts(ours):
     out, prev = [], None
     for i, r in enumerate(ours):
         st = _stage_of(r["Kernel_Name"], 0)
-        if st == "user_pool" or (st in ("gather_se", "se_weights", "gather_raw") and prev != "user_pool"):
+        if st == "user_pool" or (st in ("gather_se", "se_weights", "gather_raw", "gather_sq")
+                                 and prev != "user_pool"):
             out.append(i)
         if st is not None:
             prev = st

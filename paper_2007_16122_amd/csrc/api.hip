@@ -20,13 +20,13 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct ArenaLayout {
-  size_t tables, rows, magic, pairs, w1, b1, w2, b2, w1t, w2t;
+  size_t tables, rows, magic, pairs, w1, b1, w2, b2, w1t, w2t, w1p, w2p;
   std::vector<size_t> w, b;
   size_t total;
 };
 
 struct WorkLayout {
-  size_t err, U, zU, Uh, urow, X, E, actA, actB, sbuf, partial, mask, total;
+  size_t err, U, zU, Uh, urow, X, E, actA, actB, sbuf, zbuf, partial, mask, total;
 };
 
 }  // namespace
@@ -76,6 +76,13 @@ int hip_fail(cold_model *m, hipError_t e, const char *what) {
   return fail(m, COLD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// The top-k mask of the squeeze SE form without sequences runs as separate
+// passes: gather with squeeze, SE of the rows, mask, reweighting in place.
+bool topk_split(const cold_model &m) {
+  // the row-wise SE kernel holds M <= 256 groups and H <= 64 hidden units
+  return m.desc.topk_k > 0 && !m.literal_se && m.desc.n_seq == 0 && m.M <= 256 && m.H <= 64;
+}
+
 ArenaLayout arena_layout(const cold_model &m) {
   ArenaLayout a;
   size_t off = 0;
@@ -99,6 +106,10 @@ ArenaLayout arena_layout(const cold_model &m) {
     a.w1t = take(sizeof(float) * m.M * m.H);   // W1 as [M][H]
     a.w2t = take(sizeof(float) * m.H * m.M);   // W2 as [H][M]
   }
+  size_t n1 = 0, n2 = 0;                        // the row-wise SE kernel's operands
+  if (topk_split(m)) se_rows_packed_floats(m.M, m.H, &n1, &n2);
+  a.w1p = take(sizeof(float) * n1);
+  a.w2p = take(sizeof(float) * n2);
   const int L = m.desc.n_layers;
   for (int l = 0; l < L; ++l) {
     a.w.push_back(take((size_t)m.es * m.widths[l] * m.widths[l + 1]));
@@ -124,6 +135,7 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   w.actA = take((size_t)m.es * R * m.max_hidden);
   w.actB = take((size_t)m.es * R * m.max_hidden);
   w.sbuf = take(sbuf ? sizeof(float) * (size_t)R * m.M : 0);
+  w.zbuf = take(topk_split(m) ? sizeof(float) * (size_t)R * m.M : 0);
   w.partial = take(topk ? sizeof(float) * (size_t)Q * kMaskParts * m.M : 0);
   w.mask = take(topk ? (size_t)Q * m.M : 0);
   w.total = off;
@@ -363,6 +375,13 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
                                reinterpret_cast<float *>(A + al.w2t), m->M, m->H, s);
     if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: transpose");
   }
+  if (topk_split(*m)) {
+    hipError_t e = launch_pack_se_rows(reinterpret_cast<const float *>(A + al.w1),
+                                       reinterpret_cast<const float *>(A + al.w2), m->M, m->H,
+                                       reinterpret_cast<float *>(A + al.w1p),
+                                       reinterpret_cast<float *>(A + al.w2p), s);
+    if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: SE pack");
+  }
   for (int l = 0; l < L; ++l)
     if (packed(l)) {
       hipError_t e = launch_pack_frag(w->mlp_w[l], A + al.w[l], m->widths[l + 1], m->widths[l], s);
@@ -483,6 +502,29 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     if ((e = marks.mark("gather_se")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se launch");
+  } else if (topk_split(*m)) {
+    // gather with squeeze (rows kept exact in the input's place), SE of the
+    // rows on the matrix cores, the per-request mask, reweighting in place
+    float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
+    uint8_t *mask = W + wl.mask;
+    g.s_buf = nullptr;
+    g.z_out = reinterpret_cast<float *>(W + wl.zbuf);
+    if ((e = marks.mark("gather_sq")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_gather_se(m->dtype, kSqueezeRaw, false, m->hashed, g, s)) != hipSuccess)
+      return hip_fail(m, e, "gather_se (squeeze) launch");
+    if ((e = marks.mark("se_rows")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_se_rows(g.z_out, sb, R, m->M, m->H, reinterpret_cast<const float *>(A + al.w1p), g.b1,
+                              reinterpret_cast<const float *>(A + al.w2p), g.b2, s)) != hipSuccess)
+      return hip_fail(m, e, "se_rows launch");
+    if ((e = marks.mark("group_mask")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_group_mask(sb, b->req_off, Q, R, m->M, D.topk_k,
+                               reinterpret_cast<float *>(W + wl.partial), kMaskParts, mask,
+                               group_mask, s)) != hipSuccess)
+      return hip_fail(m, e, "group_mask launch");
+    if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
+    if ((e = launch_apply_weights(m->dtype, D.linear_log, W + wl.X, sb, mask, b->req_off, Q, R, m->M,
+                                  m->d, s)) != hipSuccess)
+      return hip_fail(m, e, "apply launch");
   } else {
     float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
     uint8_t *mask = W + wl.mask;

@@ -180,6 +180,7 @@ struct GatherArgs {
   int32_t *urow;                  // [Q][max(n_user,1)] resolved user rows
   void *X;                        // [R][M*d] network input
   float *s_buf;                   // [R][M] SE weights (written, or read in apply mode)
+  float *z_out;                   // [R][M] squeeze (kSqueezeRaw)
   const uint8_t *mask;            // [Q][M] kept groups (apply mode)
   int32_t *rows_out;              // [M][R] or null
   int32_t *err;                   // error bits
@@ -189,7 +190,9 @@ struct GatherArgs {
 // kApplyWeights: reweight with s_buf (groups outside `mask`, when given,
 // read nothing and get weight 0); kRawOut: the concatenated embedding in
 // fp32 to X, for an SE computed elsewhere
-enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3 };
+// kSqueezeRaw: the squeeze to z_out [R][M] and the gathered rows, exact in the
+// storage type, to X, for se_rows and apply_weights (models without sequences)
+enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3, kSqueezeRaw = 4 };
 
 // launchers (return hipError_t of the launch)
 bool user_pool_needed(int dtype, const GatherArgs &a);
@@ -200,6 +203,25 @@ hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t
                              int32_t M, int32_t k, float *partial, int32_t n_parts,
                              uint8_t *mask, uint8_t *mask_out, hipStream_t s);
 hipError_t launch_clear_flag(int32_t *err, hipStream_t s);
+// compute units of the current device (cached per device; 0 on error)
+int device_cus();
+// SE weights of every row from its squeeze (Eq. 2 read as squeeze ->
+// FC -> ReLU -> FC -> sigmoid): s [R][M] from z [R][M] on the fp32 matrix
+// cores, with W1 and W2 packed by launch_pack_se_rows; M <= 256, H <= 64
+hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, int32_t H,
+                          const float *w1p, const float *b1, const float *w2p, const float *b2,
+                          hipStream_t s);
+// floats of the two packed SE operands (0 when M or H is beyond the kernel)
+void se_rows_packed_floats(int32_t M, int32_t H, size_t *n1, size_t *n2);
+// W1 [H][M] and W2 [M][H] into the row-wise SE kernel's operand order
+hipError_t launch_pack_se_rows(const float *w1, const float *w2, int32_t M, int32_t H, float *w1p,
+                               float *w2p, hipStream_t s);
+// X [R][M*d] in place: the gathered rows (storage type) times s [R][M] and
+// the request's group mask [Q][M] (NULL: all kept), linear_log when ll,
+// rounded once to the storage type
+hipError_t launch_apply_weights(int dtype, bool ll, void *X, const float *s_buf,
+                                const uint8_t *mask, const int32_t *req_off, int64_t Q, int64_t R,
+                                int32_t M, int32_t d, hipStream_t s);
 // dst[c][r] = src[r][c] for a [rows][cols] fp32 matrix
 hipError_t launch_transpose_f32(const float *src, float *dst, int32_t rows, int32_t cols,
                                 hipStream_t s);

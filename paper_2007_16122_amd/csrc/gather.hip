@@ -21,6 +21,7 @@
 //              selection); ties go to the lower group index.
 #include <mutex>
 #include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "cold_internal.h"
@@ -345,7 +346,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     reinterpret_cast<float4 *>(ust)[i] =
         reinterpret_cast<const float4 *>(a.U + ((int64_t)rq[t] * nus + nu) * d)[k4];
   }
-  if constexpr (MODE == kFull || MODE == kWeightsOnly) {   // squeeze of the pooled sequences
+  if constexpr (MODE == kFull || MODE == kWeightsOnly || MODE == kSqueezeRaw) {   // squeeze of the pooled sequences
     for (int i = ln; i < Tw * ns; i += 64) {
       const int t = fast_div(i, a.mg_ns), g = nu + (i - t * ns);
       z[t * Mp + g] = r0 + t < R ? a.zU[(int64_t)rq[t] * nus + g] : 0.0f;
@@ -391,7 +392,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       advance(t, c);
     }
   }
-  if constexpr (MODE == kFull || MODE == kWeightsOnly) {
+  if constexpr (MODE == kFull || MODE == kWeightsOnly || MODE == kSqueezeRaw) {
     int t = tf, c = cf;
     asm volatile("" : "+v"(t), "+v"(c));   // recomputed per phase, not kept live
 #pragma unroll
@@ -414,6 +415,22 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
     }
     wave_sync();
 
+    if constexpr (MODE == kSqueezeRaw) {
+      // the squeeze [R][M] and the gathered rows, exact in the storage type,
+      // into the network input's place, for the separate SE and apply passes
+      for (int it = ln; it < Tw * M; it += 64) {
+        const int t = fast_div(it, a.mg_m), g = it - t * M;
+        if (r0 + t < R) a.z_out[r0 * M + it] = z[t * Mp + g];
+      }
+      TS *X = static_cast<TS *>(a.X);
+      int t = tf, c = cf;
+      asm volatile("" : "+v"(t), "+v"(c));
+#pragma unroll
+      for (int j = 0; j < CPT; ++j, advance(t, c)) {
+        const int i = ln + 64 * j;
+        if (t < tv) *reinterpret_cast<uint4 *>(X + (r0 * CPR + i) * EPC) = raw[j];
+      }
+    } else {
     // ---- SE block of the wave's rows (Eq. 2)
     // sums from the bias in index order; from LDS, weight and input rows are
     // read four at a time (rows padded to Mp / Hp); from global memory, the
@@ -472,6 +489,7 @@ __global__ __launch_bounds__(kGatherThreads, CPT <= 8 ? 4 : 2) void gather_se_ke
       sv[it] = sg;
       if (a.s_buf && r0 + t < R) a.s_buf[r0 * M + it] = sg;
     }
+    }   // SE block
   } else if constexpr (MODE == kApplyWeights) {
     for (int it = ln; it < Tw * M; it += 64) {
       const int t = fast_div(it, a.mg_m), g = it - t * M;
@@ -629,6 +647,21 @@ hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStre
   }
 }
 
+// CUs of the current device (cached per device)
+int device_cus() {
+  static std::mutex mu;
+  static std::vector<std::pair<int, int>> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const auto &e : cache)
+    if (e.first == dev) return e.second;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  cache.emplace_back(dev, cus);
+  return cus;
+}
+
 // Resident workgroups of a kernel on the current device (cached): the
 // persistent gather launches no more than fit at once.
 static int resident_blocks(const void *kernel, size_t shmem) {
@@ -717,6 +750,10 @@ static hipError_t gather_se_t(bool hashed, const GatherArgs &a, hipStream_t s) {
 template <typename TS>
 static hipError_t gather_se_dt(int mode, bool ll, bool hashed, const GatherArgs &a, hipStream_t s) {
   if (mode == kWeightsOnly) return gather_se_t<TS, kWeightsOnly, false>(hashed, a, s);
+  if (mode == kSqueezeRaw) {
+    if (a.n_seq > 0 || !a.z_out) return hipErrorInvalidValue;   // pooled sums are not exact in TS
+    return gather_se_t<TS, kSqueezeRaw, false>(hashed, a, s);
+  }
   if (mode == kRawOut) return gather_se_t<TS, kRawOut, false>(hashed, a, s);
   if (mode == kApplyWeights)
     return ll ? gather_se_t<TS, kApplyWeights, true>(hashed, a, s)
@@ -765,6 +802,282 @@ hipError_t launch_transpose_f32(const float *src, float *dst, int32_t rows, int3
   hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
                      dst, rows, cols);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------- se_rows
+// SE weights of rows from their squeeze (Eq. 2 read as squeeze -> FC ->
+// ReLU -> FC -> sigmoid), for models whose SE parameters do not fit the
+// gather's LDS budget, on the fp32 matrix cores.  A workgroup takes 16 rows
+// at a time and forms both layers transposed,
+//   h^T [H x 16] = ReLU(W1 [H x M] z^T [M x 16] + b1),
+//   s^T [M x 16] = sigmoid(W2 [M x H] h^T [H x 16] + b2),
+// as 16x16x4 fp32 MFMAs, so that layer 1's output fragments are layer 2's B
+// operand without a transpose.  Wave w owns hidden units 16w .. 16w + 15 in
+// layer 1 and output blocks w, w + 4, ... in layer 2; lane l (row or unit
+// l % 16, quarter q = l / 16) feeds K index q * MQ + t at step t of layer 1
+// and hidden unit 4 t + q at step t of layer 2.  Both weight matrices are
+// packed once at load time in that operand order (one 16-byte vector per lane
+// and 4 steps, zero past M and H), held in registers for all of the
+// workgroup's rows; the rows' squeeze is staged in LDS with coalesced loads.
+// Products and sums are fp32; the sums run in the matrix cores' order
+// instead of index order, which only moves fp32 rounding.
+constexpr int kSeTile = 16;
+constexpr int kSeMaxH = 64;     // four 16-wide hidden blocks, one per wave
+constexpr int kSeMaxGB = 16;    // M <= 256: 16-wide output blocks, four per wave
+
+__host__ __device__ static int se_rows_mq(int M) { return ((M + 3) / 4 + 3) & ~3; }   // K run of a quarter, % 4 == 0
+static int se_rows_nc(int M) {                                    // 4-step chunks the kernel holds
+  const int mq = se_rows_mq(M);
+  return mq <= 16 ? 4 : mq <= 32 ? 8 : 16;
+}
+
+void se_rows_packed_floats(int32_t M, int32_t H, size_t *n1, size_t *n2) {
+  const bool ok = M > 0 && M <= 256 && H > 0 && H <= kSeMaxH;
+  *n1 = ok ? (size_t)(kSeMaxH / 16) * se_rows_nc(M) * 256 : 0;
+  *n2 = ok ? (size_t)((M + 15) / 16) * 4 * 256 : 0;
+}
+
+// one thread per packed word: W1p [4 hidden blocks][NC chunks][64 lanes][4],
+// then W2p [output blocks][4 chunks][64 lanes][4]
+__global__ __launch_bounds__(256) void pack_se_rows_kernel(const float *__restrict__ w1,
+                                                           const float *__restrict__ w2, int M,
+                                                           int H, int MQ, int NC,
+                                                           float *__restrict__ w1p,
+                                                           float *__restrict__ w2p, int64_t n1,
+                                                           int64_t n2) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int e = (int)(i & 3), lane = (int)((i >> 2) & 63), c = lane & 15, q = lane >> 4;
+  if (i < n1) {
+    const int u = (int)((i >> 8) % NC), b = (int)((i >> 8) / NC);
+    const int j = 16 * b + c, k = 4 * u + e, g = q * MQ + k;
+    w1p[i] = j < H && k < MQ && g < M ? w1[(int64_t)j * M + g] : 0.0f;
+  } else if (i < n1 + n2) {
+    const int64_t i2 = i - n1;
+    const int v = (int)((i2 >> 8) & 3), gb = (int)(i2 >> 10);
+    const int g = 16 * gb + c, jj = 4 * (4 * v + e) + q;
+    w2p[i2] = g < M && jj < H ? w2[(int64_t)g * H + jj] : 0.0f;
+  }
+}
+
+hipError_t launch_pack_se_rows(const float *w1, const float *w2, int32_t M, int32_t H, float *w1p,
+                               float *w2p, hipStream_t s) {
+  size_t n1, n2;
+  se_rows_packed_floats(M, H, &n1, &n2);
+  if (n1 == 0) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)(n1 + n2);
+  hipLaunchKernelGGL(pack_se_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, w1, w2,
+                     M, H, se_rows_mq(M), se_rows_nc(M), w1p, w2p, (int64_t)n1, (int64_t)n2);
+  return hipGetLastError();
+}
+
+template <int NC>
+__global__ __launch_bounds__(256) void se_rows_kernel(const float *__restrict__ z,
+                                                      float *__restrict__ s_out, int64_t R, int M,
+                                                      int H, const float4 *__restrict__ w1p,
+                                                      const float *__restrict__ b1,
+                                                      const float4 *__restrict__ w2p,
+                                                      const float *__restrict__ b2) {
+  constexpr int kMaxStride = 16 * NC + 4;
+  __shared__ __align__(16) float zs[kSeTile * kMaxStride];   // row c at c * ZST
+  __shared__ float hs[kSeMaxH * kSeTile];                     // h^T: unit j, row c at j * 16 + c
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int MQ = se_rows_mq(M), MP = 4 * MQ;   // padded row: zeros from M to MP
+  const int ZST = MP + 4;                      // an odd number of 16-byte slots: no bank conflicts
+  const int GB = (M + 15) >> 4;
+  float4 wa[NC], wb[kSeMaxGB / 4][4];
+#pragma unroll
+  for (int u = 0; u < NC; ++u) wa[u] = w1p[(wave * NC + u) * 64 + lane];
+#pragma unroll
+  for (int i = 0; i < kSeMaxGB / 4; ++i) {
+    const int gb = wave + 4 * i;
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      wb[i][v] = gb < GB ? w2p[(gb * 4 + v) * 64 + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float bias1[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int jj = wave * 16 + 4 * q + e;
+    bias1[e] = jj < H ? b1[jj] : 0.0f;
+  }
+  for (int64_t r0 = (int64_t)blockIdx.x * kSeTile; r0 < R; r0 += (int64_t)gridDim.x * kSeTile) {
+    // the tile's squeeze rows (contiguous in z) into LDS; rows past R and
+    // columns past M are zeros
+    {
+      const int rows = R - r0 < kSeTile ? (int)(R - r0) : kSeTile;
+      const float *zt = z + r0 * M;
+      float v[kSeTile];
+#pragma unroll
+      for (int cc = 0; cc < kSeTile; ++cc)
+        v[cc] = tid < M && cc < rows ? zt[cc * M + tid] : 0.0f;
+#pragma unroll
+      for (int cc = 0; cc < kSeTile; ++cc)
+        if (tid < MP) zs[cc * ZST + tid] = v[cc];
+    }
+    __syncthreads();
+    // layer 1
+    f32x4 acc;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = bias1[e];
+    const float *zrow = zs + c * ZST + q * MQ;
+#pragma unroll
+    for (int u = 0; u < NC; ++u) {
+      if (4 * u < MQ) {
+        const float4 zv = *reinterpret_cast<const float4 *>(zrow + 4 * u);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u].x, zv.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u].y, zv.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u].z, zv.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[u].w, zv.w, acc, 0, 0, 0);
+      }
+    }
+    // lane holds h[row r0 + c][unit wave * 16 + 4 q + e]; padded units are 0
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      hs[(wave * 16 + 4 * q + e) * kSeTile + c] = acc[e] > 0.0f ? acc[e] : 0.0f;
+    __syncthreads();
+    // layer 2
+    float hb[kSeMaxH / 4];
+#pragma unroll
+    for (int t = 0; t < kSeMaxH / 4; ++t) hb[t] = hs[(4 * t + q) * kSeTile + c];
+    const int64_t row = r0 + c;
+#pragma unroll
+    for (int i = 0; i < kSeMaxGB / 4; ++i) {
+      const int gb = wave + 4 * i;
+      if (gb < GB) {
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int gg = gb * 16 + 4 * q + e;
+          o[e] = gg < M ? b2[gg] : 0.0f;
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          o = __builtin_amdgcn_mfma_f32_16x16x4f32(wb[i][v].x, hb[4 * v], o, 0, 0, 0);
+          o = __builtin_amdgcn_mfma_f32_16x16x4f32(wb[i][v].y, hb[4 * v + 1], o, 0, 0, 0);
+          o = __builtin_amdgcn_mfma_f32_16x16x4f32(wb[i][v].z, hb[4 * v + 2], o, 0, 0, 0);
+          o = __builtin_amdgcn_mfma_f32_16x16x4f32(wb[i][v].w, hb[4 * v + 3], o, 0, 0, 0);
+        }
+        // lane holds s[row r0 + c][group gb * 16 + 4 q + e]
+        if (row < R) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int gg = gb * 16 + 4 * q + e;
+            if (gg < M) s_out[row * M + gg] = 1.0f / (1.0f + expf(-o[e]));
+          }
+        }
+      }
+    }
+    // the next tile's staging writes only zs, which no wave reads after its
+    // layer 1; hs is written again only after the next barrier
+  }
+}
+
+hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, int32_t H,
+                          const float *w1p, const float *b1, const float *w2p, const float *b2,
+                          hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (M <= 0 || M > 256 || H <= 0 || H > kSeMaxH) return hipErrorInvalidValue;
+  if ((reinterpret_cast<uintptr_t>(w1p) | reinterpret_cast<uintptr_t>(w2p)) & 15)
+    return hipErrorInvalidValue;
+  const int cus = device_cus();
+  if (cus <= 0) return hipErrorInvalidValue;
+  const int64_t tiles = (R + kSeTile - 1) / kSeTile;
+  const unsigned grid = (unsigned)(tiles < 2 * cus ? tiles : 2 * cus);
+  const float4 *a1 = reinterpret_cast<const float4 *>(w1p);
+  const float4 *a2 = reinterpret_cast<const float4 *>(w2p);
+  switch (se_rows_nc(M)) {
+    case 4: hipLaunchKernelGGL(se_rows_kernel<4>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2); break;
+    case 8: hipLaunchKernelGGL(se_rows_kernel<8>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2); break;
+    default: hipLaunchKernelGGL(se_rows_kernel<16>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2);
+  }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- apply_weights
+// The network input in place from the gathered rows: each 16-byte chunk of
+// row r, group g becomes round(LL(s[r][g] e)) for a group the request keeps
+// and 0 for one its mask drops (Section 3.2 reweighting, Eq. 3 when LL).
+// A workgroup takes kApplyRows rows and finds their requests once, in LDS;
+// each thread loads all of its chunks and weights before it computes.
+constexpr int kApplyRows = 2;
+constexpr int kApplyPerThread = 4;
+template <typename TS, bool LL>
+__global__ __launch_bounds__(256) void apply_weights_kernel(TS *__restrict__ X,
+                                                            const float *__restrict__ s_buf,
+                                                            const uint8_t *__restrict__ mask,
+                                                            const int32_t *__restrict__ req_off,
+                                                            int64_t Q, int64_t R, int M, int lcpg,
+                                                            int CPR, uint32_t mg_cpr) {
+  constexpr int EPC = Elem<TS>::kPerChunk;
+  __shared__ int32_t s_rq[kApplyRows];
+  const int64_t r0 = (int64_t)blockIdx.x * kApplyRows;
+  const int rows = R - r0 < kApplyRows ? (int)(R - r0) : kApplyRows;
+  if (threadIdx.x < rows) s_rq[threadIdx.x] = (int32_t)request_of_row(req_off, Q, r0 + threadIdx.x);
+  __syncthreads();
+  uint4 *xc = reinterpret_cast<uint4 *>(X) + r0 * CPR;
+  const int n = rows * CPR;
+  for (int base = 0; base < n; base += 256 * kApplyPerThread) {
+    uint4 raw[kApplyPerThread];
+    float sg[kApplyPerThread];
+    bool keep[kApplyPerThread];
+#pragma unroll
+    for (int u = 0; u < kApplyPerThread; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      raw[u] = make_uint4(0, 0, 0, 0);
+      sg[u] = 0.0f;
+      keep[u] = false;
+      if (idx < n) {
+        const int t = fast_div(idx, mg_cpr), g = (idx - t * CPR) >> lcpg;
+        raw[u] = xc[idx];
+        sg[u] = s_buf[(r0 + t) * M + g];
+        keep[u] = !mask || mask[(int64_t)s_rq[t] * M + g] != 0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyPerThread; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      if (idx < n) {
+        float v[EPC], o[EPC];
+        Elem<TS>::unpack(raw[u], v);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+          const float x = sg[u] * v[e];
+          o[e] = keep[u] ? (LL ? linear_log(x) : x) : 0.0f;
+        }
+        xc[idx] = Elem<TS>::pack(o);
+      }
+    }
+  }
+}
+
+template <typename TS>
+static hipError_t apply_t(bool ll, void *X, const float *s_buf, const uint8_t *mask,
+                          const int32_t *req_off, int64_t Q, int64_t R, int32_t M, int32_t d,
+                          hipStream_t s) {
+  constexpr int EPC = Elem<TS>::kPerChunk;
+  const int cpg = d / EPC, cpr = M * cpg;
+  if (cpg <= 0 || (cpg & (cpg - 1)) || kApplyRows * (int64_t)cpr >= (1 << 16)) return hipErrorInvalidValue;
+  const int lcpg = __builtin_ctz(cpg);
+  const dim3 grid((unsigned)((R + kApplyRows - 1) / kApplyRows));
+  if (ll)
+    hipLaunchKernelGGL((apply_weights_kernel<TS, true>), grid, dim3(256), 0, s, static_cast<TS *>(X),
+                       s_buf, mask, req_off, Q, R, M, lcpg, cpr, div_magic((uint32_t)cpr));
+  else
+    hipLaunchKernelGGL((apply_weights_kernel<TS, false>), grid, dim3(256), 0, s, static_cast<TS *>(X),
+                       s_buf, mask, req_off, Q, R, M, lcpg, cpr, div_magic((uint32_t)cpr));
+  return hipGetLastError();
+}
+
+hipError_t launch_apply_weights(int dtype, bool ll, void *X, const float *s_buf,
+                                const uint8_t *mask, const int32_t *req_off, int64_t Q, int64_t R,
+                                int32_t M, int32_t d, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  switch (dtype) {
+    case kF32: return apply_t<float>(ll, X, s_buf, mask, req_off, Q, R, M, d, s);
+    case kBF16: return apply_t<__bf16>(ll, X, s_buf, mask, req_off, Q, R, M, d, s);
+    default: return apply_t<_Float16>(ll, X, s_buf, mask, req_off, Q, R, M, d, s);
+  }
 }
 
 hipError_t launch_clear_flag(int32_t *err, hipStream_t s) {

@@ -1045,11 +1045,34 @@ static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, vo
     // barrier per 64 MFMAs per wave, whole 128-byte rows per load) when K
     // allows (256 x 128 or 256 x 64 over 4 waves for narrower layers);
     // batches of a few thousand ads would leave most CUs idle with those,
-    // so 128 x 128 tiles while they still number at least one per CU, else
-    // 64 x 64
+    // so 128..192 x 128 tiles while 128-row tiles would still number one
+    // per CU, else 64 x 64.
+    // Every tile shape sums the same 32-deep K blocks in the same order, so
+    // the outputs do not depend on the shape.
     const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
     const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
     const bool k64 = K % 64 == 0;
+    if (big_tiles < 256 && mid_tiles >= 256 && k64 && N % 128 == 0) {
+      // x 128 tiles with the row height that gives the least work to the
+      // busiest CU (rounds of one tile per CU), provided the tiles still
+      // cover three quarters of the CUs (fewer, smaller layers run faster
+      // on 64 x 64 tiles, two per CU)
+      const int64_t cus = device_cus() > 0 ? device_cus() : 256;
+      const int heights[3] = {192, 160, 128};
+      int best = 0;
+      int64_t best_cost = -1;
+      for (int h : heights) {
+        const int64_t tiles = ((R + h - 1) / h) * (N / 128);
+        const int64_t cost = (tiles + cus - 1) / cus * h;
+        if (4 * tiles >= 3 * cus && (best_cost < 0 || cost < best_cost)) best = h, best_cost = cost;
+      }
+      switch (best) {
+        case 192: return dense_buf_t<TS, 192, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
+        case 160: return dense_buf_t<TS, 160, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
+        case 128: return dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
+        default: break;
+      }
+    }
     if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
       return k64 ? dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
                  : dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);

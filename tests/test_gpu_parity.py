@@ -332,6 +332,30 @@ def test_parity_odd_input_width(name):
     compare_scores(cfg, g["scores"], o["scores"], f"odd input width {name}")
 
 
+@pytest.mark.parametrize("fields,k", [((3, 5, 3), 5), ((16, 32, 16), 20), ((25, 50, 25), 41),
+                                      ((13, 25, 13), 30), ((64, 128, 64), 100)])
+def test_parity_topk_group_counts(fields, k):
+    """The top-k path's row-wise SE at other group counts M (and H = M / 4):
+    11 and 51 groups (M not a multiple of 4: word loads), 64 and 100 groups
+    (16-byte loads over 4 and 8 chunks of the K run) and 256 groups (16
+    chunks; the largest M of that path, 64 hidden units); SE weights, mask
+    and scores of every row against the checker."""
+    n_user, n_ad, n_cross = fields
+    cfg = mid("wide_prune_bf16", n_user=n_user, n_ad=n_ad, n_cross=n_cross, topk_k=k)
+    log(f"test_parity_topk_group_counts M={cfg.n_groups} H={cfg.se_hidden} k={k}")
+    tables, params, batch = problem(cfg, seed=41, cand=[333, 0, 150], model_seed=cfg.seed)
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True, want_s=True, want_mask=True)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_s=True, want_z=True)
+    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
+    assert_se_weights_close(params, g["s"], o)
+    check_mask(cfg, o, g, batch)
+    compare_scores(cfg, g["scores"], o["scores"], f"top-k M={cfg.n_groups}")
+
+
 @pytest.mark.parametrize("widths,n_req", [((768, 384, 320, 256, 128, 64, 2), 12),
                                           ((768, 1024, 512, 256, 128, 64, 2), 3),
                                           ((768, 1024, 544, 256, 128, 64, 2), 3),
