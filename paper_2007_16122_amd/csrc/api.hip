@@ -20,7 +20,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct ArenaLayout {
-  size_t tables, rows, magic, pairs, w1, b1, w2, b2, w1t, w2t, w1p, w2p;
+  size_t tables, rows, magic, pairs, w1, b1, w2, b2, w1t, w2t, w1p, w2p, w1f, w2f;
   std::vector<size_t> w, b;
   size_t total;
 };
@@ -78,6 +78,11 @@ int hip_fail(cold_model *m, hipError_t e, const char *what) {
 
 // The top-k mask of the squeeze SE form without sequences runs as separate
 // passes: gather with squeeze, SE of the rows, mask, reweighting in place.
+// SE operands of the register-resident gather (squeeze form; its shape limits)
+bool full_gather_model(const cold_model &m) {
+  return !m.literal_se && gather_full_shape(m.M, m.H, m.d * m.es, m.desc.n_seq);
+}
+
 bool topk_split(const cold_model &m) {
   // the row-wise SE kernel holds M <= 256 groups and H <= 64 hidden units
   return m.desc.topk_k > 0 && !m.literal_se && m.desc.n_seq == 0 && m.M <= 256 && m.H <= 64;
@@ -110,6 +115,8 @@ ArenaLayout arena_layout(const cold_model &m) {
   if (topk_split(m)) se_rows_packed_floats(m.M, m.H, &n1, &n2);
   a.w1p = take(sizeof(float) * n1);
   a.w2p = take(sizeof(float) * n2);
+  a.w1f = take(full_gather_model(m) ? sizeof(float) * kSeFullFloats : 0);
+  a.w2f = take(full_gather_model(m) ? sizeof(float) * kSeFullFloats : 0);
   const int L = m.desc.n_layers;
   for (int l = 0; l < L; ++l) {
     a.w.push_back(take((size_t)m.es * m.widths[l] * m.widths[l + 1]));
@@ -382,6 +389,13 @@ int cold_load_weights(cold_model *m, const cold_weights *w, void *arena, size_t 
                                        reinterpret_cast<float *>(A + al.w2p), s);
     if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: SE pack");
   }
+  if (full_gather_model(*m)) {
+    hipError_t e = launch_pack_se_full(reinterpret_cast<const float *>(A + al.w1),
+                                       reinterpret_cast<const float *>(A + al.w2), m->M, m->H,
+                                       reinterpret_cast<float *>(A + al.w1f),
+                                       reinterpret_cast<float *>(A + al.w2f), s);
+    if (e != hipSuccess) return hip_fail(m, e, "cold_load_weights: SE pack");
+  }
   for (int l = 0; l < L; ++l)
     if (packed(l)) {
       hipError_t e = launch_pack_frag(w->mlp_w[l], A + al.w[l], m->widths[l + 1], m->widths[l], s);
@@ -450,6 +464,8 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
   g.b2 = reinterpret_cast<const float *>(A + al.b2);
   g.w1t = reinterpret_cast<const float *>(A + al.w1t);
   g.w2t = reinterpret_cast<const float *>(A + al.w2t);
+  g.w1f = full_gather_model(*m) ? reinterpret_cast<const float *>(A + al.w1f) : nullptr;
+  g.w2f = full_gather_model(*m) ? reinterpret_cast<const float *>(A + al.w2f) : nullptr;
   g.U = reinterpret_cast<float *>(W + wl.U);
   g.zU = reinterpret_cast<float *>(W + wl.zU);
   g.Uh = W + wl.Uh;
@@ -464,9 +480,12 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
   static const char *kDenseNames[] = {"dense0", "dense1", "dense2", "dense3", "dense4", "dense5",
                                       "dense6", "dense7", "dense8", "dense9", "dense10", "dense11"};
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
-  if (user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
+  // the one-pass SE (no top-k) of small models runs on the register-resident
+  // gather, which reads the users' rows from the pooling pass
+  const bool full = !m->literal_se && !topk && gather_full_supported(m->dtype, g);
+  if (full || user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
     if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
-    if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
+    if ((e = launch_user_pool(m->dtype, m->hashed, g, s, full)) != hipSuccess)
       return hip_fail(m, e, "user_pool launch");
   }
   if (m->literal_se) {
@@ -500,8 +519,9 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
   } else if (!topk) {
     g.s_buf = importance;
     if ((e = marks.mark("gather_se")) != hipSuccess) return hip_fail(m, e, "profile event");
-    if ((e = launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s)) != hipSuccess)
-      return hip_fail(m, e, "gather_se launch");
+    e = full ? launch_gather_full(m->dtype, D.linear_log, m->hashed, g, s)
+             : launch_gather_se(m->dtype, kFull, D.linear_log, m->hashed, g, s);
+    if (e != hipSuccess) return hip_fail(m, e, "gather_se launch");
   } else if (topk_split(*m)) {
     // gather with squeeze (rows kept exact in the input's place), SE of the
     // rows on the matrix cores, the per-request mask, reweighting in place

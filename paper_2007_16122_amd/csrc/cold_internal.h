@@ -174,6 +174,7 @@ struct GatherArgs {
   const int32_t *cross_pairs;     // device [n_cross][2] (user field, ad field) or null
   const float *w1, *b1, *w2, *b2; // SE parameters
   const float *w1t, *w2t;         // W1 as [M][H], W2 as [H][M] (read when they are not in LDS)
+  const float *w1f, *w2f;         // W1, W2 in gather_full's operand order, or null
   float *U;                       // [Q][n_user+n_seq][d] pooled user side
   float *zU;                      // [Q][n_user+n_seq] squeeze of the user groups
   void *Uh;                       // [Q][n_user][d] single-valued user rows, storage type
@@ -196,7 +197,19 @@ enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3, k
 
 // launchers (return hipError_t of the launch)
 bool user_pool_needed(int dtype, const GatherArgs &a);
-hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s);
+// the per-request pooling pass; `force` runs it even where the gather could
+// stage the users' rows itself
+hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s,
+                            bool force = false);
+// the register-resident kFull gather (M <= 48, H <= 16, 32-byte group rows,
+// no sequences; needs the pooling pass and the packed SE operands)
+constexpr int kSeFullFloats = 4 * 64 * 4;   // floats of each packed operand
+bool gather_full_shape(int32_t M, int32_t H, int32_t row_bytes, int32_t n_seq);
+bool gather_full_supported(int dtype, const GatherArgs &a);
+hipError_t launch_gather_full(int dtype, bool linear_log, bool hashed, const GatherArgs &a,
+                              hipStream_t s);
+hipError_t launch_pack_se_full(const float *w1, const float *w2, int32_t M, int32_t H, float *w1f,
+                               float *w2f, hipStream_t s);
 hipError_t launch_gather_se(int dtype, int mode, bool linear_log, bool hashed,
                             const GatherArgs &a, hipStream_t s);
 hipError_t launch_group_mask(const float *s_buf, const int32_t *req_off, int64_t Q, int64_t R,

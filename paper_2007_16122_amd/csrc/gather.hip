@@ -638,8 +638,8 @@ bool user_pool_needed(int dtype, const GatherArgs &a) {
   return (int64_t)a.n_user * a.Q * a.d * es > kGatherMaxUserValLds;
 }
 
-hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s) {
-  if (a.Q <= 0 || !user_pool_needed(dtype, a)) return hipSuccess;
+hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s, bool force) {
+  if (a.Q <= 0 || !(force || user_pool_needed(dtype, a))) return hipSuccess;
   switch (dtype) {
     case kF32: return user_pool_t<float>(hashed, a, s);
     case kBF16: return user_pool_t<__bf16>(hashed, a, s);
@@ -680,6 +680,289 @@ static int resident_blocks(const void *kernel, size_t shmem) {
   const int blocks = per_cu * cus;
   cache.push_back({kernel, shmem, dev, blocks});
   return blocks;
+}
+
+// ------------------------------------------------------------- gather_full
+// Gather, squeeze, SE and reweighting of a row tile in registers (Section
+// 3.2: Eq. 2 read as squeeze -> FC -> ReLU -> FC -> sigmoid, Eq. 3 when LL),
+// for models with at most 48 groups, at most 16 hidden SE units, 32-byte
+// group rows and no sequence groups.  A wave takes 16 rows; lane l = 16 q + c
+// owns row c of the tile and the groups g = 4 k + q of its slots k: it loads
+// their ids and both 16-byte chunks of each group row itself, so a group's
+// squeeze is a sum inside one lane, and the lanes' squeeze values are already
+// the B operand of a 16x16x4 fp32 MFMA whose K index is g = 4 k + q at step
+// k.  Layer 1 is one 16-unit hidden block (h^T = W1 z^T, units 4 q + e in
+// lane (c, q)), which is layer 2's B operand as it stands; layer 2 forms its
+// output rows in the order g = 16 gb + 4 e + q (row 4 q + e of block gb), so
+// the weight of slot k = 4 gb + e lands in the lane that holds the group.
+// Both SE matrices are packed in that operand order at load time and held in
+// registers.  The users' rows come from the pooling pass (storage type, one
+// per request).  Products and sums are fp32; the squeeze and the SE sums run
+// in another order than index order, which only moves fp32 rounding, and
+// each row's result does not depend on the other rows of its tile.
+constexpr int kFullMaxM = 48;
+constexpr int kFullMaxH = 16;
+
+bool gather_full_shape(int32_t M, int32_t H, int32_t row_bytes, int32_t n_seq) {
+  return n_seq == 0 && M > 0 && M <= kFullMaxM && H > 0 && H <= kFullMaxH && row_bytes == 32;
+}
+
+bool gather_full_supported(int dtype, const GatherArgs &a) {
+  const int es = dtype == kF32 ? 4 : 2;
+  return gather_full_shape(a.M, a.H, a.d * es, a.n_seq) && a.w1f != nullptr && a.w2f != nullptr;
+}
+
+// W1f [4][64 lanes][4]: element e of vector (u, lane) is W1[c][4 (4 u + e) + q];
+// W2f [4][64 lanes][4]: element e of vector (gb, lane) is
+// W2[16 gb + 4 (c & 3) + (c >> 2)][4 q + e]; zero outside M x H
+__global__ __launch_bounds__(256) void pack_se_full_kernel(const float *__restrict__ w1,
+                                                           const float *__restrict__ w2, int M, int H,
+                                                           float *__restrict__ w1f,
+                                                           float *__restrict__ w2f) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= 2 * kSeFullFloats) return;
+  const int i2 = i % kSeFullFloats;
+  const int e = i2 & 3, lane = (i2 >> 2) & 63, blk = i2 >> 8, c = lane & 15, q = lane >> 4;
+  if (i < kSeFullFloats) {
+    const int g = 4 * (4 * blk + e) + q, j = c;
+    w1f[i2] = j < H && g < M ? w1[j * M + g] : 0.0f;
+  } else {
+    const int g = 16 * blk + 4 * (c & 3) + (c >> 2), j = 4 * q + e;
+    w2f[i2] = g < M && j < H ? w2[g * H + j] : 0.0f;
+  }
+}
+
+hipError_t launch_pack_se_full(const float *w1, const float *w2, int32_t M, int32_t H, float *w1f,
+                               float *w2f, hipStream_t s) {
+  if (!gather_full_shape(M, H, 32, 0)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_se_full_kernel, dim3((2 * kSeFullFloats + 255) / 256), dim3(256), 0, s, w1,
+                     w2, M, H, w1f, w2f);
+  return hipGetLastError();
+}
+
+// NS: slots per lane (M <= 4 NS); at 12 slots the group rows of two
+// workgroups per CU fit in registers (more slots, at one workgroup per CU,
+// ran slower than the general gather)
+template <typename TS, bool LL, bool HASHED, int NS>
+__global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
+  typedef typename std::conditional<HASHED, uint64_t, int32_t>::type id_t;
+  constexpr int EPC = Elem<TS>::kPerChunk;   // elements per 16-byte chunk
+  constexpr int EPG = 2 * EPC;               // elements per group (d)
+  __shared__ uint64_t s_tab[kFullMaxM];
+  __shared__ uint64_t s_magic[kFullMaxM];
+  __shared__ int32_t s_rows[kFullMaxM];
+  __shared__ int32_t s_pair[kFullMaxM];
+  __shared__ int32_t s_req[kGatherMaxReqLds + 1];
+  __shared__ float4 s_w1[kSeFullFloats / 4], s_w2[kSeFullFloats / 4];   // packed SE operands
+  __shared__ float4 s_b1[4], s_b2[16];   // b1[4 q + e]; b2[16 gb + 4 e + q] at [4 gb + q].e
+  const int M = a.M, H = a.H, nu = a.n_user, n_ad = a.n_ad;
+  const int64_t R = a.R, Q = a.Q;
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int wave = tid >> 6;
+  for (int g = tid; g < M; g += 256) {
+    s_tab[g] = reinterpret_cast<uint64_t>(a.tables[g]);
+    s_magic[g] = a.table_magic[g];
+    s_rows[g] = (int32_t)a.table_rows[g];
+  }
+  const bool gpu_cross = a.cross_pairs != nullptr;
+  if (gpu_cross)
+    for (int f = tid; f < a.n_cross; f += 256) s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
+  const bool req_in_lds = Q <= kGatherMaxReqLds;
+  if (req_in_lds)
+    for (int64_t i = tid; i <= Q; i += 256) s_req[i] = a.req_off[i];
+  s_w1[tid] = reinterpret_cast<const float4 *>(a.w1f)[tid];
+  s_w2[tid] = reinterpret_cast<const float4 *>(a.w2f)[tid];
+  if (tid < 16) {
+    const int j = tid;
+    reinterpret_cast<float *>(s_b1)[j] = j < H ? a.b1[j] : 0.0f;
+  }
+  if (tid < 64) {
+    const int gb = tid >> 4, qq = (tid >> 2) & 3, e = tid & 3, g = 16 * gb + 4 * e + qq;
+    reinterpret_cast<float *>(s_b2)[tid] = g < M ? a.b2[g] : 0.0f;
+  }
+  __syncthreads();
+
+  const int KS = (M + 3) >> 2, GB = (M + 15) >> 4;   // slots and output blocks in use
+  const float inv_d = 1.0f / (float)EPG;             // exact: EPG is a power of two
+  const TS *Uh = static_cast<const TS *>(a.Uh);
+  TS *X = static_cast<TS *>(a.X);
+  const uint64_t dummy = s_tab[0];                   // row 0 of a table: always present
+
+  const int64_t n_tiles = (R + 15) >> 4;
+  for (int64_t wt = (int64_t)blockIdx.x * 4 + wave; wt < n_tiles; wt += (int64_t)gridDim.x * 4) {
+    const int64_t r = wt * 16 + c;
+    const bool row_ok = r < R;
+    const int64_t rr = row_ok ? r : R - 1;           // clamped: loaded, never stored
+    int64_t rq = 0;
+    if (nu > 0 || gpu_cross)
+      rq = req_in_lds ? request_of_row(s_req, Q, rr) : request_of_row(a.req_off, Q, rr);
+
+    // ids of the lane's ad and cross groups, all in flight together
+    id_t idv[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const int g = 4 * k + q;
+      idv[k] = 0;
+      if (k < KS && g >= nu && g < M) {
+        const int f = g - nu;
+        const bool is_ad = f < n_ad;
+        const int fa = is_ad ? f : (gpu_cross ? s_pair[f - n_ad] >> 16 : f - n_ad);
+        const id_t *ids = static_cast<const id_t *>(is_ad || gpu_cross ? a.ad_ids : a.cross_ids);
+        idv[k] = ids[(int64_t)fa * R + rr];
+      }
+    }
+    // table rows and both chunks of every group (loads of absent rows read
+    // row 0 of a table and are zeroed)
+    uint4 raw[NS][2];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      raw[k][0] = raw[k][1] = make_uint4(0, 0, 0, 0);
+      if (k < KS) {
+        const int g = 4 * k + q;
+        uint64_t addr = 0;
+        if (g < M) {
+          if (g < nu) {
+            addr = reinterpret_cast<uint64_t>(Uh + (rq * nu + g) * EPG);
+            if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = a.urow[rq * nu + g];
+          } else {
+            int32_t row;
+            const int f = g - nu;
+            if (gpu_cross && f >= n_ad) {
+              // user x ad cross value: key = mix64(user id) ^ ad id, hashed into
+              // the group's table (ids as their unsigned bit patterns)
+              const int fu = s_pair[f - n_ad] & 0xFFFF;
+              const id_t *uids = static_cast<const id_t *>(a.user_ids);
+              uint64_t uid, aid;
+              if constexpr (HASHED) {
+                uid = (uint64_t)uids[(int64_t)fu * Q + rq];
+                aid = (uint64_t)idv[k];
+              } else {
+                uid = (uint64_t)(uint32_t)uids[(int64_t)fu * Q + rq];
+                aid = (uint64_t)(uint32_t)idv[k];
+              }
+              const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+              row = (int32_t)mod_barrett(mix64((mix64(uid) ^ aid) ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+            } else if constexpr (HASHED) {
+              const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+              row = (int32_t)mod_barrett(mix64((uint64_t)idv[k] ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+            } else {
+              row = (int32_t)idv[k];
+              if (row < 0 || row >= s_rows[g]) {
+                atomicOr(a.err, 1);
+                row = -1;
+              }
+            }
+            if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = row;
+            if (row >= 0) addr = s_tab[g] + (uint64_t)row * (EPG * sizeof(TS));
+          }
+        }
+        const uint64_t at = addr ? addr : dummy;
+        const u32x4 v0 = *reinterpret_cast<gl_u32x4 *>(at);
+        const u32x4 v1 = *reinterpret_cast<gl_u32x4 *>(at + 16);
+        if (addr) {
+          raw[k][0] = make_uint4(v0.x, v0.y, v0.z, v0.w);
+          raw[k][1] = make_uint4(v1.x, v1.y, v1.z, v1.w);
+        }
+      }
+    }
+    // squeeze and layer 1: h^T = ReLU(W1 z^T + b1)
+    f32x4 h;
+    {
+      const float4 bv = s_b1[q];
+      h[0] = bv.x; h[1] = bv.y; h[2] = bv.z; h[3] = bv.w;
+    }
+#pragma unroll
+    for (int u = 0; u < NS / 4; ++u) {
+      if (4 * u < KS) {
+        const float4 wv = s_w1[u * 64 + lane];
+        const float w[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int k = 4 * u + e;
+          float v[EPG];
+          Elem<TS>::unpack(raw[k][0], v);
+          Elem<TS>::unpack(raw[k][1], v + EPC);
+          float zs = 0.0f;
+#pragma unroll
+          for (int i = 0; i < EPG; ++i) zs += v[i];
+          h = __builtin_amdgcn_mfma_f32_16x16x4f32(w[e], zs * inv_d, h, 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = h[e] > 0.0f ? h[e] : 0.0f;
+    // layer 2: the weight of slot 4 gb + e in element e of block gb
+    float sw[NS];
+#pragma unroll
+    for (int gb = 0; gb < NS / 4; ++gb) {
+      if (gb < GB) {
+        const float4 bv = s_b2[4 * gb + q], wv = s_w2[gb * 64 + lane];
+        const float w[4] = {wv.x, wv.y, wv.z, wv.w};
+        f32x4 o;
+        o[0] = bv.x; o[1] = bv.y; o[2] = bv.z; o[3] = bv.w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o = __builtin_amdgcn_mfma_f32_16x16x4f32(w[e], h[e], o, 0, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sw[4 * gb + e] = 1.0f / (1.0f + expf(-o[e]));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sw[4 * gb + e] = 0.0f;
+      }
+    }
+    // reweight, linear_log, round once, store the group's two chunks
+    if (row_ok) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        const int g = 4 * k + q;
+        if (k < KS && g < M) {
+          float v[EPG], o[EPG];
+          Elem<TS>::unpack(raw[k][0], v);
+          Elem<TS>::unpack(raw[k][1], v + EPC);
+#pragma unroll
+          for (int e = 0; e < EPG; ++e) {
+            const float x = sw[k] * v[e];
+            o[e] = LL ? linear_log(x) : x;
+          }
+          uint4 *dst = reinterpret_cast<uint4 *>(X + (r * M + g) * EPG);
+          dst[0] = Elem<TS>::pack(o);
+          dst[1] = Elem<TS>::pack(o + EPC);
+          if (a.s_buf) a.s_buf[r * M + g] = sw[k];
+        }
+      }
+    }
+  }
+}
+
+template <typename TS, bool LL, int NS>
+static hipError_t gather_full_ns(bool hashed, const GatherArgs &a, hipStream_t s) {
+  const void *k = hashed ? reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, true, NS>)
+                         : reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, false, NS>);
+  const int resident = resident_blocks(k, 0);
+  int64_t nb = ((a.R + 15) / 16 + 3) / 4;
+  if (resident > 0 && nb > resident) nb = resident;
+  if (hashed)
+    hipLaunchKernelGGL((gather_full_kernel<TS, LL, true, NS>), dim3((unsigned)nb), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((gather_full_kernel<TS, LL, false, NS>), dim3((unsigned)nb), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename TS, bool LL>
+static hipError_t gather_full_t(bool hashed, const GatherArgs &a, hipStream_t s) {
+  return gather_full_ns<TS, LL, kFullMaxM / 4>(hashed, a, s);
+}
+
+hipError_t launch_gather_full(int dtype, bool linear_log, bool hashed, const GatherArgs &a,
+                              hipStream_t s) {
+  if (a.R <= 0) return hipSuccess;
+  if (!gather_full_supported(dtype, a)) return hipErrorInvalidValue;
+  switch (dtype) {
+    case kF32: return linear_log ? gather_full_t<float, true>(hashed, a, s) : gather_full_t<float, false>(hashed, a, s);
+    case kBF16: return linear_log ? gather_full_t<__bf16, true>(hashed, a, s) : gather_full_t<__bf16, false>(hashed, a, s);
+    default: return linear_log ? gather_full_t<_Float16, true>(hashed, a, s) : gather_full_t<_Float16, false>(hashed, a, s);
+  }
 }
 
 template <typename TS, int MODE, bool LL, int CPT, bool SE_LDS>

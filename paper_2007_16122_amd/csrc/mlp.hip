@@ -264,6 +264,7 @@ template <int BR, int BN, int S, int WN, int KB = 32> struct BufTile {
   static_assert((BN + BR) % (RPI * NW) == 0, "loads must split evenly over the waves");
   static_assert(BN % (16 * WN) == 0 && BR % 32 == 0 && BN % RPI == 0, "tile shape");
   static_assert(S >= 2 && S <= 4, "stages");
+  static_assert(RJ >= 2, "the K loop's read schedule runs two row blocks ahead");
 };
 
 // The K loop of one tile: acc[i][j] = bias + W X^T over K for the
@@ -357,16 +358,27 @@ __device__ __forceinline__ void buf_tile_kloop(
         const unsigned char *base = smem + st * STAGE;
 #pragma unroll
         for (int h = 0; h < KB / 32; ++h) {
-          frag fa[NI];
+          frag fa[NI], fb[RJ];
 #pragma unroll
           for (int i = 0; i < NI; ++i)
             fa[i] = *reinterpret_cast<const frag *>(base + a_off[h] + i * 16 * ROWB);
 #pragma unroll
-          for (int j = 0; j < RJ; ++j) {
-            const frag fb = *reinterpret_cast<const frag *>(base + b_off[h] + j * 16 * ROWB);
+          for (int j = 0; j < RJ; ++j)
+            fb[j] = *reinterpret_cast<const frag *>(base + b_off[h] + j * 16 * ROWB);
 #pragma unroll
-            for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb, acc[i][j]);
+          for (int j = 0; j < RJ; ++j)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb[j], acc[i][j]);
+          // issue order: the A fragments and two B fragments, then one B
+          // fragment read after each row block's NI MFMAs, so that a read is
+          // two blocks ahead of the MFMAs that use it
+          __builtin_amdgcn_sched_group_barrier(0x100, NI + 2, 0);   // DS reads
+#pragma unroll
+          for (int j = 0; j < RJ - 2; ++j) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NI, 0);     // MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NI, 0);
         }
       }
     }

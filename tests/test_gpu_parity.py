@@ -226,6 +226,34 @@ def test_parity_gpu_cross_features(name):
     compare_scores(cfg, g["scores"], o["scores"], f"gpu cross {name}")
 
 
+@pytest.mark.parametrize("kw", [dict(hashed=True), dict(hashed=True, cross="gpu"),
+                                dict(linear_log=True), dict(dtype="f16", linear_log=True),
+                                dict(dtype="f16", hashed=True, linear_log=True, cross="gpu"),
+                                dict(n_ad=20, n_cross=10)])
+def test_parity_register_gather_variants(kw):
+    """The register-resident gather (up to 48 groups, no sequences) in its
+    other forms: hashed ids, GPU-built crosses, linear_log, fp16 storage and
+    fewer groups (42: the last slot of half the lanes empty); gather indices
+    bit-exact, SE weights and scores against the checker."""
+    kw = dict(kw)
+    base = synth.CONFIGS["serving_bf16"]
+    if kw.pop("cross", None) == "gpu":
+        n_cross = kw.get("n_cross", base.n_cross)
+        kw["cross_pairs"] = tuple((f % base.n_user, (3 * f + 1) % base.n_ad) for f in range(n_cross))
+    cfg = mid("serving_bf16", **kw)
+    log(f"test_parity_register_gather_variants {kw}: M={cfg.n_groups}")
+    tables, params, batch = problem(cfg, seed=47, cand=MID_CANDS["serving_bf16"], model_seed=cfg.seed)
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True, want_s=True)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_s=True, want_z=True)
+    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
+    assert_se_weights_close(params, g["s"], o)
+    compare_scores(cfg, g["scores"], o["scores"], f"register gather {kw}")
+
+
 @pytest.mark.parametrize("name", ["serving_bf16", "large_fp16_ll", "multivalued_fp16_ll"])
 def test_parity_many_requests(name):
     """1,500 small requests (0-3 ads each): more request offsets and user
