@@ -480,12 +480,11 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
   static const char *kDenseNames[] = {"dense0", "dense1", "dense2", "dense3", "dense4", "dense5",
                                       "dense6", "dense7", "dense8", "dense9", "dense10", "dense11"};
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
-  // the one-pass SE (no top-k) of small models runs on the register-resident
-  // gather, which reads the users' rows from the pooling pass
+  // the one-pass SE (no top-k) of small models runs on the register-resident gather
   const bool full = !m->literal_se && !topk && gather_full_supported(m->dtype, g);
-  if (full || user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
+  if (user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
     if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
-    if ((e = launch_user_pool(m->dtype, m->hashed, g, s, full)) != hipSuccess)
+    if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "user_pool launch");
   }
   if (m->literal_se) {

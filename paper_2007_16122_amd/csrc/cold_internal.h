@@ -197,12 +197,10 @@ enum GatherMode { kFull = 0, kWeightsOnly = 1, kApplyWeights = 2, kRawOut = 3, k
 
 // launchers (return hipError_t of the launch)
 bool user_pool_needed(int dtype, const GatherArgs &a);
-// the per-request pooling pass; `force` runs it even where the gather could
-// stage the users' rows itself
-hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s,
-                            bool force = false);
+hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s);
 // the register-resident kFull gather (M <= 48, H <= 16, 32-byte group rows,
-// no sequences; needs the pooling pass and the packed SE operands)
+// no sequences; needs the packed SE operands, and the pooling pass where
+// user_pool_needed says so)
 constexpr int kSeFullFloats = 4 * 64 * 4;   // floats of each packed operand
 bool gather_full_shape(int32_t M, int32_t H, int32_t row_bytes, int32_t n_seq);
 bool gather_full_supported(int dtype, const GatherArgs &a);

@@ -638,8 +638,8 @@ bool user_pool_needed(int dtype, const GatherArgs &a) {
   return (int64_t)a.n_user * a.Q * a.d * es > kGatherMaxUserValLds;
 }
 
-hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s, bool force) {
-  if (a.Q <= 0 || !(force || user_pool_needed(dtype, a))) return hipSuccess;
+hipError_t launch_user_pool(int dtype, bool hashed, const GatherArgs &a, hipStream_t s) {
+  if (a.Q <= 0 || !user_pool_needed(dtype, a)) return hipSuccess;
   switch (dtype) {
     case kF32: return user_pool_t<float>(hashed, a, s);
     case kBF16: return user_pool_t<__bf16>(hashed, a, s);
@@ -695,9 +695,9 @@ static int resident_blocks(const void *kernel, size_t shmem) {
 // lane (c, q)), which is layer 2's B operand as it stands; layer 2 forms its
 // output rows in the order g = 16 gb + 4 e + q (row 4 q + e of block gb), so
 // the weight of slot k = 4 gb + e lands in the lane that holds the group.
-// Both SE matrices are packed in that operand order at load time and held in
-// registers.  The users' rows come from the pooling pass (storage type, one
-// per request).  Products and sums are fp32; the squeeze and the SE sums run
+// Both SE matrices are packed in that operand order at load time and staged
+// in LDS.  The users' rows come from the pooling pass (storage type, one per
+// request), or, for few requests, are resolved into LDS by every workgroup.  Products and sums are fp32; the squeeze and the SE sums run
 // in another order than index order, which only moves fp32 rounding, and
 // each row's result does not depend on the other rows of its tile.
 constexpr int kFullMaxM = 48;
@@ -707,6 +707,8 @@ bool gather_full_shape(int32_t M, int32_t H, int32_t row_bytes, int32_t n_seq) {
   return n_seq == 0 && M > 0 && M <= kFullMaxM && H > 0 && H <= kFullMaxH && row_bytes == 32;
 }
 
+// every batch size of a supported model takes this kernel, so that a row's
+// score does not depend on the batch it comes in
 bool gather_full_supported(int dtype, const GatherArgs &a) {
   const int es = dtype == kF32 ? 4 : 2;
   return gather_full_shape(a.M, a.H, a.d * es, a.n_seq) && a.w1f != nullptr && a.w2f != nullptr;
@@ -743,7 +745,7 @@ hipError_t launch_pack_se_full(const float *w1, const float *w2, int32_t M, int3
 // NS: slots per lane (M <= 4 NS); at 12 slots the group rows of two
 // workgroups per CU fit in registers (more slots, at one workgroup per CU,
 // ran slower than the general gather)
-template <typename TS, bool LL, bool HASHED, int NS>
+template <typename TS, bool LL, bool HASHED, int NS, bool ULDS>
 __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
@@ -757,23 +759,26 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   __shared__ int32_t s_req[kGatherMaxReqLds + 1];
   __shared__ float4 s_w1[kSeFullFloats / 4], s_w2[kSeFullFloats / 4];   // packed SE operands
   __shared__ float4 s_b1[4], s_b2[16];   // b1[4 q + e]; b2[16 gb + 4 e + q] at [4 gb + q].e
+  extern __shared__ __align__(16) unsigned char s_users[];   // [Q][nu][2] chunks, then [nu][Q] rows
   const int M = a.M, H = a.H, nu = a.n_user, n_ad = a.n_ad;
   const int64_t R = a.R, Q = a.Q;
   const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
-  const int wave = tid >> 6;
-  for (int g = tid; g < M; g += 256) {
+  const int wave = tid >> 6, nt = 256, nw = 4;
+  for (int g = tid; g < M; g += nt) {
     s_tab[g] = reinterpret_cast<uint64_t>(a.tables[g]);
     s_magic[g] = a.table_magic[g];
     s_rows[g] = (int32_t)a.table_rows[g];
   }
   const bool gpu_cross = a.cross_pairs != nullptr;
   if (gpu_cross)
-    for (int f = tid; f < a.n_cross; f += 256) s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
+    for (int f = tid; f < a.n_cross; f += nt) s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
   const bool req_in_lds = Q <= kGatherMaxReqLds;
   if (req_in_lds)
-    for (int64_t i = tid; i <= Q; i += 256) s_req[i] = a.req_off[i];
-  s_w1[tid] = reinterpret_cast<const float4 *>(a.w1f)[tid];
-  s_w2[tid] = reinterpret_cast<const float4 *>(a.w2f)[tid];
+    for (int64_t i = tid; i <= Q; i += nt) s_req[i] = a.req_off[i];
+  for (int i = tid; i < kSeFullFloats / 4; i += nt) {
+    s_w1[i] = reinterpret_cast<const float4 *>(a.w1f)[i];
+    s_w2[i] = reinterpret_cast<const float4 *>(a.w2f)[i];
+  }
   if (tid < 16) {
     const int j = tid;
     reinterpret_cast<float *>(s_b1)[j] = j < H ? a.b1[j] : 0.0f;
@@ -781,6 +786,30 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   if (tid < 64) {
     const int gb = tid >> 4, qq = (tid >> 2) & 3, e = tid & 3, g = 16 * gb + 4 * e + qq;
     reinterpret_cast<float *>(s_b2)[tid] = g < M ? a.b2[g] : 0.0f;
+  }
+  // few requests: their users' rows resolved and staged here (no pooling pass)
+  constexpr bool users_lds = ULDS;
+  uint4 *s_uval = reinterpret_cast<uint4 *>(s_users);
+  int32_t *s_urow = reinterpret_cast<int32_t *>(s_users + (size_t)Q * nu * 32);
+  if (users_lds) {
+    for (int64_t i = tid; i < Q * nu * 2; i += nt) {
+      const int p = (int)(i & 1);
+      const int64_t qq = (i >> 1) / nu;
+      const int f = (int)((i >> 1) - qq * nu);
+      const int32_t row = resolve_row<HASHED>(a.user_ids, (int64_t)f * Q + qq, f, a.table_rows[f],
+                                              a.table_magic[f], a.err);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (row >= 0) v = reinterpret_cast<const uint4 *>(static_cast<const TS *>(a.tables[f]) + (int64_t)row * EPG)[p];
+      s_uval[i] = v;
+      if (p == 0) s_urow[(int64_t)f * Q + qq] = row;
+    }
+    // request offsets sanity (the pooling pass checks them otherwise)
+    for (int64_t qq = (int64_t)blockIdx.x * nt + tid; qq < Q; qq += (int64_t)gridDim.x * nt) {
+      bool bad = a.req_off[qq + 1] < a.req_off[qq];
+      if (qq == 0) bad |= a.req_off[0] != 0;
+      if (qq == Q - 1) bad |= (int64_t)a.req_off[Q] != R;
+      if (bad) atomicOr(a.err, 2);
+    }
   }
   __syncthreads();
 
@@ -791,7 +820,7 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   const uint64_t dummy = s_tab[0];                   // row 0 of a table: always present
 
   const int64_t n_tiles = (R + 15) >> 4;
-  for (int64_t wt = (int64_t)blockIdx.x * 4 + wave; wt < n_tiles; wt += (int64_t)gridDim.x * 4) {
+  for (int64_t wt = (int64_t)blockIdx.x * nw + wave; wt < n_tiles; wt += (int64_t)gridDim.x * nw) {
     const int64_t r = wt * 16 + c;
     const bool row_ok = r < R;
     const int64_t rr = row_ok ? r : R - 1;           // clamped: loaded, never stored
@@ -824,8 +853,9 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
         uint64_t addr = 0;
         if (g < M) {
           if (g < nu) {
-            addr = reinterpret_cast<uint64_t>(Uh + (rq * nu + g) * EPG);
-            if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = a.urow[rq * nu + g];
+            if (!users_lds) addr = reinterpret_cast<uint64_t>(Uh + (rq * nu + g) * EPG);
+            if (a.rows_out && row_ok)
+              a.rows_out[(int64_t)g * R + r] = users_lds ? s_urow[(int64_t)g * Q + rq] : a.urow[rq * nu + g];
           } else {
             int32_t row;
             const int f = g - nu;
@@ -864,6 +894,9 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
         if (addr) {
           raw[k][0] = make_uint4(v0.x, v0.y, v0.z, v0.w);
           raw[k][1] = make_uint4(v1.x, v1.y, v1.z, v1.w);
+        } else if (users_lds && g < nu) {
+          raw[k][0] = s_uval[(rq * nu + g) * 2];
+          raw[k][1] = s_uval[(rq * nu + g) * 2 + 1];
         }
       }
     }
@@ -935,18 +968,27 @@ __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   }
 }
 
-template <typename TS, bool LL, int NS>
-static hipError_t gather_full_ns(bool hashed, const GatherArgs &a, hipStream_t s) {
-  const void *k = hashed ? reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, true, NS>)
-                         : reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, false, NS>);
-  const int resident = resident_blocks(k, 0);
+template <typename TS, bool LL, int NS, bool ULDS>
+static hipError_t gather_full_u(bool hashed, const GatherArgs &a, hipStream_t s) {
+  const void *k = hashed ? reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, true, NS, ULDS>)
+                         : reinterpret_cast<const void *>(&gather_full_kernel<TS, LL, false, NS, ULDS>);
+  const size_t shmem = ULDS ? (size_t)a.Q * a.n_user * 36 : 0;
+  const int resident = resident_blocks(k, shmem);
   int64_t nb = ((a.R + 15) / 16 + 3) / 4;
   if (resident > 0 && nb > resident) nb = resident;
   if (hashed)
-    hipLaunchKernelGGL((gather_full_kernel<TS, LL, true, NS>), dim3((unsigned)nb), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gather_full_kernel<TS, LL, true, NS, ULDS>), dim3((unsigned)nb), dim3(256), shmem, s, a);
   else
-    hipLaunchKernelGGL((gather_full_kernel<TS, LL, false, NS>), dim3((unsigned)nb), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gather_full_kernel<TS, LL, false, NS, ULDS>), dim3((unsigned)nb), dim3(256), shmem, s, a);
   return hipGetLastError();
+}
+
+// users' rows in LDS when the pooling pass does not run
+template <typename TS, bool LL, int NS>
+static hipError_t gather_full_ns(bool hashed, const GatherArgs &a, hipStream_t s) {
+  if (user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a))
+    return gather_full_u<TS, LL, NS, false>(hashed, a, s);
+  return gather_full_u<TS, LL, NS, true>(hashed, a, s);
 }
 
 template <typename TS, bool LL>

@@ -226,15 +226,21 @@ def test_parity_gpu_cross_features(name):
     compare_scores(cfg, g["scores"], o["scores"], f"gpu cross {name}")
 
 
+REGISTER_GATHER_CANDS = [1500] * 5 + [700, 0, 1, 257]   # 8,458 rows, 9 requests
+
+
 @pytest.mark.parametrize("kw", [dict(hashed=True), dict(hashed=True, cross="gpu"),
                                 dict(linear_log=True), dict(dtype="f16", linear_log=True),
                                 dict(dtype="f16", hashed=True, linear_log=True, cross="gpu"),
-                                dict(n_ad=20, n_cross=10)])
+                                dict(n_ad=20, n_cross=10), dict(n_user=30, n_ad=12, n_cross=6)])
 def test_parity_register_gather_variants(kw):
     """The register-resident gather (up to 48 groups, no sequences) in its
-    other forms: hashed ids, GPU-built crosses, linear_log, fp16 storage and
-    fewer groups (42: the last slot of half the lanes empty); gather indices
-    bit-exact, SE weights and scores against the checker."""
+    other forms, on a batch of more tiles than one round of workgroups: hashed ids,
+    GPU-built crosses, linear_log, fp16 storage, fewer groups (42: the last
+    slot of half the lanes empty) and 30 user fields over 9 requests (user
+    rows in the pooling pass's buffer instead of LDS); gather indices
+    bit-exact, SE weights and scores against the checker on a seeded sample
+    of rows (every request's first and last row included)."""
     kw = dict(kw)
     base = synth.CONFIGS["serving_bf16"]
     if kw.pop("cross", None) == "gpu":
@@ -242,16 +248,22 @@ def test_parity_register_gather_variants(kw):
         kw["cross_pairs"] = tuple((f % base.n_user, (3 * f + 1) % base.n_ad) for f in range(n_cross))
     cfg = mid("serving_bf16", **kw)
     log(f"test_parity_register_gather_variants {kw}: M={cfg.n_groups}")
-    tables, params, batch = problem(cfg, seed=47, cand=MID_CANDS["serving_bf16"], model_seed=cfg.seed)
+    tables, params, batch = problem(cfg, seed=47, cand=REGISTER_GATHER_CANDS, model_seed=cfg.seed)
     run = load(cfg, tables, params)
     try:
         g = run.score(batch, want_rows=True, want_s=True)
     finally:
         run.close()
-    o = run_oracle(cfg, tables, params, batch, want_rows=True, want_s=True, want_z=True)
-    assert np.array_equal(g["rows"], o["rows"].T.astype(np.int32)), "gather indices differ"
-    assert_se_weights_close(params, g["s"], o)
-    compare_scores(cfg, g["scores"], o["scores"], f"register gather {kw}")
+    rng = np.random.default_rng(53)
+    off = batch["req_off"]
+    ends = np.concatenate([off[:-1], off[1:] - 1])
+    sample = np.unique(np.concatenate([rng.choice(batch["n_rows"], 700, replace=False), ends]))
+    sample = sample[(sample >= 0) & (sample < batch["n_rows"])]
+    o = run_oracle(cfg, tables, params, batch, sample=sample, want_rows=True, want_s=True,
+                   want_z=True)
+    assert np.array_equal(g["rows"][:, sample], o["rows"].T.astype(np.int32)), "gather indices differ"
+    assert_se_weights_close(params, g["s"][sample], o)
+    compare_scores(cfg, g["scores"][sample], o["scores"], f"register gather {kw}")
 
 
 @pytest.mark.parametrize("name", ["serving_bf16", "large_fp16_ll", "multivalued_fp16_ll"])
@@ -469,11 +481,12 @@ def test_user_broadcast_equals_per_row_bitwise():
 
 @pytest.mark.parametrize("name", ["serving_bf16", "multivalued_fp16_ll"])
 def test_request_alone_equals_batch_bitwise(name):
-    """A 2,000-ad request scored alone (small-batch layer tiles, one row per
-    gather wave, user rows staged by the gather) gives bit-identical scores
-    to the same request inside a 32-request batch (256 x 256 layer tiles,
-    five rows per wave, pooled user rows): every sum runs in the same order
-    whatever the launch shape, so a score does not depend on the batch."""
+    """A 2,000-ad request scored alone (small-batch layer tiles; user rows
+    staged in LDS by the gather; on the sequence model one row per gather
+    wave) gives bit-identical scores to the same request inside a
+    32-request batch (256 x 256 layer tiles, pooled user rows, five rows per
+    wave): every sum runs in the same order whatever the launch shape, so a
+    score does not depend on the batch."""
     cfg = mid(name, n_requests=32, cand_per_request=2000)
     log(f"test_request_alone_equals_batch_bitwise {name}: R={cfg.n_rows}")
     tables, params, batch = problem(cfg, seed=33, model_seed=cfg.seed)
