@@ -143,7 +143,9 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   w.actB = take((size_t)m.es * R * m.max_hidden);
   w.sbuf = take(sbuf ? sizeof(float) * (size_t)R * m.M : 0);
   w.zbuf = take(topk_split(m) ? sizeof(float) * (size_t)R * m.M : 0);
-  w.partial = take(topk ? sizeof(float) * (size_t)Q * kMaskParts * m.M : 0);
+  // per-request part sums of the mask, or the row-wise SE's 16-row tile sums
+  const size_t parts = topk_split(m) ? (size_t)((R + 15) / 16) * m.M : (size_t)Q * kMaskParts * m.M;
+  w.partial = take(topk ? sizeof(float) * parts : 0);
   w.mask = take(topk ? (size_t)Q * m.M : 0);
   w.total = off;
   return w;
@@ -523,7 +525,8 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     if (e != hipSuccess) return hip_fail(m, e, "gather_se launch");
   } else if (topk_split(*m)) {
     // gather with squeeze (rows kept exact in the input's place), SE of the
-    // rows on the matrix cores, the per-request mask, reweighting in place
+    // rows on the matrix cores with their 16-row tile sums, the per-request
+    // mask in one launch, reweighting in place
     float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
     uint8_t *mask = W + wl.mask;
     g.s_buf = nullptr;
@@ -532,13 +535,13 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     if ((e = launch_gather_se(m->dtype, kSqueezeRaw, false, m->hashed, g, s)) != hipSuccess)
       return hip_fail(m, e, "gather_se (squeeze) launch");
     if ((e = marks.mark("se_rows")) != hipSuccess) return hip_fail(m, e, "profile event");
+    float *tpart = reinterpret_cast<float *>(W + wl.partial);
     if ((e = launch_se_rows(g.z_out, sb, R, m->M, m->H, reinterpret_cast<const float *>(A + al.w1p), g.b1,
-                              reinterpret_cast<const float *>(A + al.w2p), g.b2, s)) != hipSuccess)
+                              reinterpret_cast<const float *>(A + al.w2p), g.b2, tpart, s)) != hipSuccess)
       return hip_fail(m, e, "se_rows launch");
     if ((e = marks.mark("group_mask")) != hipSuccess) return hip_fail(m, e, "profile event");
-    if ((e = launch_group_mask(sb, b->req_off, Q, R, m->M, D.topk_k,
-                               reinterpret_cast<float *>(W + wl.partial), kMaskParts, mask,
-                               group_mask, s)) != hipSuccess)
+    if ((e = launch_group_mask_tiles(sb, tpart, b->req_off, Q, R, m->M, D.topk_k, mask, group_mask,
+                                     s)) != hipSuccess)
       return hip_fail(m, e, "group_mask launch");
     if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_apply_weights(m->dtype, D.linear_log, W + wl.X, sb, mask, b->req_off, Q, R, m->M,

@@ -219,9 +219,14 @@ int device_cus();
 // SE weights of every row from its squeeze (Eq. 2 read as squeeze ->
 // FC -> ReLU -> FC -> sigmoid): s [R][M] from z [R][M] on the fp32 matrix
 // cores, with W1 and W2 packed by launch_pack_se_rows; M <= 256, H <= 64
+// (tile_part, when not null: [ceil(R / 16)][M] sums of s over each 16-row tile)
 hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, int32_t H,
                           const float *w1p, const float *b1, const float *w2p, const float *b2,
-                          hipStream_t s);
+                          float *tile_part, hipStream_t s);
+// the top-k mask of every request from s [R][M] and se_rows' tile sums
+hipError_t launch_group_mask_tiles(const float *s_buf, const float *tile_part,
+                                   const int32_t *req_off, int64_t Q, int64_t R, int32_t M,
+                                   int32_t k, uint8_t *mask, uint8_t *mask_out, hipStream_t s);
 // floats of the two packed SE operands (0 when M or H is beyond the kernel)
 void se_rows_packed_floats(int32_t M, int32_t H, size_t *n1, size_t *n2);
 // W1 [H][M] and W2 [M][H] into the row-wise SE kernel's operand order

@@ -622,6 +622,120 @@ __global__ __launch_bounds__(1024) void mask_select_kernel(const float *partial,
   }
 }
 
+// The same importance and mask from the row-wise SE's 16-row tile sums:
+// request q adds, per group, the rows before its first whole tile, the sums
+// of its whole tiles in P contiguous parts (P threads per group or per four
+// groups, whose loads are all in flight together; the parts added in order)
+// and the rows after its last whole tile, in that order, so the result does
+// not depend on the launch.
+// parts of the tile sums: the block's threads but the last M (which add the
+// rows outside whole tiles) over the groups, one or four groups per thread
+__host__ __device__ inline int mask_tile_parts(int M) {
+  const int nq = M % 4 == 0 ? M / 4 : M;   // threads per part
+  const int p = (1024 - M) / nq;
+  return p < 1 ? 1 : (p > 64 ? 64 : p);
+}
+
+__global__ __launch_bounds__(1024) void mask_select_tiles_kernel(const float *s_buf,
+                                                                 const float *tpart,
+                                                                 const int32_t *req_off, int64_t R,
+                                                                 int32_t M, int32_t k, uint8_t *mask,
+                                                                 uint8_t *mask_out) {
+  extern __shared__ float lds[];  // [P][M] part sums, [M] importance, [M] ranks, [2][M] edges
+  const int P = mask_tile_parts(M);
+  float *imp = lds + P * M;
+  int *rank = reinterpret_cast<int *>(imp + M);
+  const int64_t q = blockIdx.x;
+  int64_t lo = req_off[q], hi = req_off[q + 1];
+  lo = lo < 0 ? 0 : (lo > R ? R : lo);
+  hi = hi < lo ? lo : (hi > R ? R : hi);
+  const float n = (float)(hi - lo);
+  const int64_t t0 = (lo + 15) / 16, t1 = hi / 16;   // whole tiles [t0, t1)
+  const bool whole = t0 < t1;
+  // rows outside whole tiles: fewer than 32 before them (all rows when there
+  // are none), fewer than 16 after them
+  const int64_t head_end = whole ? 16 * t0 : hi, tail_begin = whole ? 16 * t1 : hi;
+  const int64_t nt = whole ? t1 - t0 : 0, per = (nt + P - 1) / P;
+  const bool v4 = M % 4 == 0;
+  const int nq = v4 ? M / 4 : M;
+  for (int idx = threadIdx.x; idx < P * nq; idx += (int)blockDim.x - M) {
+    const int p = idx / nq, gq = idx - p * nq;
+    const int64_t a = t0 + p * per, b = a + per < t0 + nt ? a + per : t0 + nt;
+    if (v4) {
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 16
+      for (int64_t t = a; t < b; ++t) {
+        const float4 v = reinterpret_cast<const float4 *>(tpart + t * M)[gq];
+        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      }
+      reinterpret_cast<float4 *>(lds + p * M)[gq] = acc;
+    } else {
+      float acc = 0.0f;
+#pragma unroll 16
+      for (int64_t t = a; t < b; ++t) acc += tpart[t * M + gq];
+      lds[p * M + gq] = acc;
+    }
+  }
+  // the rows outside whole tiles, summed in row order by the last M threads
+  // of the block while the others add the tiles (every load in flight first)
+  float *edge = reinterpret_cast<float *>(rank + M);   // [2][M] head and tail sums
+  for (int g = (int)threadIdx.x - ((int)blockDim.x - M); g >= 0; g = -1) {
+    float hv[32], tv[16];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) hv[i] = lo + i < head_end ? s_buf[(lo + i) * M + g] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tv[i] = tail_begin + i < hi ? s_buf[(tail_begin + i) * M + g] : 0.0f;
+    float h = 0.0f, t = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) h += hv[i];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t += tv[i];
+    edge[g] = h;
+    edge[M + g] = t;
+  }
+  for (int g = threadIdx.x; g < M; g += blockDim.x) rank[g] = 0;
+  __syncthreads();
+  for (int g = threadIdx.x; g < M; g += blockDim.x) {
+    float acc = edge[g];
+    for (int p = 0; p < P; ++p) acc += lds[p * M + g];
+    acc += edge[M + g];
+    imp[g] = n > 0.0f ? acc / n : 0.0f;
+  }
+  __syncthreads();
+  // rank of group g: groups ahead of it, counted by several threads over
+  // blocks of the others (integer sums: any order gives the same count)
+  const int RP = (int)(blockDim.x / M) < 1 ? 1 : (int)(blockDim.x / M);
+  const int rper = (M + RP - 1) / RP;
+  for (int idx = threadIdx.x; idx < RP * M; idx += blockDim.x) {
+    const int rp = idx / M, g = idx - rp * M;
+    const float ig = imp[g];
+    const int o0 = rp * rper, o1 = o0 + rper < M ? o0 + rper : M;
+    int cnt = 0;
+    for (int o = o0; o < o1; ++o) {
+      const float io = imp[o];
+      cnt += (io > ig || (io == ig && o < g)) ? 1 : 0;
+    }
+    atomicAdd(&rank[g], cnt);
+  }
+  __syncthreads();
+  for (int g = threadIdx.x; g < M; g += blockDim.x) {
+    const uint8_t keep = rank[g] < k ? 1 : 0;
+    mask[q * M + g] = keep;
+    if (mask_out) mask_out[q * M + g] = keep;
+  }
+}
+
+hipError_t launch_group_mask_tiles(const float *s_buf, const float *tile_part,
+                                   const int32_t *req_off, int64_t Q, int64_t R, int32_t M,
+                                   int32_t k, uint8_t *mask, uint8_t *mask_out, hipStream_t s) {
+  if (Q <= 0) return hipSuccess;
+  if (M % 4 == 0 && (reinterpret_cast<uintptr_t>(tile_part) & 15)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(mask_select_tiles_kernel, dim3((unsigned)Q), dim3(1024),
+                     sizeof(float) * (size_t)(mask_tile_parts(M) + 4) * M, s, s_buf, tile_part,
+                     req_off, R, M, k, mask, mask_out);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------- launchers
 template <typename TS>
 static hipError_t user_pool_t(bool hashed, const GatherArgs &a, hipStream_t s) {
@@ -1201,7 +1315,8 @@ __global__ __launch_bounds__(256) void se_rows_kernel(const float *__restrict__ 
                                                       int H, const float4 *__restrict__ w1p,
                                                       const float *__restrict__ b1,
                                                       const float4 *__restrict__ w2p,
-                                                      const float *__restrict__ b2) {
+                                                      const float *__restrict__ b2,
+                                                      float *__restrict__ tpart) {
   constexpr int kMaxStride = 16 * NC + 4;
   __shared__ __align__(16) float zs[kSeTile * kMaxStride];   // row c at c * ZST
   __shared__ float hs[kSeMaxH * kSeTile];                     // h^T: unit j, row c at j * 16 + c
@@ -1284,11 +1399,31 @@ __global__ __launch_bounds__(256) void se_rows_kernel(const float *__restrict__ 
           o = __builtin_amdgcn_mfma_f32_16x16x4f32(wb[i][v].w, hb[4 * v + 3], o, 0, 0, 0);
         }
         // lane holds s[row r0 + c][group gb * 16 + 4 q + e]
+        float sv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sv[e] = 1.0f / (1.0f + expf(-o[e]));
         if (row < R) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int gg = gb * 16 + 4 * q + e;
-            if (gg < M) s_out[row * M + gg] = 1.0f / (1.0f + expf(-o[e]));
+            if (gg < M) s_out[row * M + gg] = sv[e];
+          }
+        }
+        if (tpart) {
+          // the tile's sum of each group's weight over its rows: a fixed
+          // butterfly over the 16 lanes of a quarter, lane c = 0 stores it
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sv[e] = row < R ? sv[e] : 0.0f;
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sv[e] += __shfl_xor(sv[e], off);
+          if (c == 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int gg = gb * 16 + 4 * q + e;
+              if (gg < M) tpart[(r0 / kSeTile) * M + gg] = sv[e];
+            }
           }
         }
       }
@@ -1300,7 +1435,7 @@ __global__ __launch_bounds__(256) void se_rows_kernel(const float *__restrict__ 
 
 hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, int32_t H,
                           const float *w1p, const float *b1, const float *w2p, const float *b2,
-                          hipStream_t s) {
+                          float *tile_part, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   if (M <= 0 || M > 256 || H <= 0 || H > kSeMaxH) return hipErrorInvalidValue;
   if ((reinterpret_cast<uintptr_t>(w1p) | reinterpret_cast<uintptr_t>(w2p)) & 15)
@@ -1312,9 +1447,9 @@ hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, in
   const float4 *a1 = reinterpret_cast<const float4 *>(w1p);
   const float4 *a2 = reinterpret_cast<const float4 *>(w2p);
   switch (se_rows_nc(M)) {
-    case 4: hipLaunchKernelGGL(se_rows_kernel<4>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2); break;
-    case 8: hipLaunchKernelGGL(se_rows_kernel<8>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2); break;
-    default: hipLaunchKernelGGL(se_rows_kernel<16>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2);
+    case 4: hipLaunchKernelGGL(se_rows_kernel<4>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2, tile_part); break;
+    case 8: hipLaunchKernelGGL(se_rows_kernel<8>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2, tile_part); break;
+    default: hipLaunchKernelGGL(se_rows_kernel<16>, dim3(grid), dim3(256), 0, s, z, s_out, R, M, H, a1, b1, a2, b2, tile_part);
   }
   return hipGetLastError();
 }
