@@ -748,32 +748,33 @@ __global__ __launch_bounds__(256, 2) void mlp_tail_kernel(const TS *__restrict__
 // takes two passes: pass p holds row blocks 4p .. 4p + 3 of every wave's
 // 128 rows, so each wave frees half of its accumulators per pass. The
 // layer's output never goes to HBM.
-template <typename TS, int BR, int MINB>
-__global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
+template <typename TS, int BR, int MINB, int WN = 4, int KB = 64, int S = 2>
+__global__ __launch_bounds__(128 * WN, MINB) void dense_tail_kernel(
     const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
     int K, int tiles_total, const TS *__restrict__ W1, const float *__restrict__ b1,
     const TS *__restrict__ W2, const float *__restrict__ b2, const TS *__restrict__ Wh,
     const float *__restrict__ bh, int n_out, float *__restrict__ scores) {
   typedef typename Mfma<TS>::frag frag;
-  constexpr int BN = 256, S = 2, WN = 4, KB = 64;
-  static_assert(BR == 256 || BR == 64, "tile rows");
+  constexpr int BN = 256;
   typedef BufTile<BR, BN, S, WN, KB> G;
-  constexpr int NI = G::NI, RJ = G::RJ;
+  constexpr int NI = G::NI, RJ = G::RJ, NT = G::NT;
   constexpr int N1 = 128, N2 = 64;                     // tail widths
   constexpr int S1 = N1 + 8, S2 = N2 + 4;              // padded LDS rows of the tail
   constexpr int HROW = BN * 2;                         // bytes per row of the layer's output
   constexpr int KS1 = BN / 32, KS2 = N1 / 32;
-  constexpr int PR = BR < 128 ? BR : 128;              // rows per pass
+  // rows per pass: as many as the ring holds as hi/lo pairs, at most 128
+  constexpr int PR = BR <= 128 && 2 * BR * HROW <= G::RING ? BR : (2 * 128 * HROW <= G::RING ? 128 : 64);
   constexpr int NP = BR / PR, JP = RJ / NP;            // passes; row blocks of a wave per pass
-  constexpr int JB = PR / 32;                          // row blocks of a wave in the tail layers
+  constexpr int RH = G::NW / 4;                        // row groups of the tail layers
+  constexpr int JB = PR / RH / 16;                     // row blocks of a wave in the tail layers
   constexpr int H3_BYTES = 2 * PR * HROW;              // hi and lo of the layer's output
   constexpr int H1_BYTES = 2 * PR * S1 * 2, H2_BYTES = PR * S2 * 4;
   // head weights in the ring when it has room past the layer's output
   constexpr bool WH_IN_RING = G::RING >= H3_BYTES + 2 * N2 * 4 + 16;
   static_assert(G::RING >= H3_BYTES, "a pass of the layer's output takes the ring");
-  static_assert(G::NW == N1 / 16 && G::NW == 2 * (N2 / 16), "8 waves: the tail layers split 4 (features) x 2 (rows)");
+  static_assert(G::NW == 4 || G::NW == 8, "the tail layers split 4 (features) x NW / 4 (rows)");
   static_assert(H1_BYTES + H2_BYTES <= H3_BYTES, "both hidden tiles fit where the layer's output was");
-  static_assert(RJ % NP == 0 && PR * 4 <= 512, "passes");
+  static_assert(RJ % NP == 0 && PR * 4 <= NT && JB >= 1, "passes");
   __shared__ __align__(16) unsigned char smem[G::RING];
   __shared__ float s_whb_own[WH_IN_RING ? 1 : 2 * N2 + 4];
   float *s_wh = WH_IN_RING ? reinterpret_cast<float *>(smem + H3_BYTES) : s_whb_own;
@@ -835,9 +836,9 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
     }
     __syncthreads();   // the pass's tile (and the head weights) are in the LDS
 
-    // first tail layer (each wave reads half of the pass's rows once for its
-    // two feature blocks); the tile is dead once every wave has its sums, and
-    // the layer's output takes its place
+    // first tail layer (each wave reads its row group of the pass once for
+    // its two feature blocks); the tile is dead once every wave has its
+    // sums, and the layer's output takes its place
     auto in0 = [&](int row, int c) {
       return reinterpret_cast<const TS *>(smem + row * HROW + ((c ^ (row & 7)) << 4));
     };
@@ -846,7 +847,7 @@ __global__ __launch_bounds__(512, MINB) void dense_tail_kernel(
     __syncthreads();
     tail_store_ext<TS, 2, JB>(a1, b1, s_h1, S1, PR * S1, 2 * (wave % 4), (wave / 4) * JB, lane);
     __syncthreads();
-    // second tail layer (wave w: feature block w % 4, rows PR/2 (w / 4) ..),
+    // second tail layer (wave w: feature block w % 4 over its row group),
     // output in fp32 after the first layer's
     auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
     f32x4 a2[1][JB];
@@ -1141,13 +1142,13 @@ bool dense_tail_supported(int dtype, int64_t R, int32_t N, int32_t K) {
   return dtype != kF32 && N == 256 && K > 0 && K % 64 == 0 && R > 0 && (R + 63) / 64 <= 0x7FFFFFFF;
 }
 
-template <typename TS, int BR, int MINB>
+template <typename TS, int BR, int MINB, int WN = 4, int KB = 64, int S = 2>
 static void launch_dense_tail_t(const void *x, const void *w, const float *b, int32_t K,
                                 const void *w1, const float *b1, const void *w2, const float *b2,
                                 const void *wh, const float *bh, int32_t n_out, float *scores,
                                 int64_t R, hipStream_t s) {
   const int tiles = (int)((R + BR - 1) / BR);
-  hipLaunchKernelGGL((dense_tail_kernel<TS, BR, MINB>), dim3(tiles), dim3(512), 0, s,
+  hipLaunchKernelGGL((dense_tail_kernel<TS, BR, MINB, WN, KB, S>), dim3(tiles), dim3(128 * WN), 0, s,
                      static_cast<const TS *>(x), static_cast<const TS *>(w), b, R, K, tiles,
                      static_cast<const TS *>(w1), b1, static_cast<const TS *>(w2), b2,
                      static_cast<const TS *>(wh), bh, n_out, scores);
@@ -1158,14 +1159,22 @@ hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const floa
                              const float *b2, const void *wh, const float *bh, int32_t n_out,
                              float *scores, int64_t R, hipStream_t s) {
   if (!dense_tail_supported(dtype, R, N, K)) return hipErrorNotSupported;
-  // 256-row tiles where the separate layer would use 256 x 256 tiles (at
-  // least one tile per CU), 64-row tiles for smaller batches
+  // 256-row tiles over 8 waves while the separate layer would use 256 x 256
+  // tiles (at least one tile per CU); for batches of many rounds of tiles,
+  // 128-row tiles over 4 waves in 72 KB of LDS, two workgroups per CU, so
+  // that one's tail phase overlaps the other's K loop (the large workload,
+  // 1.28 M rows: 720 -> 650 us; at 64,000 rows, one round, 40 -> 42 us);
+  // 64-row tiles for smaller batches. Every variant sums in the same order.
   const bool big = ((R + 255) / 256) * 2 >= 256;
+  const int cus = device_cus() > 0 ? device_cus() : 256;
+  const bool rounds = (R + 127) / 128 >= 8 * (int64_t)cus;
   if (dtype == kBF16) {
-    if (big) launch_dense_tail_t<__bf16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    if (big && rounds) launch_dense_tail_t<__bf16, 128, 2, 2, 32, 3>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else if (big) launch_dense_tail_t<__bf16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else launch_dense_tail_t<__bf16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   } else {
-    if (big) launch_dense_tail_t<_Float16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    if (big && rounds) launch_dense_tail_t<_Float16, 128, 2, 2, 32, 3>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else if (big) launch_dense_tail_t<_Float16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else launch_dense_tail_t<_Float16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   }
   return hipGetLastError();

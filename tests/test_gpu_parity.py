@@ -479,18 +479,21 @@ def test_user_broadcast_equals_per_row_bitwise():
     assert np.array_equal(got, base)
 
 
-@pytest.mark.parametrize("name", ["serving_bf16", "multivalued_fp16_ll"])
-def test_request_alone_equals_batch_bitwise(name):
+@pytest.mark.parametrize("name,n_req", [("serving_bf16", 32), ("multivalued_fp16_ll", 32),
+                                        ("large_fp16_ll", 140)])
+def test_request_alone_equals_batch_bitwise(name, n_req):
     """A 2,000-ad request scored alone (small-batch layer tiles; user rows
     staged in LDS by the gather; on the sequence model one row per gather
-    wave) gives bit-identical scores to the same request inside a
-    32-request batch (256 x 256 layer tiles, pooled user rows, five rows per
-    wave): every sum runs in the same order whatever the launch shape, so a
-    score does not depend on the batch."""
-    cfg = mid(name, n_requests=32, cand_per_request=2000)
+    wave) gives bit-identical scores to the same request inside a batch
+    (256 x 256 layer tiles, pooled user rows, five rows per wave; at 140
+    requests, 280,000 rows, the fused last layers on 128-row tiles over four
+    waves instead of 256-row tiles over eight): every sum runs in the same
+    order whatever the launch shape, so a score does not depend on the
+    batch."""
+    cfg = mid(name, n_requests=n_req, cand_per_request=2000)
     log(f"test_request_alone_equals_batch_bitwise {name}: R={cfg.n_rows}")
     tables, params, batch = problem(cfg, seed=33, model_seed=cfg.seed)
-    qs = [0, 17, 31]
+    qs = [0, 17, n_req - 1]
     run = load(cfg, tables, params)
     try:
         full = run.score(batch)["scores"]
