@@ -466,7 +466,7 @@ def _stage_of(kernel_name, dense_index):
         mode = mt.group(1) if mt else "0"
         return {"0": "gather_se", "1": "se_weights", "2": "gather_apply", "3": "gather_raw",
                 "4": "gather_sq"}.get(mode, "gather_se")
-    if "gather_full_kernel" in kernel_name:
+    if "gather_full" in kernel_name:
         return "gather_se"
     if "se_rows_kernel" in kernel_name:
         return "se_rows"

@@ -799,23 +799,33 @@ static int resident_blocks(const void *kernel, size_t shmem) {
 // ------------------------------------------------------------- gather_full
 // Gather, squeeze, SE and reweighting of a row tile in registers (Section
 // 3.2: Eq. 2 read as squeeze -> FC -> ReLU -> FC -> sigmoid, Eq. 3 when LL),
-// for models with at most 48 groups, at most 16 hidden SE units, 32-byte
-// group rows and no sequence groups.  A wave takes 16 rows; lane l = 16 q + c
-// owns row c of the tile and the groups g = 4 k + q of its slots k: it loads
-// their ids and both 16-byte chunks of each group row itself, so a group's
-// squeeze is a sum inside one lane, and the lanes' squeeze values are already
-// the B operand of a 16x16x4 fp32 MFMA whose K index is g = 4 k + q at step
-// k.  Layer 1 is one 16-unit hidden block (h^T = W1 z^T, units 4 q + e in
-// lane (c, q)), which is layer 2's B operand as it stands; layer 2 forms its
-// output rows in the order g = 16 gb + 4 e + q (row 4 q + e of block gb), so
-// the weight of slot k = 4 gb + e lands in the lane that holds the group.
-// Both SE matrices are packed in that operand order at load time and staged
-// in LDS.  The users' rows come from the pooling pass (storage type, one per
-// request), or, for few requests, are resolved into LDS by every workgroup.  Products and sums are fp32; the squeeze and the SE sums run
-// in another order than index order, which only moves fp32 rounding, and
-// each row's result does not depend on the other rows of its tile.
-constexpr int kFullMaxM = 48;
+// for models with at most 64 groups, at most 16 hidden SE units, 32-byte
+// group rows and no sequence groups.  A tile is 16 rows; lane l = 16 q + c
+// of a wave owns row c and groups g = 4 k + q of its slots k: it loads their
+// ids and both 16-byte chunks of each group row itself, so a group's squeeze
+// is a sum inside one lane, and the lanes' squeeze values are already the B
+// operand of a 16x16x4 fp32 MFMA whose K index is g = 4 k + q at step k.
+// Layer 1 is one 16-unit hidden block (h^T = W1 z^T); its output fragment
+// (units 4 q + e of row c in lane (c, q)) is layer 2's B operand as it
+// stands.  Layer 2 forms its output rows in the order g = 16 gb + 4 e + q
+// (row 4 q + e of block gb), so the weight of slot k = 4 gb + e lands in the
+// lane that holds the group's values.  Both SE matrices are packed in that
+// operand order at load time and staged in LDS.  The users' rows come from
+// the pooling pass (storage type, one per request), or, for few requests,
+// are resolved into LDS by every workgroup.
+//   Up to 48 groups, one wave takes a whole tile (12 slots per lane, held in
+// registers from the gather to the store).  Above that, a workgroup takes a
+// tile with one wave per 16 groups (4 slots per lane); each wave forms
+// layer 1's sum over its own slots (wave 0's from b1), the parts are added
+// in wave order through LDS, and wave w forms layer 2's block gb = w.
+//   Products and sums are fp32; the squeeze and the SE sums run in another
+// order than the general gather's index order, which only moves fp32
+// rounding.  A row's result does not depend on the other rows of its tile,
+// and every batch size of a model takes the same form, so a score does not
+// depend on the batch it comes in.
+constexpr int kFullMaxM = 64;
 constexpr int kFullMaxH = 16;
+constexpr int kFullTileM = 48;   // the one-wave-per-tile form up to this many groups
 
 bool gather_full_shape(int32_t M, int32_t H, int32_t row_bytes, int32_t n_seq) {
   return n_seq == 0 && M > 0 && M <= kFullMaxM && H > 0 && H <= kFullMaxH && row_bytes == 32;
@@ -856,9 +866,9 @@ hipError_t launch_pack_se_full(const float *w1, const float *w2, int32_t M, int3
   return hipGetLastError();
 }
 
-// NS: slots per lane (M <= 4 NS); at 12 slots the group rows of two
-// workgroups per CU fit in registers (more slots, at one workgroup per CU,
-// ran slower than the general gather)
+// Models of up to 48 groups: one wave per 16-row tile and all its groups,
+// NS slots per lane (M <= 4 NS); at 12 slots the group rows of two
+// workgroups per CU fit in registers.
 template <typename TS, bool LL, bool HASHED, int NS, bool ULDS>
 __global__ __launch_bounds__(256, 2) void gather_full_kernel(GatherArgs a) {
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -1097,17 +1107,250 @@ static hipError_t gather_full_u(bool hashed, const GatherArgs &a, hipStream_t s)
   return hipGetLastError();
 }
 
-// users' rows in LDS when the pooling pass does not run
-template <typename TS, bool LL, int NS>
-static hipError_t gather_full_ns(bool hashed, const GatherArgs &a, hipStream_t s) {
-  if (user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a))
-    return gather_full_u<TS, LL, NS, false>(hashed, a, s);
-  return gather_full_u<TS, LL, NS, true>(hashed, a, s);
+// One wave per 16 groups (models of 49 to 64 groups)
+template <typename TS, bool LL, bool HASHED, bool ULDS>
+__global__ __launch_bounds__(256) void gather_full_split_kernel(GatherArgs a) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
+  typedef typename std::conditional<HASHED, uint64_t, int32_t>::type id_t;
+  constexpr int EPC = Elem<TS>::kPerChunk;   // elements per 16-byte chunk
+  constexpr int EPG = 2 * EPC;               // elements per group (d)
+  __shared__ uint64_t s_tab[kFullMaxM];
+  __shared__ uint64_t s_magic[kFullMaxM];
+  __shared__ int32_t s_rows[kFullMaxM];
+  __shared__ int32_t s_pair[kFullMaxM];
+  __shared__ int32_t s_req[kGatherMaxReqLds + 1];
+  __shared__ float4 s_w1[kSeFullFloats / 4], s_w2[kSeFullFloats / 4];   // packed SE operands
+  __shared__ float4 s_b1[4], s_b2[16];   // b1[4 q + e]; b2[16 gb + 4 e + q] at [4 gb + q].e
+  __shared__ float4 s_hp[2][kFullMaxM / 16][64];   // the waves' layer-1 partial sums, by tile parity
+  extern __shared__ __align__(16) unsigned char s_users[];   // [Q][nu][2] chunks, then [nu][Q] rows
+  const int M = a.M, H = a.H, nu = a.n_user, n_ad = a.n_ad;
+  const int64_t R = a.R, Q = a.Q;
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nt = blockDim.x, GB = nt >> 6;   // one wave per 16 groups
+  for (int g = tid; g < M; g += nt) {
+    s_tab[g] = reinterpret_cast<uint64_t>(a.tables[g]);
+    s_magic[g] = a.table_magic[g];
+    s_rows[g] = (int32_t)a.table_rows[g];
+  }
+  const bool gpu_cross = a.cross_pairs != nullptr;
+  if (gpu_cross)
+    for (int f = tid; f < a.n_cross; f += nt) s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
+  const bool req_in_lds = Q <= kGatherMaxReqLds;
+  if (req_in_lds)
+    for (int64_t i = tid; i <= Q; i += nt) s_req[i] = a.req_off[i];
+  for (int i = tid; i < kSeFullFloats / 4; i += nt) {
+    s_w1[i] = reinterpret_cast<const float4 *>(a.w1f)[i];
+    s_w2[i] = reinterpret_cast<const float4 *>(a.w2f)[i];
+  }
+  if (tid < 16) {
+    const int j = tid;
+    reinterpret_cast<float *>(s_b1)[j] = j < H ? a.b1[j] : 0.0f;
+  }
+  if (tid < 64) {
+    const int gb = tid >> 4, qq = (tid >> 2) & 3, e = tid & 3, g = 16 * gb + 4 * e + qq;
+    reinterpret_cast<float *>(s_b2)[tid] = g < M ? a.b2[g] : 0.0f;
+  }
+  // few requests: their users' rows resolved and staged here (no pooling pass)
+  uint4 *s_uval = reinterpret_cast<uint4 *>(s_users);
+  int32_t *s_urow = reinterpret_cast<int32_t *>(s_users + (size_t)Q * nu * 32);
+  if (ULDS) {
+    for (int64_t i = tid; i < Q * nu * 2; i += nt) {
+      const int p = (int)(i & 1);
+      const int64_t qq = (i >> 1) / nu;
+      const int f = (int)((i >> 1) - qq * nu);
+      const int32_t row = resolve_row<HASHED>(a.user_ids, (int64_t)f * Q + qq, f, a.table_rows[f],
+                                              a.table_magic[f], a.err);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (row >= 0) v = reinterpret_cast<const uint4 *>(static_cast<const TS *>(a.tables[f]) + (int64_t)row * EPG)[p];
+      s_uval[i] = v;
+      if (p == 0) s_urow[(int64_t)f * Q + qq] = row;
+    }
+    // request offsets sanity (the pooling pass checks them otherwise)
+    for (int64_t qq = (int64_t)blockIdx.x * nt + tid; qq < Q; qq += (int64_t)gridDim.x * nt) {
+      bool bad = a.req_off[qq + 1] < a.req_off[qq];
+      if (qq == 0) bad |= a.req_off[0] != 0;
+      if (qq == Q - 1) bad |= (int64_t)a.req_off[Q] != R;
+      if (bad) atomicOr(a.err, 2);
+    }
+  }
+  __syncthreads();
+
+  const float inv_d = 1.0f / (float)EPG;             // exact: EPG is a power of two
+  const TS *Uh = static_cast<const TS *>(a.Uh);
+  TS *X = static_cast<TS *>(a.X);
+  const uint64_t dummy = s_tab[0];                   // row 0 of a table: always present
+  const float4 w1v = s_w1[wave * 64 + lane], w2v = s_w2[wave * 64 + lane];
+  const float4 b2v = s_b2[4 * wave + q];
+  const float4 b1v = wave == 0 ? s_b1[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+  const float w1s[4] = {w1v.x, w1v.y, w1v.z, w1v.w}, w2s[4] = {w2v.x, w2v.y, w2v.z, w2v.w};
+
+  const int64_t n_tiles = (R + 15) >> 4;
+  int parity = 0;
+  for (int64_t wt = blockIdx.x; wt < n_tiles; wt += gridDim.x, parity ^= 1) {
+    const int64_t r = wt * 16 + c;
+    const bool row_ok = r < R;
+    const int64_t rr = row_ok ? r : R - 1;           // clamped: loaded, never stored
+    int64_t rq = 0;
+    if (nu > 0 || gpu_cross)
+      rq = req_in_lds ? request_of_row(s_req, Q, rr) : request_of_row(a.req_off, Q, rr);
+
+    // ids of the lane's ad and cross groups, all in flight together
+    id_t idv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int g = 16 * wave + 4 * j + q;
+      idv[j] = 0;
+      if (g >= nu && g < M) {
+        const int f = g - nu;
+        const bool is_ad = f < n_ad;
+        const int fa = is_ad ? f : (gpu_cross ? s_pair[f - n_ad] >> 16 : f - n_ad);
+        const id_t *ids = static_cast<const id_t *>(is_ad || gpu_cross ? a.ad_ids : a.cross_ids);
+        idv[j] = ids[(int64_t)fa * R + rr];
+      }
+    }
+    // table rows and both chunks of every group (loads of absent rows read
+    // row 0 of a table and are zeroed)
+    uint4 raw[4][2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      raw[j][0] = raw[j][1] = make_uint4(0, 0, 0, 0);
+      const int g = 16 * wave + 4 * j + q;
+      uint64_t addr = 0;
+      if (g < M) {
+        if (g < nu) {
+          if (!ULDS) addr = reinterpret_cast<uint64_t>(Uh + (rq * nu + g) * EPG);
+          if (a.rows_out && row_ok)
+            a.rows_out[(int64_t)g * R + r] = ULDS ? s_urow[(int64_t)g * Q + rq] : a.urow[rq * nu + g];
+        } else {
+          int32_t row;
+          const int f = g - nu;
+          if (gpu_cross && f >= n_ad) {
+            // user x ad cross value: key = mix64(user id) ^ ad id, hashed into
+            // the group's table (ids as their unsigned bit patterns)
+            const int fu = s_pair[f - n_ad] & 0xFFFF;
+            const id_t *uids = static_cast<const id_t *>(a.user_ids);
+            uint64_t uid, aid;
+            if constexpr (HASHED) {
+              uid = (uint64_t)uids[(int64_t)fu * Q + rq];
+              aid = (uint64_t)idv[j];
+            } else {
+              uid = (uint64_t)(uint32_t)uids[(int64_t)fu * Q + rq];
+              aid = (uint64_t)(uint32_t)idv[j];
+            }
+            const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+            row = (int32_t)mod_barrett(mix64((mix64(uid) ^ aid) ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+          } else if constexpr (HASHED) {
+            const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+            row = (int32_t)mod_barrett(mix64((uint64_t)idv[j] ^ salt), (uint64_t)s_rows[g], s_magic[g]);
+          } else {
+            row = (int32_t)idv[j];
+            if (row < 0 || row >= s_rows[g]) {
+              atomicOr(a.err, 1);
+              row = -1;
+            }
+          }
+          if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = row;
+          if (row >= 0) addr = s_tab[g] + (uint64_t)row * (EPG * sizeof(TS));
+        }
+      }
+      const uint64_t at = addr ? addr : dummy;
+      const u32x4 v0 = *reinterpret_cast<gl_u32x4 *>(at);
+      const u32x4 v1 = *reinterpret_cast<gl_u32x4 *>(at + 16);
+      if (addr) {
+        raw[j][0] = make_uint4(v0.x, v0.y, v0.z, v0.w);
+        raw[j][1] = make_uint4(v1.x, v1.y, v1.z, v1.w);
+      } else if (ULDS && g < nu) {
+        raw[j][0] = s_uval[(rq * nu + g) * 2];
+        raw[j][1] = s_uval[(rq * nu + g) * 2 + 1];
+      }
+    }
+    // squeeze and this wave's part of layer 1 (wave 0's part starts at b1)
+    f32x4 hp;
+    hp[0] = b1v.x; hp[1] = b1v.y; hp[2] = b1v.z; hp[3] = b1v.w;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float v[EPG];
+      Elem<TS>::unpack(raw[j][0], v);
+      Elem<TS>::unpack(raw[j][1], v + EPC);
+      float zs = 0.0f;
+#pragma unroll
+      for (int e = 0; e < EPG; ++e) zs += v[e];
+      hp = __builtin_amdgcn_mfma_f32_16x16x4f32(w1s[j], zs * inv_d, hp, 0, 0, 0);
+    }
+    s_hp[parity][wave][lane] = make_float4(hp[0], hp[1], hp[2], hp[3]);
+    __syncthreads();   // every wave's part is in; the other parity's buffer is free
+    // h^T = ReLU(the parts in wave order), then layer 2 for block gb = wave
+    f32x4 h;
+    {
+      float4 t = s_hp[parity][0][lane];
+      h[0] = t.x; h[1] = t.y; h[2] = t.z; h[3] = t.w;
+      for (int w = 1; w < GB; ++w) {
+        t = s_hp[parity][w][lane];
+        h[0] += t.x; h[1] += t.y; h[2] += t.z; h[3] += t.w;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = h[e] > 0.0f ? h[e] : 0.0f;
+    f32x4 o;
+    o[0] = b2v.x; o[1] = b2v.y; o[2] = b2v.z; o[3] = b2v.w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o = __builtin_amdgcn_mfma_f32_16x16x4f32(w2s[e], h[e], o, 0, 0, 0);
+    // reweight, linear_log, round once, store the group's two chunks
+    if (row_ok) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int g = 16 * wave + 4 * j + q;
+        if (g < M) {
+          const float sw = 1.0f / (1.0f + expf(-o[j]));
+          float v[EPG], out[EPG];
+          Elem<TS>::unpack(raw[j][0], v);
+          Elem<TS>::unpack(raw[j][1], v + EPC);
+#pragma unroll
+          for (int e = 0; e < EPG; ++e) {
+            const float x = sw * v[e];
+            out[e] = LL ? linear_log(x) : x;
+          }
+          uint4 *dst = reinterpret_cast<uint4 *>(X + (r * M + g) * EPG);
+          dst[0] = Elem<TS>::pack(out);
+          dst[1] = Elem<TS>::pack(out + EPC);
+          if (a.s_buf) a.s_buf[r * M + g] = sw;
+        }
+      }
+    }
+  }
 }
 
+template <typename TS, bool LL, bool ULDS>
+static hipError_t gather_full_split_u(bool hashed, const GatherArgs &a, hipStream_t s) {
+  const void *k = hashed ? reinterpret_cast<const void *>(&gather_full_split_kernel<TS, LL, true, ULDS>)
+                         : reinterpret_cast<const void *>(&gather_full_split_kernel<TS, LL, false, ULDS>);
+  const size_t shmem = ULDS ? (size_t)a.Q * a.n_user * 36 : 0;
+  const int threads = 64 * ((a.M + 15) / 16);
+  int per_cu = 0, dev = 0, cus = device_cus();
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, shmem) != hipSuccess)
+    per_cu = 0;
+  int64_t nb = (a.R + 15) / 16;
+  if (per_cu > 0 && cus > 0 && nb > (int64_t)per_cu * cus) nb = (int64_t)per_cu * cus;
+  if (hashed)
+    hipLaunchKernelGGL((gather_full_split_kernel<TS, LL, true, ULDS>), dim3((unsigned)nb), dim3(threads), shmem, s, a);
+  else
+    hipLaunchKernelGGL((gather_full_split_kernel<TS, LL, false, ULDS>), dim3((unsigned)nb), dim3(threads), shmem, s, a);
+  return hipGetLastError();
+}
+
+// users' rows in LDS when the pooling pass does not run; up to 48 groups
+// one wave per tile, above that one wave per 16 groups
 template <typename TS, bool LL>
 static hipError_t gather_full_t(bool hashed, const GatherArgs &a, hipStream_t s) {
-  return gather_full_ns<TS, LL, kFullMaxM / 4>(hashed, a, s);
+  const bool pool = user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a);
+  if (a.M <= kFullTileM)
+    return pool ? gather_full_u<TS, LL, kFullTileM / 4, false>(hashed, a, s)
+                : gather_full_u<TS, LL, kFullTileM / 4, true>(hashed, a, s);
+  return pool ? gather_full_split_u<TS, LL, false>(hashed, a, s)
+              : gather_full_split_u<TS, LL, true>(hashed, a, s);
 }
 
 hipError_t launch_gather_full(int dtype, bool linear_log, bool hashed, const GatherArgs &a,
