@@ -170,6 +170,24 @@ def latency(model, dev_batch, scores, iters, torch, graph):
     return float(np.median(t)), float(np.quantile(t, 0.99))
 
 
+def launch_sync_floor(torch, dev, iters):
+    """p50 host time of launching one trivial kernel (a one-element add) on
+    the current stream and synchronising it: the part of a request's latency
+    that no kernel work can remove."""
+    stream = torch.cuda.current_stream()
+    t = torch.zeros(1, device=dev)
+    for _ in range(10):
+        t.add_(1)
+    stream.synchronize()
+    times = []
+    for _ in range(iters):
+        t0 = time.perf_counter()
+        t.add_(1)
+        stream.synchronize()
+        times.append(time.perf_counter() - t0)
+    return float(np.median(np.array(times) * 1e3))
+
+
 def serving_curve(model, batch, cfg, streams, iters, torch, binding):
     """Concurrent serving of single requests: K streams, each replaying a HIP
     graph of one request's cold_score call back to back with its own
@@ -864,7 +882,7 @@ def main():
     m_flops = sum(e["work_per_launch"] for e in stage_rows if e["bound"] == "mfma")
 
     p50 = p99 = g50 = g99 = None
-    lat_stages = None
+    lat_stages = floor = None
     if not args.no_latency:
         lat_np = request_slice(batch, 0, cfg)
         lat_dev = binding.batch_to_device(lat_np, dev)
@@ -883,6 +901,8 @@ def main():
         except Exception as exc:  # graph capture is an optional measurement
             log(f"graph replay unavailable: {exc}")
         log(f"2,000-ad request latency p50 {p50:.4f} ms (graph {g50}), p99 {p99:.4f} ms")
+        floor = launch_sync_floor(torch, dev, args.latency_iters)
+        log(f"host floor: one trivial kernel launched and synchronised, p50 {floor:.4f} ms")
 
     if args.no_latency:
         args.batching, args.serving_streams, args.topn, args.groups_sweep = "", "", 0, ""
@@ -965,6 +985,7 @@ def main():
         "p50_latency_ms": None if p50 is None else round(p50, 4),
         "p99_latency_ms": None if p99 is None else round(p99, 4),
         "p50_latency_graph_ms": None if g50 is None else round(g50, 4),
+        "launch_sync_floor_ms": None if floor is None else round(floor, 4),
         "latency_stages_us": lat_stages,
         "p99_latency_graph_ms": None if g99 is None else round(g99, 4),
         "roofline": roofline,

@@ -79,3 +79,35 @@ def test_trace_split_handles_demangled_names(tmp_path):
     assert int(lines["se_weights"][1]) == 2
     assert int(lines["group_mask"][1]) == 4      # two kernels per call
     assert float(lines["dense_tail"][2]) == 0.5  # mean duration in us
+
+
+def test_trace_split_of_the_topk_rows_path_and_register_gather(tmp_path):
+    """The wide workload's passes (gather with squeeze, row-wise SE, one mask
+    kernel, reweighting) and the register-resident gathers of the other
+    workloads map to their stage names, one call each."""
+    wide = ["_ZN4cold16gather_se_kernelIDF16bLi4ELb0ELb0ELi8ELb0EEEvNS_10GatherArgsE",
+            "void cold::se_rows_kernel<16>(float const*, float*, long, int, int, "
+            "HIP_vector_type<float, 4u> const*, float const*, HIP_vector_type<float, 4u> const*, "
+            "float const*, float*)",
+            "cold::mask_select_tiles_kernel(float const*, float const*, int const*, long, int, int, "
+            "unsigned char*, unsigned char*)",
+            "_ZN4cold20apply_weights_kernelIDF16bLb0EEEvPT_PKfPKhPKilliiij",
+            MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    serving = ["_ZN4cold16user_pool_kernelIDF16bLb0EEEvNS_10GatherArgsE",
+               "_ZN4cold18gather_full_kernelIDF16bLb0ELb0ELi12ELb0EEEvNS_10GatherArgsE",
+               MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    large = ["_ZN4cold16user_pool_kernelIDF16_Lb1EEEvNS_10GatherArgsE",
+             "_ZN4cold24gather_full_split_kernelIDF16_Lb1ELb1ELb0EEEvNS_10GatherArgsE",
+             MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    for calls, want in [
+            ([wide, wide], ["gather_sq", "se_rows", "group_mask", "apply", "dense0", "dense1",
+                            "dense_tail"]),
+            ([serving, serving], ["user_pool", "gather_se", "dense0", "dense1", "dense_tail"]),
+            ([large], ["user_pool", "gather_se", "dense0", "dense1", "dense_tail"])]:
+        d = tmp_path / want[1] / str(len(calls))
+        d.mkdir(parents=True)
+        _write_trace(os.path.join(d, "bench_kernel_trace.csv"), calls)
+        rows = list(csv.DictReader(open(os.path.join(d, "bench_kernel_trace.csv"))))
+        assert [st for st, _ in bench._last_call(rows)] == want
+        text = bench.summarize_trace(str(d), "cmd")
+        assert f"# {len(calls)} calls profiled" in text
