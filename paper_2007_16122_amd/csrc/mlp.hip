@@ -847,21 +847,64 @@ __global__ __launch_bounds__(128 * WN, MINB) void dense_tail_kernel(
     __syncthreads();
     tail_store_ext<TS, 2, JB>(a1, b1, s_h1, S1, PR * S1, 2 * (wave % 4), (wave / 4) * JB, lane);
     __syncthreads();
-    // second tail layer (wave w: feature block w % 4 over its row group),
-    // output in fp32 after the first layer's
+    // second tail layer (wave w: feature block fb = w % 4 over its row
+    // group), bias and ReLU in fp32, and the head's sums over the block's 16
+    // features straight from the accumulators: lane (c, q) holds features
+    // 16 fb + 4 q + e of row c; its four products are added in e order, the
+    // four quarters by two shuffles; the feature blocks' sums meet in LDS
     auto in1 = [&](int row, int c) { return s_h1 + row * S1 + c * 8; };
     f32x4 a2[1][JB];
     tail_mma<TS, KS2, 1, JB, true>(in1, PR * S1 * 2, w2f, (wave / 4) * JB, lane, a2);
-    tail_store_f32<1, JB>(a2, b2, s_h2, S2, wave % 4, (wave / 4) * JB, lane);
+    {
+      const int fb = wave % 4, q4 = lane >> 4;
+      float wz0[4], wz1[4], bb[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int k = 16 * fb + 4 * q4 + e;
+        wz0[e] = s_wh[k];
+        wz1[e] = n_out > 1 ? s_wh[N2 + k] : 0.0f;
+        bb[e] = b2[k];
+      }
+#pragma unroll
+      for (int j = 0; j < JB; ++j) {
+        float z0 = 0.0f, z1 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float v = a2[0][j][e] + bb[e];
+          v = v > 0.0f ? v : 0.0f;
+          z0 += wz0[e] * v;
+          z1 += wz1[e] * v;
+        }
+        z0 += __shfl_xor(z0, 16);
+        z0 += __shfl_xor(z0, 32);
+        z1 += __shfl_xor(z1, 16);
+        z1 += __shfl_xor(z1, 32);
+        if (q4 == 0) {
+          const int lr = ((wave / 4) * JB + j) * 16 + dr;
+          s_h2[(fb * PR + lr) * 2] = z0;
+          s_h2[(fb * PR + lr) * 2 + 1] = z1;
+        }
+      }
+    }
     __syncthreads();
-    // head: LDS row lr of the pass is row (lr / (PR/2)) * (BR/2) + p * (PR/2)
-    // + lr % (PR/2) of the tile
-    if (tid < PR * 4)
-      tail_head<N2>(s_h2, S2, s_wh, s_bh, n_out, scores,
-                    [&](int lr) {
-                      return r0 + (lr / (PR / 2)) * (BR / 2) + p * (PR / 2) + lr % (PR / 2);
-                    },
-                    R, tid);
+    // head: the four blocks' sums in block order, then the bias; LDS row lr
+    // of the pass is row (lr / (PR/2)) * (BR/2) + p * (PR/2) + lr % (PR/2) of
+    // the tile
+    if (tid < PR) {
+      const int lr = tid;
+      float z0 = s_h2[lr * 2], z1 = s_h2[lr * 2 + 1];
+#pragma unroll
+      for (int fb = 1; fb < 4; ++fb) {
+        z0 += s_h2[(fb * PR + lr) * 2];
+        z1 += s_h2[(fb * PR + lr) * 2 + 1];
+      }
+      const int64_t r = r0 + (lr / (PR / 2)) * (BR / 2) + p * (PR / 2) + lr % (PR / 2);
+      if (r < R) {
+        z0 += s_bh[0];
+        if (n_out > 1) z1 += s_bh[1];
+        scores[r] = n_out == 1 ? 1.0f / (1.0f + expf(-z0)) : 1.0f / (1.0f + expf(z0 - z1));
+      }
+    }
     if (p + 1 < NP) __syncthreads();   // the next pass overwrites the tail's tiles
   }
 }
