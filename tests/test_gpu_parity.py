@@ -232,15 +232,17 @@ REGISTER_GATHER_CANDS = [1500] * 5 + [700, 0, 1, 257]   # 8,458 rows, 9 requests
 @pytest.mark.parametrize("kw", [dict(hashed=True), dict(hashed=True, cross="gpu"),
                                 dict(linear_log=True), dict(dtype="f16", linear_log=True),
                                 dict(dtype="f16", hashed=True, linear_log=True, cross="gpu"),
-                                dict(n_ad=20, n_cross=10), dict(n_user=30, n_ad=12, n_cross=6)])
+                                dict(n_ad=20, n_cross=10), dict(n_user=30, n_ad=12, n_cross=6),
+                                dict(n_ad=32), dict(n_ad=32, hashed=True, cross="gpu")])
 def test_parity_register_gather_variants(kw):
     """The register-resident gather (up to 48 groups, no sequences) in its
     other forms, on a batch of more tiles than one round of workgroups: hashed ids,
     GPU-built crosses, linear_log, fp16 storage, fewer groups (42: the last
-    slot of half the lanes empty) and 30 user fields over 9 requests (user
-    rows in the pooling pass's buffer instead of LDS); gather indices
-    bit-exact, SE weights and scores against the checker on a seeded sample
-    of rows (every request's first and last row included)."""
+    slot of half the lanes empty), 30 user fields over 9 requests (user
+    rows in the pooling pass's buffer instead of LDS) and 56 groups (the
+    form with one wave per 16 groups, its last wave half empty); gather
+    indices bit-exact, SE weights and scores against the checker on a
+    seeded sample of rows (every request's first and last row included)."""
     kw = dict(kw)
     base = synth.CONFIGS["serving_bf16"]
     if kw.pop("cross", None) == "gpu":
