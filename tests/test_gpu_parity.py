@@ -398,20 +398,23 @@ def test_parity_topk_group_counts(fields, k):
     compare_scores(cfg, g["scores"], o["scores"], f"top-k M={cfg.n_groups}")
 
 
-@pytest.mark.parametrize("widths,n_req", [((768, 384, 320, 256, 128, 64, 2), 12),
-                                          ((768, 1024, 512, 256, 128, 64, 2), 3),
-                                          ((768, 1024, 544, 256, 128, 64, 2), 3),
-                                          ((768, 1024, 544, 256, 128, 64, 2), 36)])
-def test_parity_layer_tile_shapes(widths, n_req):
+@pytest.mark.parametrize("widths,n_req,cand", [((768, 384, 320, 256, 128, 64, 2), 12, 1993),
+                                               ((768, 1024, 512, 256, 128, 64, 2), 2, 1993),
+                                               ((768, 1024, 512, 256, 128, 64, 2), 5, 911),
+                                               ((768, 1024, 512, 256, 128, 64, 2), 3, 1993),
+                                               ((768, 1024, 544, 256, 128, 64, 2), 3, 1993),
+                                               ((768, 1024, 544, 256, 128, 64, 2), 36, 1993)])
+def test_parity_layer_tile_shapes(widths, n_req, cand):
     """The dense layer's other tile shapes: hidden widths that are multiples
     of 128 but not 256 (384: 256 x 128 tiles) and of 64 but not 128 (320:
-    256 x 64 tiles) on a batch large enough for 256-row tiles, and a
-    6,000-row batch of the serving widths (128 x 128 tiles for the
-    1,024-wide layer, 64-row tiles of the fused last layers). A 544-wide
-    layer (256 x 64 tiles; 32-deep K steps into the 256-wide layer) keeps
-    the tail in its own kernel: two workgroups per CU on 6,000 rows, three
-    on 72,000. Ragged last row tiles; checker on a seeded sample of rows."""
-    cfg = mid("serving_bf16", widths=widths, n_requests=n_req, cand_per_request=2000 - 7)
+    256 x 64 tiles) on a batch large enough for 256-row tiles; batches of
+    the serving widths with 3,986, 4,555 and 5,979 rows (128, 160 and 192 x
+    128 tiles for the 1,024-wide layer, 64-row tiles of the fused last
+    layers). A 544-wide layer (256 x 64 tiles; 32-deep K steps into the
+    256-wide layer) keeps the tail in its own kernel: two workgroups per CU
+    on 6,000 rows, three on 72,000. Ragged last row tiles; checker on a
+    seeded sample of rows."""
+    cfg = mid("serving_bf16", widths=widths, n_requests=n_req, cand_per_request=cand)
     log(f"test_parity_layer_tile_shapes widths={widths} R={cfg.n_rows}")
     tables, params, batch = problem(cfg, seed=29, model_seed=cfg.seed)
     run = load(cfg, tables, params)
