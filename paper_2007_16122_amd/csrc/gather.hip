@@ -1341,14 +1341,292 @@ static hipError_t gather_full_split_u(bool hashed, const GatherArgs &a, hipStrea
   return hipGetLastError();
 }
 
+// Batches of few tiles, up to 48 groups: the one-wave form's arithmetic on
+// one wave per 16 groups of a tile (wave w: slots 4 w .. 4 w + 3, groups
+// 16 w + 4 j + q), so that a tile's gather, squeeze, reweighting and stores
+// spread over GB = ceil(M / 16) waves. Layer 1's MFMA steps keep the one-wave
+// order: wave w takes steps 4 w .. 4 w + 3 on the running sums that wave
+// w - 1 left in LDS (wave 0 starts from b1), and the last wave's sums are
+// every wave's h; layer 2's block w and the weights of the wave's slots are
+// then the one-wave form's, bit for bit. Each wave keeps its groups' table
+// pointers and SE operands in registers, and the first tile's ids and rows
+// are fetched before the workgroup's set-up barrier, so their latency
+// overlaps the users' resolution.
+template <typename TS, bool LL, bool HASHED, bool ULDS>
+__global__ __launch_bounds__(64 * (kFullTileM / 16)) void gather_full_chain_kernel(GatherArgs a) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const u32x4 gl_u32x4;
+  typedef typename std::conditional<HASHED, uint64_t, int32_t>::type id_t;
+  constexpr int EPC = Elem<TS>::kPerChunk;   // elements per 16-byte chunk
+  constexpr int EPG = 2 * EPC;               // elements per group (d)
+  __shared__ int32_t s_pair[kFullMaxM];
+  __shared__ int32_t s_req[kGatherMaxReqLds + 1];
+  __shared__ float4 s_h[2][kFullTileM / 16][64];   // layer-1 sums after wave w's steps, by tile parity
+  extern __shared__ __align__(16) unsigned char s_users[];   // [Q][nu][2] chunks, then [nu][Q] rows
+  const int M = a.M, H = a.H, nu = a.n_user, n_ad = a.n_ad;
+  const int64_t R = a.R, Q = a.Q;
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nt = blockDim.x, GB = nt >> 6;   // one wave per 16 groups
+  const bool gpu_cross = a.cross_pairs != nullptr;
+  const int64_t n_tiles = (R + 15) >> 4;
+  const float inv_d = 1.0f / (float)EPG;     // exact: EPG is a power of two
+  const TS *Uh = static_cast<const TS *>(a.Uh);
+  TS *X = static_cast<TS *>(a.X);
+  uint4 *s_uval = reinterpret_cast<uint4 *>(s_users);
+  int32_t *s_urow = reinterpret_cast<int32_t *>(s_users + (size_t)Q * nu * 32);
+
+  // this lane's groups: table, row count and divisor magic
+  const uint64_t dummy = reinterpret_cast<uint64_t>(a.tables[0]);   // row 0 of a table: always present
+  uint64_t tab[4], magic[4];
+  int32_t nrows[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int g = 16 * wave + 4 * j + q;
+    const int gg = g < M ? g : 0;
+    tab[j] = reinterpret_cast<uint64_t>(a.tables[gg]);
+    magic[j] = a.table_magic[gg];
+    nrows[j] = (int32_t)a.table_rows[gg];
+  }
+  // the wave's SE operands: b1[4 q + e]; W1, W2 and b2 of block gb = wave
+  const float4 w1v = reinterpret_cast<const float4 *>(a.w1f)[wave * 64 + lane];
+  const float4 w2v = reinterpret_cast<const float4 *>(a.w2f)[wave * 64 + lane];
+  const float w1s[4] = {w1v.x, w1v.y, w1v.z, w1v.w}, w2s[4] = {w2v.x, w2v.y, w2v.z, w2v.w};
+  float b1v[4], b2v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    b1v[e] = 4 * q + e < H ? a.b1[4 * q + e] : 0.0f;
+    const int g2 = 16 * wave + 4 * e + q;
+    b2v[e] = g2 < M ? a.b2[g2] : 0.0f;
+  }
+
+  // ids, table rows and both chunks of the tile's ad and cross groups (and
+  // of the user groups from the pooling pass); loads of absent rows read row
+  // 0 of a table and are zeroed
+  id_t idv[4];
+  uint4 raw[4][2];
+  auto fetch = [&](int64_t wt, int64_t rq) {
+    const int64_t r = wt * 16 + c;
+    const bool row_ok = r < R;
+    const int64_t rr = row_ok ? r : R - 1;   // clamped: loaded, never stored
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int g = 16 * wave + 4 * j + q;
+      idv[j] = 0;
+      if (g >= nu && g < M) {
+        const int f = g - nu;
+        const bool is_ad = f < n_ad;
+        const int fa = is_ad ? f : (gpu_cross ? s_pair[f - n_ad] >> 16 : f - n_ad);
+        const id_t *ids = static_cast<const id_t *>(is_ad || gpu_cross ? a.ad_ids : a.cross_ids);
+        idv[j] = ids[(int64_t)fa * R + rr];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      raw[j][0] = raw[j][1] = make_uint4(0, 0, 0, 0);
+      const int g = 16 * wave + 4 * j + q;
+      uint64_t addr = 0;
+      if (g < M) {
+        if (g < nu) {
+          if (!ULDS) {
+            addr = reinterpret_cast<uint64_t>(Uh + (rq * nu + g) * EPG);
+            if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = a.urow[rq * nu + g];
+          }
+        } else {
+          int32_t row;
+          const int f = g - nu;
+          if (gpu_cross && f >= n_ad) {
+            // user x ad cross value: key = mix64(user id) ^ ad id, hashed into
+            // the group's table (ids as their unsigned bit patterns)
+            const int fu = s_pair[f - n_ad] & 0xFFFF;
+            const id_t *uids = static_cast<const id_t *>(a.user_ids);
+            uint64_t uid, aid;
+            if constexpr (HASHED) {
+              uid = (uint64_t)uids[(int64_t)fu * Q + rq];
+              aid = (uint64_t)idv[j];
+            } else {
+              uid = (uint64_t)(uint32_t)uids[(int64_t)fu * Q + rq];
+              aid = (uint64_t)(uint32_t)idv[j];
+            }
+            const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+            row = (int32_t)mod_barrett(mix64((mix64(uid) ^ aid) ^ salt), (uint64_t)nrows[j], magic[j]);
+          } else if constexpr (HASHED) {
+            const uint64_t salt = (uint64_t)(g + 1) * 0x9e3779b97f4a7c15ull;
+            row = (int32_t)mod_barrett(mix64((uint64_t)idv[j] ^ salt), (uint64_t)nrows[j], magic[j]);
+          } else {
+            row = (int32_t)idv[j];
+            if (row < 0 || row >= nrows[j]) {
+              atomicOr(a.err, 1);
+              row = -1;
+            }
+          }
+          if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = row;
+          if (row >= 0) addr = tab[j] + (uint64_t)row * (EPG * sizeof(TS));
+        }
+      }
+      if (g < M && (g >= nu || !ULDS)) {
+        const uint64_t at = addr ? addr : dummy;
+        const u32x4 v0 = *reinterpret_cast<gl_u32x4 *>(at);
+        const u32x4 v1 = *reinterpret_cast<gl_u32x4 *>(at + 16);
+        if (addr) {
+          raw[j][0] = make_uint4(v0.x, v0.y, v0.z, v0.w);
+          raw[j][1] = make_uint4(v1.x, v1.y, v1.z, v1.w);
+        }
+      }
+    }
+  };
+
+  // the first tile's fetch needs no LDS unless user rows or cross pairs enter
+  // it (request of a row from the LDS offsets)
+  const bool hoist = !gpu_cross && (ULDS || nu == 0);
+  int64_t wt = blockIdx.x;
+  if (hoist && wt < n_tiles) fetch(wt, 0);
+
+  if (gpu_cross)
+    for (int f = tid; f < a.n_cross; f += nt) s_pair[f] = a.cross_pairs[2 * f] | (a.cross_pairs[2 * f + 1] << 16);
+  const bool req_in_lds = Q <= kGatherMaxReqLds;
+  if (req_in_lds)
+    for (int64_t i = tid; i <= Q; i += nt) s_req[i] = a.req_off[i];
+  // few requests: their users' rows resolved and staged here (no pooling pass)
+  if (ULDS) {
+    for (int64_t i = tid; i < Q * nu * 2; i += nt) {
+      const int p = (int)(i & 1);
+      const int64_t qq = (i >> 1) / nu;
+      const int f = (int)((i >> 1) - qq * nu);
+      const int32_t row = resolve_row<HASHED>(a.user_ids, (int64_t)f * Q + qq, f, a.table_rows[f],
+                                              a.table_magic[f], a.err);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (row >= 0) v = reinterpret_cast<const uint4 *>(static_cast<const TS *>(a.tables[f]) + (int64_t)row * EPG)[p];
+      s_uval[i] = v;
+      if (p == 0) s_urow[(int64_t)f * Q + qq] = row;
+    }
+    // request offsets sanity (the pooling pass checks them otherwise)
+    for (int64_t qq = (int64_t)blockIdx.x * nt + tid; qq < Q; qq += (int64_t)gridDim.x * nt) {
+      bool bad = a.req_off[qq + 1] < a.req_off[qq];
+      if (qq == 0) bad |= a.req_off[0] != 0;
+      if (qq == Q - 1) bad |= (int64_t)a.req_off[Q] != R;
+      if (bad) atomicOr(a.err, 2);
+    }
+  }
+  __syncthreads();
+
+  int parity = 0;
+  for (bool first = true; wt < n_tiles; wt += gridDim.x, parity ^= 1, first = false) {
+    const int64_t r = wt * 16 + c;
+    const bool row_ok = r < R;
+    const int64_t rr = row_ok ? r : R - 1;
+    int64_t rq = 0;
+    if (nu > 0 || gpu_cross)
+      rq = req_in_lds ? request_of_row(s_req, Q, rr) : request_of_row(a.req_off, Q, rr);
+    if (!(hoist && first)) fetch(wt, rq);
+    if (ULDS) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int g = 16 * wave + 4 * j + q;
+        if (g < nu) {
+          raw[j][0] = s_uval[(rq * nu + g) * 2];
+          raw[j][1] = s_uval[(rq * nu + g) * 2 + 1];
+          if (a.rows_out && row_ok) a.rows_out[(int64_t)g * R + r] = s_urow[(int64_t)g * Q + rq];
+        }
+      }
+    }
+    // squeeze of the wave's slots
+    float zs[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float v[EPG];
+      Elem<TS>::unpack(raw[j][0], v);
+      Elem<TS>::unpack(raw[j][1], v + EPC);
+      float t = 0.0f;
+#pragma unroll
+      for (int e = 0; e < EPG; ++e) t += v[e];
+      zs[j] = t;
+    }
+    // layer 1 in the one-wave step order, handed from wave to wave
+    for (int t = 0; t < GB; ++t) {
+      if (wave == t) {
+        f32x4 hp;
+        if (t == 0) {
+          hp[0] = b1v[0]; hp[1] = b1v[1]; hp[2] = b1v[2]; hp[3] = b1v[3];
+        } else {
+          const float4 v = s_h[parity][t - 1][lane];
+          hp[0] = v.x; hp[1] = v.y; hp[2] = v.z; hp[3] = v.w;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) hp = __builtin_amdgcn_mfma_f32_16x16x4f32(w1s[j], zs[j] * inv_d, hp, 0, 0, 0);
+        s_h[parity][t][lane] = make_float4(hp[0], hp[1], hp[2], hp[3]);
+      }
+      __syncthreads();
+    }
+    f32x4 h;
+    {
+      const float4 v = s_h[parity][GB - 1][lane];
+      h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = h[e] > 0.0f ? h[e] : 0.0f;
+    // layer 2, block gb = wave: the weight of slot 4 gb + e in element e
+    f32x4 o;
+    o[0] = b2v[0]; o[1] = b2v[1]; o[2] = b2v[2]; o[3] = b2v[3];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o = __builtin_amdgcn_mfma_f32_16x16x4f32(w2s[e], h[e], o, 0, 0, 0);
+    // reweight, linear_log, round once, store the group's two chunks
+    if (row_ok) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int g = 16 * wave + 4 * j + q;
+        if (g < M) {
+          const float sw = 1.0f / (1.0f + expf(-o[j]));
+          float v[EPG], out[EPG];
+          Elem<TS>::unpack(raw[j][0], v);
+          Elem<TS>::unpack(raw[j][1], v + EPC);
+#pragma unroll
+          for (int e = 0; e < EPG; ++e) {
+            const float x = sw * v[e];
+            out[e] = LL ? linear_log(x) : x;
+          }
+          uint4 *dst = reinterpret_cast<uint4 *>(X + (r * M + g) * EPG);
+          dst[0] = Elem<TS>::pack(out);
+          dst[1] = Elem<TS>::pack(out + EPC);
+          if (a.s_buf) a.s_buf[r * M + g] = sw;
+        }
+      }
+    }
+  }
+}
+
+template <typename TS, bool LL, bool ULDS>
+static hipError_t gather_full_chain_u(bool hashed, const GatherArgs &a, hipStream_t s) {
+  const size_t shmem = ULDS ? (size_t)a.Q * a.n_user * 36 : 0;
+  const int threads = 64 * ((a.M + 15) / 16);
+  const int64_t nb = (a.R + 15) / 16;   // one tile per workgroup (few tiles)
+  if (hashed)
+    hipLaunchKernelGGL((gather_full_chain_kernel<TS, LL, true, ULDS>), dim3((unsigned)nb), dim3(threads), shmem, s, a);
+  else
+    hipLaunchKernelGGL((gather_full_chain_kernel<TS, LL, false, ULDS>), dim3((unsigned)nb), dim3(threads), shmem, s, a);
+  return hipGetLastError();
+}
+
+// batches of at most two 16-row tiles per CU take the chained form (the
+// one-wave form at 1,000 tiles and more)
+static bool gather_full_chained(int64_t R) {
+  const int cus = device_cus() > 0 ? device_cus() : 256;
+  return (R + 15) / 16 <= 2 * (int64_t)cus;
+}
+
 // users' rows in LDS when the pooling pass does not run; up to 48 groups
-// one wave per tile, above that one wave per 16 groups
+// one wave per tile (the chained form of it for few tiles), above that one
+// wave per 16 groups
 template <typename TS, bool LL>
 static hipError_t gather_full_t(bool hashed, const GatherArgs &a, hipStream_t s) {
   const bool pool = user_pool_needed(std::is_same<TS, float>::value ? kF32 : kBF16, a);
-  if (a.M <= kFullTileM)
+  if (a.M <= kFullTileM) {
+    if (gather_full_chained(a.R))
+      return pool ? gather_full_chain_u<TS, LL, false>(hashed, a, s)
+                  : gather_full_chain_u<TS, LL, true>(hashed, a, s);
     return pool ? gather_full_u<TS, LL, kFullTileM / 4, false>(hashed, a, s)
                 : gather_full_u<TS, LL, kFullTileM / 4, true>(hashed, a, s);
+  }
   return pool ? gather_full_split_u<TS, LL, false>(hashed, a, s)
               : gather_full_split_u<TS, LL, true>(hashed, a, s);
 }

@@ -264,7 +264,7 @@ template <int BR, int BN, int S, int WN, int KB = 32> struct BufTile {
   static_assert((BN + BR) % (RPI * NW) == 0, "loads must split evenly over the waves");
   static_assert(BN % (16 * WN) == 0 && BR % 32 == 0 && BN % RPI == 0, "tile shape");
   static_assert(S >= 2 && S <= 4, "stages");
-  static_assert(RJ >= 2, "the K loop's read schedule runs two row blocks ahead");
+  static_assert(RJ >= 1, "row blocks");
 };
 
 // The K loop of one tile: acc[i][j] = bias + W X^T over K for the
@@ -369,16 +369,18 @@ __device__ __forceinline__ void buf_tile_kloop(
           for (int j = 0; j < RJ; ++j)
 #pragma unroll
             for (int i = 0; i < NI; ++i) acc[i][j] = Mfma<TS>::mac(fa[i], fb[j], acc[i][j]);
-          // issue order: the A fragments and two B fragments, then one B
-          // fragment read after each row block's NI MFMAs, so that a read is
-          // two blocks ahead of the MFMAs that use it
-          __builtin_amdgcn_sched_group_barrier(0x100, NI + 2, 0);   // DS reads
+          // issue order: the A fragments and two B fragments (one with a
+          // single row block), then one B fragment read after each row
+          // block's NI MFMAs, so that a read is two blocks ahead of the
+          // MFMAs that use it
+          constexpr int AHEAD = RJ < 2 ? RJ : 2;
+          __builtin_amdgcn_sched_group_barrier(0x100, NI + AHEAD, 0);   // DS reads
 #pragma unroll
-          for (int j = 0; j < RJ - 2; ++j) {
-            __builtin_amdgcn_sched_group_barrier(0x008, NI, 0);     // MFMAs
+          for (int j = 0; j < RJ - AHEAD; ++j) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NI, 0);         // MFMAs
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NI, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, AHEAD * NI, 0);
         }
       }
     }
@@ -1132,9 +1134,16 @@ static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, vo
     if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
       return k64 ? dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
                  : dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    if (big_tiles < 256)
+    if (big_tiles < 256) {
+      // at most two tiles per CU: a third 64-deep stage in flight (the K
+      // steps wait on load latency, not on the CU's throughput); more tiles
+      // than that run better with the smaller ring, more workgroups per CU
+      const int64_t cus = device_cus() > 0 ? device_cus() : 256;
+      const int64_t small_tiles = ((R + 63) / 64) * ((N + 63) / 64);
+      if (k64 && small_tiles <= 2 * cus) return dense_buf_t<TS, 64, 64, 3, 2, 2, 64>(x, w, b, y, R, N, K, s);
       return k64 ? dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
                  : dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
+    }
     if (N % 256 == 0 && k64) return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s);
     if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
     if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
@@ -1207,17 +1216,21 @@ hipError_t launch_dense_tail(int dtype, const void *x, const void *w, const floa
   // 128-row tiles over 4 waves in 72 KB of LDS, two workgroups per CU, so
   // that one's tail phase overlaps the other's K loop (the large workload,
   // 1.28 M rows: 720 -> 650 us; at 64,000 rows, one round, 40 -> 42 us);
-  // 64-row tiles for smaller batches. Every variant sums in the same order.
+  // 64-row tiles for smaller batches, and 32-row tiles over 4 waves when
+  // 64-row tiles would leave CUs idle. Every variant sums in the same order.
   const bool big = ((R + 255) / 256) * 2 >= 256;
   const int cus = device_cus() > 0 ? device_cus() : 256;
   const bool rounds = (R + 127) / 128 >= 8 * (int64_t)cus;
+  const bool few = (R + 63) / 64 < cus;
   if (dtype == kBF16) {
     if (big && rounds) launch_dense_tail_t<__bf16, 128, 2, 2, 32, 3>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else if (big) launch_dense_tail_t<__bf16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else if (few) launch_dense_tail_t<__bf16, 32, 2, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else launch_dense_tail_t<__bf16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   } else {
     if (big && rounds) launch_dense_tail_t<_Float16, 128, 2, 2, 32, 3>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else if (big) launch_dense_tail_t<_Float16, 256, 1>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
+    else if (few) launch_dense_tail_t<_Float16, 32, 2, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
     else launch_dense_tail_t<_Float16, 64, 2>(x, w, b, K, w1, b1, w2, b2, wh, bh, n_out, scores, R, s);
   }
   return hipGetLastError();

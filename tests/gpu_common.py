@@ -149,19 +149,22 @@ def compare_scores(cfg, got, want, label=""):
     return stats
 
 
-def request_slice(cfg, batch, q):
-    """Request q of a host batch as a batch of its own."""
+def request_slice(cfg, batch, q, q_end=None):
+    """Requests q .. q_end - 1 (default: request q alone) of a host batch as
+    a batch of their own."""
+    q_end = q + 1 if q_end is None else q_end
     off = batch["req_off"]
-    lo, hi = int(off[q]), int(off[q + 1])
+    lo, hi = int(off[q]), int(off[q_end])
     Q = len(off) - 1
-    out = dict(req_off=np.array([0, hi - lo], np.int32),
-               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q + 1]),
+    out = dict(req_off=(off[q:q_end + 1] - lo).astype(np.int32),
+               user_ids=np.ascontiguousarray(batch["user_ids"][:, q:q_end]),
                ad_ids=np.ascontiguousarray(batch["ad_ids"][:, lo:hi]),
                cross_ids=np.ascontiguousarray(batch["cross_ids"][:, lo:hi]),
-               n_rows=hi - lo, n_requests=1)
+               n_rows=hi - lo, n_requests=q_end - q)
     if cfg.n_seq:
         so = batch["seq_off"]
-        segs = [batch["seq_ids"][so[f * Q + q]:so[f * Q + q + 1]] for f in range(cfg.n_seq)]
+        segs = [batch["seq_ids"][so[f * Q + qq]:so[f * Q + qq + 1]]
+                for f in range(cfg.n_seq) for qq in range(q, q_end)]
         out["seq_off"] = np.concatenate([[0], np.cumsum([len(x) for x in segs])]).astype(np.int32)
         out["seq_ids"] = np.concatenate(segs)
     else:

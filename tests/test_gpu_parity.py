@@ -242,7 +242,12 @@ def test_parity_register_gather_variants(kw):
     rows in the pooling pass's buffer instead of LDS) and 56 groups (the
     form with one wave per 16 groups, its last wave half empty); gather
     indices bit-exact, SE weights and scores against the checker on a
-    seeded sample of rows (every request's first and last row included)."""
+    seeded sample of rows (every request's first and last row included).
+    Parts of the batch scored on their own (1,500 rows of one request; 2,458
+    rows of five requests, whose user rows overflow the LDS when there are
+    30 user fields) take the small-batch form of the same arithmetic (one
+    wave per 16 groups, layer 1's steps handed from wave to wave), and give
+    bit-identical rows, SE weights and scores."""
     kw = dict(kw)
     base = synth.CONFIGS["serving_bf16"]
     if kw.pop("cross", None) == "gpu":
@@ -252,12 +257,22 @@ def test_parity_register_gather_variants(kw):
     log(f"test_parity_register_gather_variants {kw}: M={cfg.n_groups}")
     tables, params, batch = problem(cfg, seed=47, cand=REGISTER_GATHER_CANDS, model_seed=cfg.seed)
     run = load(cfg, tables, params)
+    parts = [(0, 1), (4, 9)]
     try:
         g = run.score(batch, want_rows=True, want_s=True)
+        alone = [run.score(request_slice(cfg, batch, lo, hi), want_rows=True, want_s=True)
+                 for lo, hi in parts]
     finally:
         run.close()
-    rng = np.random.default_rng(53)
     off = batch["req_off"]
+    for (lo, hi), a in zip(parts, alone):
+        r0, r1 = int(off[lo]), int(off[hi])
+        assert np.array_equal(a["rows"], g["rows"][:, r0:r1]), f"requests {lo}..{hi - 1}: rows"
+        assert np.array_equal(a["s"].view(np.uint32), g["s"][r0:r1].view(np.uint32)), \
+            f"requests {lo}..{hi - 1}: SE weights"
+        assert np.array_equal(a["scores"].view(np.uint32), g["scores"][r0:r1].view(np.uint32)), \
+            f"requests {lo}..{hi - 1}: scores"
+    rng = np.random.default_rng(53)
     ends = np.concatenate([off[:-1], off[1:] - 1])
     sample = np.unique(np.concatenate([rng.choice(batch["n_rows"], 700, replace=False), ends]))
     sample = sample[(sample >= 0) & (sample < batch["n_rows"])]
