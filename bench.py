@@ -40,9 +40,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def stage_work(cfg, batch, stage):
+def stage_work(cfg, batch, stage, compact=False):
     """Algorithmic work of one launch of a stage: ('hbm', bytes) or
-    ('mfma', flops)."""
+    ('mfma', flops). compact: the top-k model's network input keeps only
+    each request's k groups (the first layer runs on k * d inputs)."""
     es = {"f32": 4, "bf16": 2, "f16": 2}[cfg.dtype]
     idb = 8 if cfg.hashed else 4
     R, Q = batch["n_rows"], len(batch["req_off"]) - 1
@@ -61,8 +62,13 @@ def stage_work(cfg, batch, stage):
         return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * es + R * m * 4 + Q * nus * d * 4
     if stage == "se_rows":      # squeeze read, SE weights written
         return "hbm", 2 * R * m * 4
-    if stage == "apply":        # rows read and written in place, SE weights read
-        return "hbm", 2 * R * cfg.d_in * es + R * m * 4
+    kin = min(cfg.topk_k, m) * d if compact else cfg.d_in   # width of the network input
+    if stage == "apply":
+        if compact:              # kept groups read, compacted rows written, SE weights read
+            return "hbm", 2 * R * kin * es + R * m * 4
+        return "hbm", 2 * R * cfg.d_in * es + R * m * 4   # rows read and written in place
+    if stage == "weight_cols":   # each request's columns of the first layer's weights
+        return "hbm", 2 * Q * cfg.widths[1] * kin * es + Q * min(cfg.topk_k, m) * 4
     if stage == "gather_raw":
         # ids + gathered ad/cross rows + the fp32 concatenated embedding written
         return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * 4 + Q * nus * d * 4
@@ -73,7 +79,8 @@ def stage_work(cfg, batch, stage):
         return "mfma", 2.0 * R * (w[-5] * w[-4] + w[-4] * w[-3] + w[-3] * w[-2] + w[-2] * w[-1])
     if stage.startswith("dense"):
         li = int(stage[5:])
-        return "mfma", 2.0 * R * cfg.widths[li] * cfg.widths[li + 1]
+        k_in = kin if li == 0 else cfg.widths[li]
+        return "mfma", 2.0 * R * k_in * cfg.widths[li + 1]
     if stage == "tail":
         w = cfg.widths
         return "mfma", 2.0 * R * (w[-4] * w[-3] + w[-3] * w[-2] + w[-2] * w[-1])
@@ -85,8 +92,8 @@ def stage_work(cfg, batch, stage):
     return "hbm", 0
 
 
-def roofline_entry(cfg, batch, stage, ms):
-    kind, work = stage_work(cfg, batch, stage)
+def roofline_entry(cfg, batch, stage, ms, compact=False):
+    kind, work = stage_work(cfg, batch, stage, compact)
     if kind in ("mfma", "mfma_f32"):
         ach = work / (ms * 1e-3) / 1e12
         peak = PEAK_MFMA_TFLOPS["f32" if kind == "mfma_f32" else cfg.dtype]
@@ -488,8 +495,10 @@ def _stage_of(kernel_name, dense_index):
         return "gather_se"
     if "se_rows_kernel" in kernel_name:
         return "se_rows"
-    if "apply_weights_kernel" in kernel_name:
+    if "apply_weights_kernel" in kernel_name or "apply_compact_kernel" in kernel_name:
         return "apply"
+    if "gather_weight_cols" in kernel_name:
+        return "weight_cols"
     if "dense_f32" in kernel_name:
         return "se_dense"
     if "dense_tail_kernel" in kernel_name:
@@ -859,9 +868,10 @@ def main():
     log(f"with stage events: {ms_profiled:.4f} ms/step")
 
     stage_rows = []
+    compact = any(name == "weight_cols" for name, _ in stages)
     for name, tot in stages:
         ms = tot / max(n_calls, 1)
-        e = roofline_entry(cfg, batch, name, ms)
+        e = roofline_entry(cfg, batch, name, ms, compact)
         e.update(name=name, ms=round(ms, 5))
         stage_rows.append(e)
         log(f"  {name:12s} {ms * 1e3:9.2f} us  {e['achieved']:>9} {e['unit']}  ({100 * e['frac']:.1f}%)")

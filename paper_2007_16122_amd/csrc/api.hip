@@ -26,7 +26,9 @@ struct ArenaLayout {
 };
 
 struct WorkLayout {
-  size_t err, U, zU, Uh, urow, X, E, actA, actB, sbuf, zbuf, partial, mask, total;
+  size_t err, U, zU, Uh, urow, X, E, actA, actB, sbuf, zbuf, partial, mask;
+  size_t Xc, Wc, kept, rtiles, n_rtiles;   // compacted network input (see compact_input)
+  size_t total;
 };
 
 }  // namespace
@@ -88,6 +90,25 @@ bool topk_split(const cold_model &m) {
   return m.desc.topk_k > 0 && !m.literal_se && m.desc.n_seq == 0 && m.M <= 256 && m.H <= 64;
 }
 
+// Top-k models whose first layer is a plain dense layer: each request's
+// network input keeps only its k groups (in group order) and the first
+// layer runs on them with the matching columns of its weights, which gives
+// the masked input's products without the dropped groups' zeros (their
+// products add nothing). Chosen by the model alone, for every batch size.
+int kept_groups(const cold_model &m) { return m.desc.topk_k < m.M ? m.desc.topk_k : m.M; }
+
+bool compact_input(const cold_model &m) {
+  if (!topk_split(m) || kept_groups(m) >= m.M || m.dtype == kF32) return false;
+  const int L = m.desc.n_layers;
+  const bool fuse_tail = L >= 3 && tail_supported(m.dtype, m.widths[L - 3], m.widths[L - 2],
+                                                  m.widths[L - 1], m.widths[L]);
+  const int n_separate = fuse_tail ? L - 3 : L - 1;
+  const bool dense_tail = fuse_tail && n_separate >= 1 &&
+                          dense_tail_supported(m.dtype, 1, m.widths[n_separate], m.widths[n_separate - 1]);
+  return n_separate - (dense_tail ? 1 : 0) >= 1 &&
+         dense_grouped_supported(m.dtype, m.widths[1], kept_groups(m) * m.d);
+}
+
 ArenaLayout arena_layout(const cold_model &m) {
   ArenaLayout a;
   size_t off = 0;
@@ -147,6 +168,13 @@ WorkLayout work_layout(const cold_model &m, int64_t R, int64_t Q) {
   const size_t parts = topk_split(m) ? (size_t)((R + 15) / 16) * m.M : (size_t)Q * kMaskParts * m.M;
   w.partial = take(topk ? sizeof(float) * parts : 0);
   w.mask = take(topk ? (size_t)Q * m.M : 0);
+  const bool compact = compact_input(m);
+  const size_t kin = compact ? (size_t)kept_groups(m) * m.d : 0;   // compacted input width
+  w.Xc = take((size_t)m.es * R * kin);
+  w.Wc = take(compact ? (size_t)m.es * Q * m.widths[1] * kin : 0);
+  w.kept = take(compact ? sizeof(int32_t) * (size_t)Q * kept_groups(m) : 0);
+  w.rtiles = take(compact ? sizeof(RowTile) * (size_t)row_tile_capacity(R, Q) : 0);
+  w.n_rtiles = take(compact ? sizeof(int32_t) : 0);
   w.total = off;
   return w;
 }
@@ -484,6 +512,9 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
   if (validate && (e = launch_clear_flag(g.err, s)) != hipSuccess) return hip_fail(m, e, "clear");
   // the one-pass SE (no top-k) of small models runs on the register-resident gather
   const bool full = !m->literal_se && !topk && gather_full_supported(m->dtype, g);
+  // top-k models with a compacted network input (the first layer per request)
+  const bool compact = compact_input(*m);
+  float *sb_compact = compact ? (importance ? importance : reinterpret_cast<float *>(W + wl.sbuf)) : nullptr;
   if (user_pool_needed(m->dtype, g)) {   // per-request user rows and pooled sequences
     if ((e = marks.mark("user_pool")) != hipSuccess) return hip_fail(m, e, "profile event");
     if ((e = launch_user_pool(m->dtype, m->hashed, g, s)) != hipSuccess)
@@ -540,13 +571,30 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
                               reinterpret_cast<const float *>(A + al.w2p), g.b2, tpart, s)) != hipSuccess)
       return hip_fail(m, e, "se_rows launch");
     if ((e = marks.mark("group_mask")) != hipSuccess) return hip_fail(m, e, "profile event");
+    int32_t *kept = compact ? reinterpret_cast<int32_t *>(W + wl.kept) : nullptr;
     if ((e = launch_group_mask_tiles(sb, tpart, b->req_off, Q, R, m->M, D.topk_k, mask, group_mask,
-                                     s)) != hipSuccess)
+                                     kept, s)) != hipSuccess)
       return hip_fail(m, e, "group_mask launch");
-    if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
-    if ((e = launch_apply_weights(m->dtype, D.linear_log, W + wl.X, sb, mask, b->req_off, Q, R, m->M,
-                                  m->d, s)) != hipSuccess)
-      return hip_fail(m, e, "apply launch");
+    if (compact) {
+      // every request's columns of the first layer's weights (and the
+      // layer's row tiles), and the rows' kept groups reweighted into the
+      // compacted input
+      if ((e = marks.mark("weight_cols")) != hipSuccess) return hip_fail(m, e, "profile event");
+      if ((e = launch_gather_weight_cols(m->dtype, A + al.w[0], m->widths[1], m->D_in, kept, Q,
+                                         kept_groups(*m), m->d, W + wl.Wc, b->req_off, R,
+                                         reinterpret_cast<RowTile *>(W + wl.rtiles),
+                                         reinterpret_cast<int32_t *>(W + wl.n_rtiles), s)) != hipSuccess)
+        return hip_fail(m, e, "weight columns launch");
+      if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
+      if ((e = launch_apply_compact(m->dtype, D.linear_log, W + wl.X, W + wl.Xc, sb, kept, b->req_off,
+                                    Q, R, m->M, kept_groups(*m), m->d, s)) != hipSuccess)
+        return hip_fail(m, e, "apply launch");
+    } else {
+      if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
+      if ((e = launch_apply_weights(m->dtype, D.linear_log, W + wl.X, sb, mask, b->req_off, Q, R, m->M,
+                                    m->d, s)) != hipSuccess)
+        return hip_fail(m, e, "apply launch");
+    }
   } else {
     float *sb = importance ? importance : reinterpret_cast<float *>(W + wl.sbuf);
     uint8_t *mask = W + wl.mask;
@@ -569,6 +617,11 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     if ((e = hipMemcpyAsync(x_out, W + wl.X, (size_t)m->es * R * m->D_in, hipMemcpyDeviceToDevice,
                             s)) != hipSuccess)
       return hip_fail(m, e, "network input copy");
+    // the compacted form keeps the gathered rows in X: the masked input
+    // (dropped groups zero) is formed in the copy
+    if (compact && (e = launch_apply_weights(m->dtype, D.linear_log, x_out, sb_compact, W + wl.mask,
+                                             b->req_off, Q, R, m->M, m->d, s)) != hipSuccess)
+      return hip_fail(m, e, "network input copy (masked)");
   }
   // network: hidden layers ping-pong between two activation buffers; the
   // last two hidden layers and the head run fused when their widths allow
@@ -588,9 +641,16 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     void *outp = bufs[l & 1];
     if ((e = marks.mark(l < 12 ? kDenseNames[l] : "dense")) != hipSuccess)
       return hip_fail(m, e, "profile event");
-    if ((e = launch_dense_relu(m->dtype, in, A + al.w[l], reinterpret_cast<const float *>(A + al.b[l]),
-                               outp, R, m->widths[l + 1], m->widths[l], s)) != hipSuccess)
-      return hip_fail(m, e, "dense layer launch");
+    if (l == 0 && compact)
+      e = launch_dense_relu_grouped(m->dtype, W + wl.Xc, W + wl.Wc,
+                                    reinterpret_cast<const float *>(A + al.b[0]), outp, R, Q,
+                                    b->req_off, m->widths[1], kept_groups(*m) * m->d,
+                                    reinterpret_cast<RowTile *>(W + wl.rtiles),
+                                    reinterpret_cast<int32_t *>(W + wl.n_rtiles), s);
+    else
+      e = launch_dense_relu(m->dtype, in, A + al.w[l], reinterpret_cast<const float *>(A + al.b[l]),
+                            outp, R, m->widths[l + 1], m->widths[l], s);
+    if (e != hipSuccess) return hip_fail(m, e, "dense layer launch");
     in = outp;
   }
   if (dense_tail) {

@@ -223,10 +223,18 @@ int device_cus();
 hipError_t launch_se_rows(const float *z, float *s_out, int64_t R, int32_t M, int32_t H,
                           const float *w1p, const float *b1, const float *w2p, const float *b2,
                           float *tile_part, hipStream_t s);
-// the top-k mask of every request from s [R][M] and se_rows' tile sums
+// the top-k mask of every request from s [R][M] and se_rows' tile sums;
+// kept (when not null, M <= 256): [Q][min(k, M)] the kept groups in group order
 hipError_t launch_group_mask_tiles(const float *s_buf, const float *tile_part,
                                    const int32_t *req_off, int64_t Q, int64_t R, int32_t M,
-                                   int32_t k, uint8_t *mask, uint8_t *mask_out, hipStream_t s);
+                                   int32_t k, uint8_t *mask, uint8_t *mask_out, int32_t *kept,
+                                   hipStream_t s);
+// Xc [R][kp*d]: the kp kept groups of each row's request (kept [Q][kp]) taken
+// from the gathered rows Xraw [R][M*d], times s [R][M], linear_log when ll,
+// rounded once to the storage type
+hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, const float *s_buf,
+                                const int32_t *kept, const int32_t *req_off, int64_t Q, int64_t R,
+                                int32_t M, int32_t kp, int32_t d, hipStream_t s);
 // floats of the two packed SE operands (0 when M or H is beyond the kernel)
 void se_rows_packed_floats(int32_t M, int32_t H, size_t *n1, size_t *n2);
 // W1 [H][M] and W2 [M][H] into the row-wise SE kernel's operand order
@@ -244,6 +252,33 @@ hipError_t launch_transpose_f32(const float *src, float *dst, int32_t rows, int3
 
 hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
                              int64_t R, int32_t N, int32_t K, hipStream_t s);
+// One row tile of a layer whose requests each have their own weights: rows
+// [r0, r0 + n) of request q
+struct RowTile {
+  int64_t r0;
+  int32_t n, q;
+};
+// entries of the row-tile table for R rows in Q requests (any tile height)
+inline int64_t row_tile_capacity(int64_t R, int64_t Q) { return (R + 63) / 64 + Q + 1; }
+// Wc [Q][N][kp*d]: for every request q, the columns of W [N][K] (K = M*d)
+// of the groups kept[q][0..kp) in that order (storage type); the same launch
+// lays out the row tiles of launch_dense_relu_grouped for these R rows
+// (tiles [row_tile_capacity], n_tiles [1])
+hipError_t launch_gather_weight_cols(int dtype, const void *W, int32_t N, int32_t K,
+                                     const int32_t *kept, int64_t Q, int32_t kp, int32_t d,
+                                     void *Wc, const int32_t *req_off, int64_t R, RowTile *tiles,
+                                     int32_t *n_tiles, hipStream_t s);
+// Y = ReLU(X W_q^T + b) where row r of X [R][K] belongs to request q(r)
+// (req_off [Q+1]) and W_q = W + q * N * K; the row tiles never straddle two
+// requests (the table and count that launch_gather_weight_cols built for
+// the same R, Q, N and K).
+// Same tile shapes and sum order as launch_dense_relu; bf16 and fp16 with
+// K % 32 == 0 and N % 8 == 0.
+bool dense_grouped_supported(int dtype, int32_t N, int32_t K);
+hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, const float *b,
+                                     void *y, int64_t R, int64_t Q, const int32_t *req_off,
+                                     int32_t N, int32_t K, RowTile *tiles, int32_t *n_tiles,
+                                     hipStream_t s);
 bool tail_supported(int dtype, int K0, int N1, int N2, int n_out);
 // the fused tail reads its two hidden layers' weights fragment-major
 // (mlp.hip, frag_offset): [N][K] row-major -> that order (N % 16 == 0, K % 32 == 0)

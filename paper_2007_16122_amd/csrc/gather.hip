@@ -640,8 +640,9 @@ __global__ __launch_bounds__(1024) void mask_select_tiles_kernel(const float *s_
                                                                  const float *tpart,
                                                                  const int32_t *req_off, int64_t R,
                                                                  int32_t M, int32_t k, uint8_t *mask,
-                                                                 uint8_t *mask_out) {
+                                                                 uint8_t *mask_out, int32_t *kept) {
   extern __shared__ float lds[];  // [P][M] part sums, [M] importance, [M] ranks, [2][M] edges
+  __shared__ int32_t s_wkept[4];  // kept groups per wave of the first 256 threads
   const int P = mask_tile_parts(M);
   float *imp = lds + P * M;
   int *rank = reinterpret_cast<int *>(imp + M);
@@ -661,18 +662,32 @@ __global__ __launch_bounds__(1024) void mask_select_tiles_kernel(const float *s_
   for (int idx = threadIdx.x; idx < P * nq; idx += (int)blockDim.x - M) {
     const int p = idx / nq, gq = idx - p * nq;
     const int64_t a = t0 + p * per, b = a + per < t0 + nt ? a + per : t0 + nt;
+    // blocks of 16 tiles: every load of a block in flight before its sums,
+    // which run in tile order (the block's slots past b add +0 to a sum of
+    // non-negative weights, which leaves it unchanged)
     if (v4) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 16
-      for (int64_t t = a; t < b; ++t) {
-        const float4 v = reinterpret_cast<const float4 *>(tpart + t * M)[gq];
-        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      for (int64_t t = a; t < b; t += 16) {
+        float4 v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          v[i] = t + i < b ? reinterpret_cast<const float4 *>(tpart + (t + i) * M)[gq]
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          acc.x += v[i].x; acc.y += v[i].y; acc.z += v[i].z; acc.w += v[i].w;
+        }
       }
       reinterpret_cast<float4 *>(lds + p * M)[gq] = acc;
     } else {
       float acc = 0.0f;
-#pragma unroll 16
-      for (int64_t t = a; t < b; ++t) acc += tpart[t * M + gq];
+      for (int64_t t = a; t < b; t += 16) {
+        float v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = t + i < b ? tpart[(t + i) * M + gq] : 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc += v[i];
+      }
       lds[p * M + gq] = acc;
     }
   }
@@ -723,16 +738,41 @@ __global__ __launch_bounds__(1024) void mask_select_tiles_kernel(const float *s_
     mask[q * M + g] = keep;
     if (mask_out) mask_out[q * M + g] = keep;
   }
+  if (kept) {
+    // the kept groups in group order, min(k, M) of them: thread g < 256
+    // takes group g (M <= 256), its place is the count of kept groups
+    // before it (wave ballots, then the earlier waves' counts)
+    const int g = threadIdx.x, lane = g & 63, w = g >> 6;
+    const bool f = g < M && rank[g] < k;
+    unsigned long long bal = 0;
+    if (g < 256) {
+      bal = __ballot(f);
+      if (lane == 0) s_wkept[w] = __popcll(bal);
+    }
+    __syncthreads();
+    const int kp = k < M ? k : M;
+    if (f) {
+      int pos = __popcll(bal & ((1ull << lane) - 1));
+      for (int v = 0; v < w; ++v) pos += s_wkept[v];
+      if (pos < kp) kept[q * kp + pos] = g;
+    }
+    // ranks form a permutation unless an importance is NaN; then the list
+    // is still filled with valid groups
+    const int n_kept = s_wkept[0] + s_wkept[1] + s_wkept[2] + s_wkept[3];
+    for (int j = n_kept + (int)threadIdx.x; j < kp; j += (int)blockDim.x) kept[q * kp + j] = 0;
+  }
 }
 
 hipError_t launch_group_mask_tiles(const float *s_buf, const float *tile_part,
                                    const int32_t *req_off, int64_t Q, int64_t R, int32_t M,
-                                   int32_t k, uint8_t *mask, uint8_t *mask_out, hipStream_t s) {
+                                   int32_t k, uint8_t *mask, uint8_t *mask_out, int32_t *kept,
+                                   hipStream_t s) {
   if (Q <= 0) return hipSuccess;
   if (M % 4 == 0 && (reinterpret_cast<uintptr_t>(tile_part) & 15)) return hipErrorInvalidValue;
+  if (kept && (M > 256 || k <= 0)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(mask_select_tiles_kernel, dim3((unsigned)Q), dim3(1024),
                      sizeof(float) * (size_t)(mask_tile_parts(M) + 4) * M, s, s_buf, tile_part,
-                     req_off, R, M, k, mask, mask_out);
+                     req_off, R, M, k, mask, mask_out, kept);
   return hipGetLastError();
 }
 
@@ -2048,6 +2088,105 @@ static hipError_t apply_t(bool ll, void *X, const float *s_buf, const uint8_t *m
     hipLaunchKernelGGL((apply_weights_kernel<TS, false>), grid, dim3(256), 0, s, static_cast<TS *>(X),
                        s_buf, mask, req_off, Q, R, M, lcpg, cpr, div_magic((uint32_t)cpr));
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------- apply_compact
+// The network input of a model whose requests keep k of the M groups, with
+// the dropped groups left out instead of zeroed (Section 3.2 feature group
+// selection): row r of request q holds, in group order, the kp = min(k, M)
+// groups that q keeps (kept[q][j]), each 16-byte chunk round(LL(s[r][g] e))
+// of the gathered row (Eq. 3 when LL). The gathered rows stay in place; the
+// compacted rows go to Xc [R][kp * d]. A workgroup takes kApplyRows rows and
+// finds their requests and kept lists once, in LDS.
+template <typename TS, bool LL>
+__global__ __launch_bounds__(256) void apply_compact_kernel(const TS *__restrict__ Xraw,
+                                                            TS *__restrict__ Xc,
+                                                            const float *__restrict__ s_buf,
+                                                            const int32_t *__restrict__ kept,
+                                                            const int32_t *__restrict__ req_off,
+                                                            int64_t Q, int64_t R, int M, int kp,
+                                                            int lcpg, int CPR, int CPRC,
+                                                            uint32_t mg_cprc) {
+  constexpr int EPC = Elem<TS>::kPerChunk;
+  __shared__ int32_t s_rq[kApplyRows];
+  __shared__ int32_t s_kept[kApplyRows][256];
+  const int64_t r0 = (int64_t)blockIdx.x * kApplyRows;
+  const int rows = R - r0 < kApplyRows ? (int)(R - r0) : kApplyRows;
+  if (threadIdx.x < rows) s_rq[threadIdx.x] = (int32_t)request_of_row(req_off, Q, r0 + threadIdx.x);
+  __syncthreads();
+  for (int i = threadIdx.x; i < rows * kp; i += 256) {
+    const int t = i / kp, j = i - t * kp;
+    s_kept[t][j] = kept[(int64_t)s_rq[t] * kp + j];
+  }
+  __syncthreads();
+  const uint4 *xr = reinterpret_cast<const uint4 *>(Xraw) + r0 * CPR;
+  uint4 *xc = reinterpret_cast<uint4 *>(Xc) + r0 * CPRC;
+  const int n = rows * CPRC;
+  for (int base = 0; base < n; base += 256 * kApplyPerThread) {
+    uint4 raw[kApplyPerThread];
+    float sg[kApplyPerThread];
+#pragma unroll
+    for (int u = 0; u < kApplyPerThread; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      raw[u] = make_uint4(0, 0, 0, 0);
+      sg[u] = 0.0f;
+      if (idx < n) {
+        const int t = fast_div(idx, mg_cprc), c = idx - t * CPRC;
+        const int j = c >> lcpg, h = c & ((1 << lcpg) - 1);
+        int g = s_kept[t][j];
+        g = g < 0 ? 0 : (g < M ? g : M - 1);
+        raw[u] = xr[(int64_t)t * CPR + (g << lcpg) + h];
+        sg[u] = s_buf[(r0 + t) * M + g];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyPerThread; ++u) {
+      const int idx = base + u * 256 + threadIdx.x;
+      if (idx < n) {
+        float v[EPC], o[EPC];
+        Elem<TS>::unpack(raw[u], v);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+          const float x = sg[u] * v[e];
+          o[e] = LL ? linear_log(x) : x;
+        }
+        xc[idx] = Elem<TS>::pack(o);
+      }
+    }
+  }
+}
+
+template <typename TS>
+static hipError_t apply_compact_t(bool ll, const void *Xraw, void *Xc, const float *s_buf,
+                                  const int32_t *kept, const int32_t *req_off, int64_t Q,
+                                  int64_t R, int32_t M, int32_t kp, int32_t d, hipStream_t s) {
+  constexpr int EPC = Elem<TS>::kPerChunk;
+  const int cpg = d / EPC, cpr = M * cpg, cprc = kp * cpg;
+  if (cpg <= 0 || (cpg & (cpg - 1)) || kp <= 0 || kp > M || M > 256 ||
+      kApplyRows * (int64_t)cpr >= (1 << 16))
+    return hipErrorInvalidValue;
+  const int lcpg = __builtin_ctz(cpg);
+  const dim3 grid((unsigned)((R + kApplyRows - 1) / kApplyRows));
+  if (ll)
+    hipLaunchKernelGGL((apply_compact_kernel<TS, true>), grid, dim3(256), 0, s,
+                       static_cast<const TS *>(Xraw), static_cast<TS *>(Xc), s_buf, kept, req_off,
+                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc));
+  else
+    hipLaunchKernelGGL((apply_compact_kernel<TS, false>), grid, dim3(256), 0, s,
+                       static_cast<const TS *>(Xraw), static_cast<TS *>(Xc), s_buf, kept, req_off,
+                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc));
+  return hipGetLastError();
+}
+
+hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, const float *s_buf,
+                                const int32_t *kept, const int32_t *req_off, int64_t Q, int64_t R,
+                                int32_t M, int32_t kp, int32_t d, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  switch (dtype) {
+    case kF32: return apply_compact_t<float>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
+    case kBF16: return apply_compact_t<__bf16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
+    default: return apply_compact_t<_Float16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
+  }
 }
 
 hipError_t launch_apply_weights(int dtype, bool ll, void *X, const float *s_buf,

@@ -388,13 +388,20 @@ __device__ __forceinline__ void buf_tile_kloop(
   wait_vm<0>();
 }
 
-template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2, int KB = 32>
+// GRP: the rows belong to requests with weights of their own; row tile tr
+// is entry tr of the device-built table (rows [r0, r0 + n) of request q,
+// whose weights start w_stride elements after the previous request's), and
+// workgroups past the table's count have no tile.
+template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2, int KB = 32, bool GRP = false>
 __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
                                                                      const TS *__restrict__ W,
                                                                      const float *__restrict__ bias,
                                                                      TS *__restrict__ Y, int64_t R,
                                                                      int N, int K, int tiles_n,
-                                                                     int tiles_total) {
+                                                                     int tiles_total,
+                                                                     const RowTile *__restrict__ rtiles,
+                                                                     const int32_t *__restrict__ n_rtiles,
+                                                                     int64_t w_stride) {
   typedef BufTile<BR, BN, S, WN, KB> G;
   constexpr int NT = G::NT, NI = G::NI, RJ = G::RJ;
   constexpr int OUT_STRIDE = BN + 8;                 // elements per staged output row
@@ -407,7 +414,15 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
 
   const int tile = xcd_tile(blockIdx.x, tiles_total);
   const int tr = tile / tiles_n, tn = tile - tr * tiles_n;
-  const int64_t r0 = (int64_t)tr * BR;
+  int64_t r0 = (int64_t)tr * BR;
+  const TS *Wt = W;
+  if constexpr (GRP) {
+    if (tr >= *n_rtiles) return;   // the same for the whole workgroup
+    const RowTile t = rtiles[tr];
+    r0 = t.r0;
+    R = t.r0 + t.n;
+    Wt = W + (int64_t)t.q * w_stride;
+  }
   const int n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -415,7 +430,7 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
   const int dn = (lane >> 4) * 4, dr = lane & 15;
 
   f32x4 acc[NI][RJ];
-  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, N, K, r0, n0, smem, acc);
+  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, Wt, bias, R, N, K, r0, n0, smem, acc);
 
   // epilogue: round, ReLU, stage the tile in LDS, write rows with 16-byte
   // stores.
@@ -788,23 +803,32 @@ __global__ __launch_bounds__(128 * WN, MINB) void dense_tail_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave % WN, wr = wave / WN;
 
-  f32x4 acc[NI][RJ];
-  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, BN, K, r0, 0, smem, acc);
-
   // tail weights: wave w owns feature blocks 2 (w % 4) and 2 (w % 4) + 1 of
   // the first tail layer, and feature block w % 4 of the second, each on
-  // the rows PR/2 (w / 4) .. PR/2 (w / 4 + 1) of a pass
+  // the rows PR/2 (w / 4) .. PR/2 (w / 4 + 1) of a pass. With few
+  // accumulators they are loaded before the K loop, so their latency hides
+  // behind it (the loads are older than the ring's, which the K loop's
+  // counted waits allow for); with many, after it.
+  constexpr bool W_EARLY = NI * RJ <= 8;
   frag w1f[KS1][2], w2f[KS2][1];
+  float whv, bhv;
+  auto load_tail_weights = [&]() {
 #pragma unroll
-  for (int k = 0; k < KS1; ++k)
+    for (int k = 0; k < KS1; ++k)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      w1f[k][i] = *reinterpret_cast<const frag *>(W1 + frag_offset(2 * (wave % 4) + i, k, KS1, lane));
+      for (int i = 0; i < 2; ++i)
+        w1f[k][i] = *reinterpret_cast<const frag *>(W1 + frag_offset(2 * (wave % 4) + i, k, KS1, lane));
 #pragma unroll
-  for (int k = 0; k < KS2; ++k)
-    w2f[k][0] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave % 4, k, KS2, lane));
-  const float whv = Elem<TS>::to_f32(Wh[tid < n_out * N2 ? tid : 0]);
-  const float bhv = bh[tid < n_out ? tid : 0];
+    for (int k = 0; k < KS2; ++k)
+      w2f[k][0] = *reinterpret_cast<const frag *>(W2 + frag_offset(wave % 4, k, KS2, lane));
+    whv = Elem<TS>::to_f32(Wh[tid < n_out * N2 ? tid : 0]);
+    bhv = bh[tid < n_out ? tid : 0];
+  };
+  if constexpr (W_EARLY) load_tail_weights();
+
+  f32x4 acc[NI][RJ];
+  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, W, bias, R, BN, K, r0, 0, smem, acc);
+  if constexpr (!W_EARLY) load_tail_weights();
   compiler_fence();
   __builtin_amdgcn_s_barrier();   // every wave is past the K loop: the ring is free
   compiler_fence();
@@ -1082,75 +1106,170 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
   return hipGetLastError();
 }
 
+// Row tiles of height BR over requests: the bound on their count (request q
+// of n_q rows takes ceil(n_q / BR) <= (n_q + BR - 1) / BR tiles; exact for
+// one request, so a one-request batch has no idle workgroups).
+static int64_t row_tiles_bound(int64_t R, int64_t Q, int BR) { return (R + Q * (BR - 1)) / BR; }
+
+// The table of those tiles, by one workgroup of NT threads: request q's rows
+// [lo, hi) (offsets clamped to [0, R]) take ceil((hi - lo) / BR) tiles, in
+// request order; entries past cap are not written (cap bounds the table and
+// the layer's grid whatever the offsets are). Requests in blocks of NT with
+// a running start.
+template <int NT>
+__device__ void build_row_tiles(const int32_t *__restrict__ req_off, int64_t Q, int64_t R, int BR,
+                                int64_t cap, RowTile *__restrict__ tiles,
+                                int32_t *__restrict__ n_tiles, int64_t *s_scan) {
+  const int tid = threadIdx.x;
+  int64_t start0 = 0;
+  for (int64_t base = 0; base < Q; base += NT) {
+    const int64_t q = base + tid;
+    int64_t lo = 0, hi = 0;
+    if (q < Q) {
+      lo = req_off[q];
+      hi = req_off[q + 1];
+      lo = lo < 0 ? 0 : (lo > R ? R : lo);
+      hi = hi < lo ? lo : (hi > R ? R : hi);
+    }
+    const int64_t c = (hi - lo + BR - 1) / BR;
+    s_scan[tid] = c;
+    __syncthreads();
+    for (int off = 1; off < NT; off <<= 1) {
+      const int64_t v = tid >= off ? s_scan[tid - off] : 0;
+      __syncthreads();
+      s_scan[tid] += v;
+      __syncthreads();
+    }
+    const int64_t start = start0 + s_scan[tid] - c;
+    for (int64_t t = 0; t < c && start + t < cap; ++t) {
+      const int64_t r = lo + t * BR;
+      RowTile e;
+      e.r0 = r;
+      e.n = (int32_t)(hi - r < BR ? hi - r : BR);
+      e.q = (int32_t)q;
+      tiles[start + t] = e;
+    }
+    start0 += s_scan[NT - 1];
+    __syncthreads();   // s_scan is rewritten by the next block of requests
+  }
+  if (tid == 0) n_tiles[0] = (int32_t)(start0 < cap ? start0 : cap);
+}
+
+// requests with weights of their own (see dense_relu_buf_kernel's GRP)
+struct GroupArgs {
+  const int32_t *req_off;
+  int64_t Q;
+  RowTile *tiles;
+  int32_t *n_tiles;
+  int64_t w_stride;
+};
+
 template <typename TS, int BR, int BN, int S, int WN, int MINW, int KB = 32>
 static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void *y, int64_t R,
-                              int N, int K, hipStream_t s) {
+                              int N, int K, hipStream_t s, const GroupArgs *ga = nullptr) {
   const int tiles_n = (N + BN - 1) / BN;
-  const int64_t tiles_r = (R + BR - 1) / BR;
+  const int64_t tiles_r = ga ? row_tiles_bound(R, ga->Q, BR) : (R + BR - 1) / BR;
   const int64_t total = tiles_r * tiles_n;
   if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB>), dim3((unsigned)total),
-                     dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
-                     static_cast<TS *>(y), R, N, K, tiles_n, (int)total);
+  if (ga) {
+    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB, true>), dim3((unsigned)total),
+                       dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
+                       static_cast<TS *>(y), R, N, K, tiles_n, (int)total, ga->tiles, ga->n_tiles,
+                       ga->w_stride);
+  } else {
+    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB>), dim3((unsigned)total),
+                       dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
+                       static_cast<TS *>(y), R, N, K, tiles_n, (int)total,
+                       static_cast<const RowTile *>(nullptr), static_cast<const int32_t *>(nullptr),
+                       (int64_t)0);
+  }
   return hipGetLastError();
+}
+
+// The tile shape of a layer of R rows, N outputs and K inputs (the
+// buffered kernel for K % 32 == 0 and N % 8 == 0, else the plain one).
+//   Large batches: 256 x 256 tiles over 8 waves, in 64-deep stages (one
+// barrier per 64 MFMAs per wave, whole 128-byte rows per load) when K
+// allows (256 x 128 or 256 x 64 over 4 waves for narrower layers); batches
+// of a few thousand ads would leave most CUs idle with those, so 128..192 x
+// 128 tiles while 128-row tiles would still number one per CU, else 64 x 64.
+//   Every tile shape sums the same 32-deep K blocks in the same order, so the
+// outputs do not depend on the shape.
+enum class DTile {
+  k192x128, k160x128, k128x128_64, k128x128_32, k64x64_3s, k64x64_64, k64x64_32,
+  k256x256_64, k256x256_32, k256x128, k256x64, kPlain128, kPlain64
+};
+
+static DTile dense_tile(int64_t R, int N, int K) {
+  if (K % kBK != 0 || N % 8 != 0) return N % 128 == 0 ? DTile::kPlain128 : DTile::kPlain64;
+  const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
+  const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
+  const bool k64 = K % 64 == 0;
+  const int64_t cus = device_cus() > 0 ? device_cus() : 256;
+  if (big_tiles < 256 && mid_tiles >= 256 && k64 && N % 128 == 0) {
+    // x 128 tiles with the row height that gives the least work to the
+    // busiest CU (rounds of one tile per CU), provided the tiles still
+    // cover three quarters of the CUs (fewer, smaller layers run faster on
+    // 64 x 64 tiles, two per CU)
+    const int heights[3] = {192, 160, 128};
+    int best = 0;
+    int64_t best_cost = -1;
+    for (int h : heights) {
+      const int64_t tiles = ((R + h - 1) / h) * (N / 128);
+      const int64_t cost = (tiles + cus - 1) / cus * h;
+      if (4 * tiles >= 3 * cus && (best_cost < 0 || cost < best_cost)) best = h, best_cost = cost;
+    }
+    if (best == 192) return DTile::k192x128;
+    if (best == 160) return DTile::k160x128;
+    if (best == 128) return DTile::k128x128_64;
+  }
+  if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
+    return k64 ? DTile::k128x128_64 : DTile::k128x128_32;
+  if (big_tiles < 256) {
+    // at most two tiles per CU: a third 64-deep stage in flight (the K steps
+    // wait on load latency, not on the CU's throughput); more tiles than
+    // that run better with the smaller ring, more workgroups per CU
+    const int64_t small_tiles = ((R + 63) / 64) * ((N + 63) / 64);
+    if (k64 && small_tiles <= 2 * cus) return DTile::k64x64_3s;
+    return k64 ? DTile::k64x64_64 : DTile::k64x64_32;
+  }
+  if (N % 256 == 0) return k64 ? DTile::k256x256_64 : DTile::k256x256_32;
+  return N % 128 == 0 ? DTile::k256x128 : DTile::k256x64;
+}
+
+// rows of a tile (the buffered shapes)
+static int dense_tile_rows(DTile t) {
+  switch (t) {
+    case DTile::k192x128: return 192;
+    case DTile::k160x128: return 160;
+    case DTile::k128x128_64: case DTile::k128x128_32: return 128;
+    case DTile::k64x64_3s: case DTile::k64x64_64: case DTile::k64x64_32: return 64;
+    default: return 256;
+  }
 }
 
 template <typename TS>
 static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, void *y, int64_t R,
-                                int N, int K, hipStream_t s) {
-  if (K % kBK == 0 && N % 8 == 0) {
-    // large batches: 256 x 256 tiles over 8 waves, in 64-deep stages (one
-    // barrier per 64 MFMAs per wave, whole 128-byte rows per load) when K
-    // allows (256 x 128 or 256 x 64 over 4 waves for narrower layers);
-    // batches of a few thousand ads would leave most CUs idle with those,
-    // so 128..192 x 128 tiles while 128-row tiles would still number one
-    // per CU, else 64 x 64.
-    // Every tile shape sums the same 32-deep K blocks in the same order, so
-    // the outputs do not depend on the shape.
-    const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
-    const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
-    const bool k64 = K % 64 == 0;
-    if (big_tiles < 256 && mid_tiles >= 256 && k64 && N % 128 == 0) {
-      // x 128 tiles with the row height that gives the least work to the
-      // busiest CU (rounds of one tile per CU), provided the tiles still
-      // cover three quarters of the CUs (fewer, smaller layers run faster
-      // on 64 x 64 tiles, two per CU)
-      const int64_t cus = device_cus() > 0 ? device_cus() : 256;
-      const int heights[3] = {192, 160, 128};
-      int best = 0;
-      int64_t best_cost = -1;
-      for (int h : heights) {
-        const int64_t tiles = ((R + h - 1) / h) * (N / 128);
-        const int64_t cost = (tiles + cus - 1) / cus * h;
-        if (4 * tiles >= 3 * cus && (best_cost < 0 || cost < best_cost)) best = h, best_cost = cost;
-      }
-      switch (best) {
-        case 192: return dense_buf_t<TS, 192, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
-        case 160: return dense_buf_t<TS, 160, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
-        case 128: return dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s);
-        default: break;
-      }
-    }
-    if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
-      return k64 ? dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
-                 : dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    if (big_tiles < 256) {
-      // at most two tiles per CU: a third 64-deep stage in flight (the K
-      // steps wait on load latency, not on the CU's throughput); more tiles
-      // than that run better with the smaller ring, more workgroups per CU
-      const int64_t cus = device_cus() > 0 ? device_cus() : 256;
-      const int64_t small_tiles = ((R + 63) / 64) * ((N + 63) / 64);
-      if (k64 && small_tiles <= 2 * cus) return dense_buf_t<TS, 64, 64, 3, 2, 2, 64>(x, w, b, y, R, N, K, s);
-      return k64 ? dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s)
-                 : dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    }
-    if (N % 256 == 0 && k64) return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s);
-    if (N % 256 == 0) return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s);
-    if (N % 128 == 0) return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s);
-    return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s);
+                                int N, int K, hipStream_t s, const GroupArgs *ga = nullptr) {
+  switch (dense_tile(R, N, K)) {
+    case DTile::k192x128: return dense_buf_t<TS, 192, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k160x128: return dense_buf_t<TS, 160, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k128x128_64: return dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k128x128_32: return dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k64x64_3s: return dense_buf_t<TS, 64, 64, 3, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k64x64_64: return dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k64x64_32: return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k256x256_64: return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k256x256_32: return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k256x128: return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k256x64: return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
+    case DTile::kPlain128:
+      if (ga) return hipErrorInvalidValue;
+      return dense_mfma_t<TS, 256, 128>(x, w, b, y, R, N, K, s);
+    default:
+      if (ga) return hipErrorInvalidValue;
+      return dense_mfma_t<TS, 256, 64>(x, w, b, y, R, N, K, s);
   }
-  if (N % 128 == 0) return dense_mfma_t<TS, 256, 128>(x, w, b, y, R, N, K, s);
-  return dense_mfma_t<TS, 256, 64>(x, w, b, y, R, N, K, s);
 }
 
 hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const float *b, void *y,
@@ -1164,6 +1283,73 @@ hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const floa
   }
   if (dtype == kBF16) return dense_mfma_dt<__bf16>(x, w, b, y, R, N, K, s);
   return dense_mfma_dt<_Float16>(x, w, b, y, R, N, K, s);
+}
+
+bool dense_grouped_supported(int dtype, int32_t N, int32_t K) {
+  return dtype != kF32 && K > 0 && K % kBK == 0 && N > 0 && N % 8 == 0;
+}
+
+hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, const float *b,
+                                     void *y, int64_t R, int64_t Q, const int32_t *req_off,
+                                     int32_t N, int32_t K, RowTile *tiles, int32_t *n_tiles,
+                                     hipStream_t s) {
+  if (R <= 0 || Q <= 0) return hipSuccess;
+  if (!dense_grouped_supported(dtype, N, K)) return hipErrorInvalidValue;
+  const GroupArgs ga{req_off, Q, tiles, n_tiles, (int64_t)N * K};
+  if (dtype == kBF16) return dense_mfma_dt<__bf16>(x, w, b, y, R, N, K, s, &ga);
+  return dense_mfma_dt<_Float16>(x, w, b, y, R, N, K, s, &ga);
+}
+
+// Wc [Q][N][kp * cpg chunks]: workgroup q * N + n copies row n of W's kept
+// columns for request q (its kp groups of cpg 16-byte chunks); the grid's
+// last workgroup lays out the first layer's row tiles (build_row_tiles) for
+// the tile height that layer will use.
+__global__ __launch_bounds__(256) void gather_weight_cols_kernel(const uint4 *__restrict__ W,
+                                                                 int64_t N, int32_t cpr,
+                                                                 const int32_t *__restrict__ kept,
+                                                                 int64_t Q, int32_t kp, int32_t lcpg,
+                                                                 uint4 *__restrict__ Wc,
+                                                                 const int32_t *__restrict__ req_off,
+                                                                 int64_t R, int BR, int64_t cap,
+                                                                 RowTile *__restrict__ tiles,
+                                                                 int32_t *__restrict__ n_tiles) {
+  __shared__ int64_t s_scan[256];
+  const int64_t row = blockIdx.x;
+  if (row == (int64_t)gridDim.x - 1) {
+    build_row_tiles<256>(req_off, Q, R, BR, cap, tiles, n_tiles, s_scan);
+    return;
+  }
+  const int64_t q = row / N, n = row - q * N;
+  const int cprc = kp << lcpg, ng = cpr >> lcpg;   // chunks of a compacted row; groups of W's
+  const int32_t *kq = kept + q * kp;
+  const uint4 *src = W + n * cpr;
+  uint4 *dst = Wc + row * cprc;
+  for (int c = threadIdx.x; c < cprc; c += 256) {
+    const int j = c >> lcpg, h = c & ((1 << lcpg) - 1);
+    int g = kq[j];
+    g = g < 0 ? 0 : (g < ng ? g : ng - 1);
+    dst[c] = src[(g << lcpg) + h];
+  }
+}
+
+hipError_t launch_gather_weight_cols(int dtype, const void *W, int32_t N, int32_t K,
+                                     const int32_t *kept, int64_t Q, int32_t kp, int32_t d,
+                                     void *Wc, const int32_t *req_off, int64_t R, RowTile *tiles,
+                                     int32_t *n_tiles, hipStream_t s) {
+  const int es = dtype == kF32 ? 4 : 2;
+  const int cpg = d * es / 16;
+  if (cpg <= 0 || (cpg & (cpg - 1)) || (d * es) % 16 || K % d || kp <= 0 || kp > K / d || Q <= 0)
+    return hipErrorInvalidValue;
+  const int Kc = kp * d;   // the first layer's inputs after compaction
+  if (!dense_grouped_supported(dtype, N, Kc)) return hipErrorInvalidValue;
+  const int BR = dense_tile_rows(dense_tile(R, N, Kc));
+  const int64_t rows = Q * (int64_t)N;
+  if (rows + 1 > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_weight_cols_kernel, dim3((unsigned)(rows + 1)), dim3(256), 0, s,
+                     static_cast<const uint4 *>(W), (int64_t)N, (int32_t)(K * es / 16), kept, Q, kp,
+                     (int32_t)__builtin_ctz(cpg), static_cast<uint4 *>(Wc), req_off, R, BR,
+                     row_tiles_bound(R, Q, BR), tiles, n_tiles);
+  return hipGetLastError();
 }
 
 bool tail_supported(int dtype, int K0, int N1, int N2, int n_out) {

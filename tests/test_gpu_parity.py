@@ -309,6 +309,35 @@ def test_parity_many_requests(name):
     compare_scores(cfg, g["scores"], o["scores"], f"many requests {name}")
 
 
+def test_parity_topk_many_requests():
+    """1,100 small requests (0-3 ads each) of the top-k model: more requests
+    than one block of the scan that lays out the first layer's row tiles
+    (each request's rows keep only its k groups, so no tile spans two
+    requests), most tiles of one to three rows. Every request keeps exactly
+    k groups; where the checker's importance leaves a clear gap at the k-th
+    group (1e-4), the mask is bit-exact and the scores match."""
+    cfg = mid("wide_prune_bf16")
+    cand = [int(c) for c in np.random.default_rng(17).integers(0, 4, size=1100)]
+    log(f"test_parity_topk_many_requests: Q={len(cand)} R={sum(cand)}")
+    tables, params, batch = problem(cfg, seed=35, cand=cand, model_seed=cfg.seed)
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_s=True, want_mask=True)
+    finally:
+        run.close()
+    o = run_oracle(cfg, tables, params, batch, want_s=True, want_z=True)
+    assert np.all(g["mask"].sum(axis=1) == cfg.topk_k)
+    off = batch["req_off"]
+    nonempty = [q for q in range(len(off) - 1) if off[q + 1] > off[q]]
+    clear = [q for q in nonempty if mask_gap(o["importance"], cfg.topk_k, [q]) > 1e-4]
+    log(f"{len(clear)} of {len(nonempty)} non-empty requests with a clear top-k gap")
+    assert len(clear) >= len(nonempty) // 2
+    assert np.array_equal(g["mask"][clear], o["mask"][clear])
+    rows = np.concatenate([np.arange(off[q], off[q + 1]) for q in clear])
+    assert_se_weights_close(params, g["s"], o)
+    compare_scores(cfg, g["scores"][rows], o["scores"][rows], "top-k, many requests")
+
+
 @pytest.mark.parametrize("name", ["tiny_fp32", "serving_bf16", "multivalued_fp16_ll",
                                   "wide_prune_bf16"])
 def test_parity_literal_se(name):
