@@ -43,7 +43,8 @@ def log(msg):
 def stage_work(cfg, batch, stage, compact=False):
     """Algorithmic work of one launch of a stage: ('hbm', bytes) or
     ('mfma', flops). compact: the top-k model's network input keeps only
-    each request's k groups (the first layer runs on k * d inputs)."""
+    each request's k groups (the first layer runs on k * d inputs; the
+    call has an apply_compact stage)."""
     es = {"f32": 4, "bf16": 2, "f16": 2}[cfg.dtype]
     idb = 8 if cfg.hashed else 4
     R, Q = batch["n_rows"], len(batch["req_off"]) - 1
@@ -63,12 +64,12 @@ def stage_work(cfg, batch, stage, compact=False):
     if stage == "se_rows":      # squeeze read, SE weights written
         return "hbm", 2 * R * m * 4
     kin = min(cfg.topk_k, m) * d if compact else cfg.d_in   # width of the network input
-    if stage == "apply":
-        if compact:              # kept groups read, compacted rows written, SE weights read
-            return "hbm", 2 * R * kin * es + R * m * 4
-        return "hbm", 2 * R * cfg.d_in * es + R * m * 4   # rows read and written in place
-    if stage == "weight_cols":   # each request's columns of the first layer's weights
-        return "hbm", 2 * Q * cfg.widths[1] * kin * es + Q * min(cfg.topk_k, m) * 4
+    if stage == "apply":        # rows read and written in place, SE weights read
+        return "hbm", 2 * R * cfg.d_in * es + R * m * 4
+    if stage == "apply_compact":
+        # kept groups read, compacted rows written, SE weights read; each
+        # request's columns of the first layer's weights read and written
+        return "hbm", 2 * R * kin * es + R * m * 4 + 2 * Q * cfg.widths[1] * kin * es
     if stage == "gather_raw":
         # ids + gathered ad/cross rows + the fp32 concatenated embedding written
         return "hbm", R * nax * (idb + d * es) + R * cfg.d_in * 4 + Q * nus * d * 4
@@ -495,10 +496,10 @@ def _stage_of(kernel_name, dense_index):
         return "gather_se"
     if "se_rows_kernel" in kernel_name:
         return "se_rows"
-    if "apply_weights_kernel" in kernel_name or "apply_compact_kernel" in kernel_name:
+    if "apply_weights_kernel" in kernel_name:
         return "apply"
-    if "gather_weight_cols" in kernel_name:
-        return "weight_cols"
+    if "apply_compact_kernel" in kernel_name:
+        return "apply_compact"
     if "dense_f32" in kernel_name:
         return "se_dense"
     if "dense_tail_kernel" in kernel_name:
@@ -868,7 +869,7 @@ def main():
     log(f"with stage events: {ms_profiled:.4f} ms/step")
 
     stage_rows = []
-    compact = any(name == "weight_cols" for name, _ in stages)
+    compact = any(name == "apply_compact" for name, _ in stages)
     for name, tot in stages:
         ms = tot / max(n_calls, 1)
         e = roofline_entry(cfg, batch, name, ms, compact)

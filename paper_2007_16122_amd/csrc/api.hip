@@ -576,18 +576,14 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
                                      kept, s)) != hipSuccess)
       return hip_fail(m, e, "group_mask launch");
     if (compact) {
-      // every request's columns of the first layer's weights (and the
-      // layer's row tiles), and the rows' kept groups reweighted into the
-      // compacted input
-      if ((e = marks.mark("weight_cols")) != hipSuccess) return hip_fail(m, e, "profile event");
-      if ((e = launch_gather_weight_cols(m->dtype, A + al.w[0], m->widths[1], m->D_in, kept, Q,
-                                         kept_groups(*m), m->d, W + wl.Wc, b->req_off, R,
-                                         reinterpret_cast<RowTile *>(W + wl.rtiles),
-                                         reinterpret_cast<int32_t *>(W + wl.n_rtiles), s)) != hipSuccess)
-        return hip_fail(m, e, "weight columns launch");
-      if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");
+      // the rows' kept groups reweighted into the compacted input, every
+      // request's columns of the first layer's weights and the layer's row
+      // tiles, in one launch
+      if ((e = marks.mark("apply_compact")) != hipSuccess) return hip_fail(m, e, "profile event");
       if ((e = launch_apply_compact(m->dtype, D.linear_log, W + wl.X, W + wl.Xc, sb, kept, b->req_off,
-                                    Q, R, m->M, kept_groups(*m), m->d, s)) != hipSuccess)
+                                    Q, R, m->M, kept_groups(*m), m->d, A + al.w[0], m->widths[1],
+                                    W + wl.Wc, reinterpret_cast<RowTile *>(W + wl.rtiles),
+                                    reinterpret_cast<int32_t *>(W + wl.n_rtiles), s)) != hipSuccess)
         return hip_fail(m, e, "apply launch");
     } else {
       if ((e = marks.mark("apply")) != hipSuccess) return hip_fail(m, e, "profile event");

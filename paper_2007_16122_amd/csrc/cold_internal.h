@@ -229,12 +229,7 @@ hipError_t launch_group_mask_tiles(const float *s_buf, const float *tile_part,
                                    const int32_t *req_off, int64_t Q, int64_t R, int32_t M,
                                    int32_t k, uint8_t *mask, uint8_t *mask_out, int32_t *kept,
                                    hipStream_t s);
-// Xc [R][kp*d]: the kp kept groups of each row's request (kept [Q][kp]) taken
-// from the gathered rows Xraw [R][M*d], times s [R][M], linear_log when ll,
-// rounded once to the storage type
-hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, const float *s_buf,
-                                const int32_t *kept, const int32_t *req_off, int64_t Q, int64_t R,
-                                int32_t M, int32_t kp, int32_t d, hipStream_t s);
+
 // floats of the two packed SE operands (0 when M or H is beyond the kernel)
 void se_rows_packed_floats(int32_t M, int32_t H, size_t *n1, size_t *n2);
 // W1 [H][M] and W2 [M][H] into the row-wise SE kernel's operand order
@@ -260,21 +255,74 @@ struct RowTile {
 };
 // entries of the row-tile table for R rows in Q requests (any tile height)
 inline int64_t row_tile_capacity(int64_t R, int64_t Q) { return (R + 63) / 64 + Q + 1; }
-// Wc [Q][N][kp*d]: for every request q, the columns of W [N][K] (K = M*d)
-// of the groups kept[q][0..kp) in that order (storage type); the same launch
-// lays out the row tiles of launch_dense_relu_grouped for these R rows
-// (tiles [row_tile_capacity], n_tiles [1])
-hipError_t launch_gather_weight_cols(int dtype, const void *W, int32_t N, int32_t K,
-                                     const int32_t *kept, int64_t Q, int32_t kp, int32_t d,
-                                     void *Wc, const int32_t *req_off, int64_t R, RowTile *tiles,
-                                     int32_t *n_tiles, hipStream_t s);
+// Row tiles of height BR over requests: the bound on their count (request q
+// of n_q rows takes ceil(n_q / BR) <= (n_q + BR - 1) / BR tiles; exact for
+// one request, so a one-request batch has no idle workgroups).
+inline int64_t row_tiles_bound(int64_t R, int64_t Q, int BR) { return (R + Q * (BR - 1)) / BR; }
+
+// The table of those tiles, by one workgroup of NT threads: request q's rows
+// [lo, hi) (offsets clamped to [0, R]) take ceil((hi - lo) / BR) tiles, in
+// request order; entries past cap are not written (cap bounds the table and
+// the layer's grid whatever the offsets are). Requests in blocks of NT with
+// a running start.
+template <int NT>
+__device__ void build_row_tiles(const int32_t *__restrict__ req_off, int64_t Q, int64_t R, int BR,
+                                int64_t cap, RowTile *__restrict__ tiles,
+                                int32_t *__restrict__ n_tiles, int64_t *s_scan) {
+  const int tid = threadIdx.x;
+  int64_t start0 = 0;
+  for (int64_t base = 0; base < Q; base += NT) {
+    const int64_t q = base + tid;
+    int64_t lo = 0, hi = 0;
+    if (q < Q) {
+      lo = req_off[q];
+      hi = req_off[q + 1];
+      lo = lo < 0 ? 0 : (lo > R ? R : lo);
+      hi = hi < lo ? lo : (hi > R ? R : hi);
+    }
+    const int64_t c = (hi - lo + BR - 1) / BR;
+    s_scan[tid] = c;
+    __syncthreads();
+    for (int off = 1; off < NT; off <<= 1) {
+      const int64_t v = tid >= off ? s_scan[tid - off] : 0;
+      __syncthreads();
+      s_scan[tid] += v;
+      __syncthreads();
+    }
+    const int64_t start = start0 + s_scan[tid] - c;
+    for (int64_t t = 0; t < c && start + t < cap; ++t) {
+      const int64_t r = lo + t * BR;
+      RowTile e;
+      e.r0 = r;
+      e.n = (int32_t)(hi - r < BR ? hi - r : BR);
+      e.q = (int32_t)q;
+      tiles[start + t] = e;
+    }
+    start0 += s_scan[NT - 1];
+    __syncthreads();   // s_scan is rewritten by the next block of requests
+  }
+  if (tid == 0) n_tiles[0] = (int32_t)(start0 < cap ? start0 : cap);
+}
+
+// rows of the tile launch_dense_relu_grouped uses for R rows, N outputs and K inputs
+int dense_grouped_tile_rows(int64_t R, int32_t N, int32_t K);
 // Y = ReLU(X W_q^T + b) where row r of X [R][K] belongs to request q(r)
 // (req_off [Q+1]) and W_q = W + q * N * K; the row tiles never straddle two
-// requests (the table and count that launch_gather_weight_cols built for
-// the same R, Q, N and K).
+// requests (the table and count that launch_apply_compact built for the
+// same R, Q, N and K).
 // Same tile shapes and sum order as launch_dense_relu; bf16 and fp16 with
 // K % 32 == 0 and N % 8 == 0.
 bool dense_grouped_supported(int dtype, int32_t N, int32_t K);
+// Xc [R][kp*d]: the kp kept groups of each row's request (kept [Q][kp]) taken
+// from the gathered rows Xraw [R][M*d], times s [R][M], linear_log when ll,
+// rounded once to the storage type. The same launch writes Wc [Q][N][kp*d],
+// every request's columns of the first layer's weights W [N][M*d] for its
+// kept groups, and lays out the row tiles of launch_dense_relu_grouped for
+// these R rows (tiles [row_tile_capacity], n_tiles [1]).
+hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, const float *s_buf,
+                                const int32_t *kept, const int32_t *req_off, int64_t Q, int64_t R,
+                                int32_t M, int32_t kp, int32_t d, const void *W, int32_t N,
+                                void *Wc, RowTile *tiles, int32_t *n_tiles, hipStream_t s);
 hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, const float *b,
                                      void *y, int64_t R, int64_t Q, const int32_t *req_off,
                                      int32_t N, int32_t K, RowTile *tiles, int32_t *n_tiles,

@@ -2097,7 +2097,12 @@ static hipError_t apply_t(bool ll, void *X, const float *s_buf, const uint8_t *m
 // groups that q keeps (kept[q][j]), each 16-byte chunk round(LL(s[r][g] e))
 // of the gathered row (Eq. 3 when LL). The gathered rows stay in place; the
 // compacted rows go to Xc [R][kp * d]. A workgroup takes kApplyRows rows and
-// finds their requests and kept lists once, in LDS.
+// finds their requests and kept lists once, in LDS. The grid's next Q * N
+// workgroups copy, for request q, row n of the first layer's weights W
+// [N][M * d] restricted to the kept groups into Wc [Q][N][kp * d] (the
+// first layer's operand for that request), and its last one lays out the
+// first layer's row tiles (build_row_tiles) for the tile height that layer
+// uses.
 template <typename TS, bool LL>
 __global__ __launch_bounds__(256) void apply_compact_kernel(const TS *__restrict__ Xraw,
                                                             TS *__restrict__ Xc,
@@ -2106,10 +2111,33 @@ __global__ __launch_bounds__(256) void apply_compact_kernel(const TS *__restrict
                                                             const int32_t *__restrict__ req_off,
                                                             int64_t Q, int64_t R, int M, int kp,
                                                             int lcpg, int CPR, int CPRC,
-                                                            uint32_t mg_cprc) {
+                                                            uint32_t mg_cprc, int64_t n_apply,
+                                                            const uint4 *__restrict__ W, int64_t N,
+                                                            uint4 *__restrict__ Wc, int BR, int64_t cap,
+                                                            RowTile *__restrict__ tiles,
+                                                            int32_t *__restrict__ n_tiles) {
   constexpr int EPC = Elem<TS>::kPerChunk;
   __shared__ int32_t s_rq[kApplyRows];
   __shared__ int32_t s_kept[kApplyRows][256];
+  __shared__ int64_t s_scan[256];
+  if ((int64_t)blockIdx.x >= n_apply) {
+    const int64_t wrow = (int64_t)blockIdx.x - n_apply;
+    if (wrow == Q * N) {
+      build_row_tiles<256>(req_off, Q, R, BR, cap, tiles, n_tiles, s_scan);
+      return;
+    }
+    const int64_t q = wrow / N, n = wrow - q * N;
+    const int32_t *kq = kept + q * kp;
+    const uint4 *src = W + n * CPR;
+    uint4 *dst = Wc + wrow * CPRC;
+    for (int c = threadIdx.x; c < CPRC; c += 256) {
+      const int j = c >> lcpg, h = c & ((1 << lcpg) - 1);
+      int g = kq[j];
+      g = g < 0 ? 0 : (g < M ? g : M - 1);
+      dst[c] = src[(g << lcpg) + h];
+    }
+    return;
+  }
   const int64_t r0 = (int64_t)blockIdx.x * kApplyRows;
   const int rows = R - r0 < kApplyRows ? (int)(R - r0) : kApplyRows;
   if (threadIdx.x < rows) s_rq[threadIdx.x] = (int32_t)request_of_row(req_off, Q, r0 + threadIdx.x);
@@ -2159,33 +2187,46 @@ __global__ __launch_bounds__(256) void apply_compact_kernel(const TS *__restrict
 template <typename TS>
 static hipError_t apply_compact_t(bool ll, const void *Xraw, void *Xc, const float *s_buf,
                                   const int32_t *kept, const int32_t *req_off, int64_t Q,
-                                  int64_t R, int32_t M, int32_t kp, int32_t d, hipStream_t s) {
+                                  int64_t R, int32_t M, int32_t kp, int32_t d, const void *W,
+                                  int32_t N, void *Wc, RowTile *tiles, int32_t *n_tiles,
+                                  hipStream_t s) {
   constexpr int EPC = Elem<TS>::kPerChunk;
   const int cpg = d / EPC, cpr = M * cpg, cprc = kp * cpg;
-  if (cpg <= 0 || (cpg & (cpg - 1)) || kp <= 0 || kp > M || M > 256 ||
-      kApplyRows * (int64_t)cpr >= (1 << 16))
+  if (cpg <= 0 || (cpg & (cpg - 1)) || kp <= 0 || kp > M || M > 256 || N <= 0 || Q <= 0 ||
+      kApplyRows * (int64_t)cpr >= (1 << 16) || !dense_grouped_supported(
+          std::is_same<TS, float>::value ? kF32 : kBF16, N, kp * d))
     return hipErrorInvalidValue;
   const int lcpg = __builtin_ctz(cpg);
-  const dim3 grid((unsigned)((R + kApplyRows - 1) / kApplyRows));
+  const int64_t n_apply = (R + kApplyRows - 1) / kApplyRows;
+  const int64_t blocks = n_apply + Q * (int64_t)N + 1;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const int BR = dense_grouped_tile_rows(R, N, kp * d);
+  const int64_t cap = row_tiles_bound(R, Q, BR);
+  const dim3 grid((unsigned)blocks);
   if (ll)
     hipLaunchKernelGGL((apply_compact_kernel<TS, true>), grid, dim3(256), 0, s,
                        static_cast<const TS *>(Xraw), static_cast<TS *>(Xc), s_buf, kept, req_off,
-                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc));
+                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc), n_apply,
+                       static_cast<const uint4 *>(W), (int64_t)N, static_cast<uint4 *>(Wc), BR, cap,
+                       tiles, n_tiles);
   else
     hipLaunchKernelGGL((apply_compact_kernel<TS, false>), grid, dim3(256), 0, s,
                        static_cast<const TS *>(Xraw), static_cast<TS *>(Xc), s_buf, kept, req_off,
-                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc));
+                       Q, R, M, kp, lcpg, cpr, cprc, div_magic((uint32_t)cprc), n_apply,
+                       static_cast<const uint4 *>(W), (int64_t)N, static_cast<uint4 *>(Wc), BR, cap,
+                       tiles, n_tiles);
   return hipGetLastError();
 }
 
 hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, const float *s_buf,
                                 const int32_t *kept, const int32_t *req_off, int64_t Q, int64_t R,
-                                int32_t M, int32_t kp, int32_t d, hipStream_t s) {
+                                int32_t M, int32_t kp, int32_t d, const void *W, int32_t N,
+                                void *Wc, RowTile *tiles, int32_t *n_tiles, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   switch (dtype) {
-    case kF32: return apply_compact_t<float>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
-    case kBF16: return apply_compact_t<__bf16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
-    default: return apply_compact_t<_Float16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, s);
+    case kBF16: return apply_compact_t<__bf16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, W, N, Wc, tiles, n_tiles, s);
+    case kF16: return apply_compact_t<_Float16>(ll, Xraw, Xc, s_buf, kept, req_off, Q, R, M, kp, d, W, N, Wc, tiles, n_tiles, s);
+    default: return hipErrorInvalidValue;   // the grouped first layer is bf16 or fp16
   }
 }
 

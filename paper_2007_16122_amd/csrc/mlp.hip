@@ -1106,55 +1106,6 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
   return hipGetLastError();
 }
 
-// Row tiles of height BR over requests: the bound on their count (request q
-// of n_q rows takes ceil(n_q / BR) <= (n_q + BR - 1) / BR tiles; exact for
-// one request, so a one-request batch has no idle workgroups).
-static int64_t row_tiles_bound(int64_t R, int64_t Q, int BR) { return (R + Q * (BR - 1)) / BR; }
-
-// The table of those tiles, by one workgroup of NT threads: request q's rows
-// [lo, hi) (offsets clamped to [0, R]) take ceil((hi - lo) / BR) tiles, in
-// request order; entries past cap are not written (cap bounds the table and
-// the layer's grid whatever the offsets are). Requests in blocks of NT with
-// a running start.
-template <int NT>
-__device__ void build_row_tiles(const int32_t *__restrict__ req_off, int64_t Q, int64_t R, int BR,
-                                int64_t cap, RowTile *__restrict__ tiles,
-                                int32_t *__restrict__ n_tiles, int64_t *s_scan) {
-  const int tid = threadIdx.x;
-  int64_t start0 = 0;
-  for (int64_t base = 0; base < Q; base += NT) {
-    const int64_t q = base + tid;
-    int64_t lo = 0, hi = 0;
-    if (q < Q) {
-      lo = req_off[q];
-      hi = req_off[q + 1];
-      lo = lo < 0 ? 0 : (lo > R ? R : lo);
-      hi = hi < lo ? lo : (hi > R ? R : hi);
-    }
-    const int64_t c = (hi - lo + BR - 1) / BR;
-    s_scan[tid] = c;
-    __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {
-      const int64_t v = tid >= off ? s_scan[tid - off] : 0;
-      __syncthreads();
-      s_scan[tid] += v;
-      __syncthreads();
-    }
-    const int64_t start = start0 + s_scan[tid] - c;
-    for (int64_t t = 0; t < c && start + t < cap; ++t) {
-      const int64_t r = lo + t * BR;
-      RowTile e;
-      e.r0 = r;
-      e.n = (int32_t)(hi - r < BR ? hi - r : BR);
-      e.q = (int32_t)q;
-      tiles[start + t] = e;
-    }
-    start0 += s_scan[NT - 1];
-    __syncthreads();   // s_scan is rewritten by the next block of requests
-  }
-  if (tid == 0) n_tiles[0] = (int32_t)(start0 < cap ? start0 : cap);
-}
-
 // requests with weights of their own (see dense_relu_buf_kernel's GRP)
 struct GroupArgs {
   const int32_t *req_off;
@@ -1300,56 +1251,8 @@ hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, co
   return dense_mfma_dt<_Float16>(x, w, b, y, R, N, K, s, &ga);
 }
 
-// Wc [Q][N][kp * cpg chunks]: workgroup q * N + n copies row n of W's kept
-// columns for request q (its kp groups of cpg 16-byte chunks); the grid's
-// last workgroup lays out the first layer's row tiles (build_row_tiles) for
-// the tile height that layer will use.
-__global__ __launch_bounds__(256) void gather_weight_cols_kernel(const uint4 *__restrict__ W,
-                                                                 int64_t N, int32_t cpr,
-                                                                 const int32_t *__restrict__ kept,
-                                                                 int64_t Q, int32_t kp, int32_t lcpg,
-                                                                 uint4 *__restrict__ Wc,
-                                                                 const int32_t *__restrict__ req_off,
-                                                                 int64_t R, int BR, int64_t cap,
-                                                                 RowTile *__restrict__ tiles,
-                                                                 int32_t *__restrict__ n_tiles) {
-  __shared__ int64_t s_scan[256];
-  const int64_t row = blockIdx.x;
-  if (row == (int64_t)gridDim.x - 1) {
-    build_row_tiles<256>(req_off, Q, R, BR, cap, tiles, n_tiles, s_scan);
-    return;
-  }
-  const int64_t q = row / N, n = row - q * N;
-  const int cprc = kp << lcpg, ng = cpr >> lcpg;   // chunks of a compacted row; groups of W's
-  const int32_t *kq = kept + q * kp;
-  const uint4 *src = W + n * cpr;
-  uint4 *dst = Wc + row * cprc;
-  for (int c = threadIdx.x; c < cprc; c += 256) {
-    const int j = c >> lcpg, h = c & ((1 << lcpg) - 1);
-    int g = kq[j];
-    g = g < 0 ? 0 : (g < ng ? g : ng - 1);
-    dst[c] = src[(g << lcpg) + h];
-  }
-}
-
-hipError_t launch_gather_weight_cols(int dtype, const void *W, int32_t N, int32_t K,
-                                     const int32_t *kept, int64_t Q, int32_t kp, int32_t d,
-                                     void *Wc, const int32_t *req_off, int64_t R, RowTile *tiles,
-                                     int32_t *n_tiles, hipStream_t s) {
-  const int es = dtype == kF32 ? 4 : 2;
-  const int cpg = d * es / 16;
-  if (cpg <= 0 || (cpg & (cpg - 1)) || (d * es) % 16 || K % d || kp <= 0 || kp > K / d || Q <= 0)
-    return hipErrorInvalidValue;
-  const int Kc = kp * d;   // the first layer's inputs after compaction
-  if (!dense_grouped_supported(dtype, N, Kc)) return hipErrorInvalidValue;
-  const int BR = dense_tile_rows(dense_tile(R, N, Kc));
-  const int64_t rows = Q * (int64_t)N;
-  if (rows + 1 > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gather_weight_cols_kernel, dim3((unsigned)(rows + 1)), dim3(256), 0, s,
-                     static_cast<const uint4 *>(W), (int64_t)N, (int32_t)(K * es / 16), kept, Q, kp,
-                     (int32_t)__builtin_ctz(cpg), static_cast<uint4 *>(Wc), req_off, R, BR,
-                     row_tiles_bound(R, Q, BR), tiles, n_tiles);
-  return hipGetLastError();
+int dense_grouped_tile_rows(int64_t R, int32_t N, int32_t K) {
+  return dense_tile_rows(dense_tile(R, N, K));
 }
 
 bool tail_supported(int dtype, int K0, int N1, int N2, int n_out) {
