@@ -297,6 +297,15 @@ class ColdModel:
                           ad_ids=_ptr(batch["ad_ids"]), cross_ids=_ptr(batch["cross_ids"]),
                           seq_off=_ptr(batch.get("seq_off")), seq_ids=_ptr(batch.get("seq_ids")))
 
+    def prepare(self, batch: dict, scores, importance=None, group_mask=None, rows_out=None,
+                validate=False, workspace=None, x_out=None) -> "ScoreCall":
+        """The same call as score() on fixed device buffers, on the current
+        stream, prepared once: calling the result enqueues it (for serving
+        loops that reuse their input and output buffers; the buffers must
+        stay alive and in place)."""
+        return ScoreCall(self, batch, scores, importance, group_mask, rows_out, workspace, x_out,
+                         validate, self._stream())
+
     def score(self, batch: dict, scores=None, importance=None, group_mask=None, rows_out=None,
               validate=False, workspace=None, x_out=None):
         """Score every row; returns the fp32 score tensor (asynchronous on
@@ -314,6 +323,34 @@ class ColdModel:
         if st != COLD_OK:
             raise ColdError(st, "cold_score: " + cold_last_error(self.h))
         return scores
+
+
+class ScoreCall:
+    """One cold_score call on fixed buffers, ready to enqueue again and
+    again (see ColdModel.prepare): the batch struct, the pointers and the
+    stream are resolved once, so a call costs the C function alone."""
+
+    def __init__(self, model, batch, scores, importance, group_mask, rows_out, workspace, x_out,
+                 validate, stream):
+        self._keep = (model, batch, scores, importance, group_mask, rows_out, workspace, x_out)
+        self._b = model.make_batch_struct(batch)
+        ws = (model.ensure_workspace(self._b.n_rows, self._b.n_requests)
+              if workspace is None else workspace)
+        self._ws = ws
+        vp = ctypes.c_void_p
+        self._fn = lib().cold_score
+        self._h = model.h
+        self._args = (model.h, ctypes.byref(self._b), vp(_ptr(ws)), ctypes.c_size_t(ws.numel()),
+                      vp(_ptr(scores)), vp(_ptr(importance)), vp(_ptr(group_mask)),
+                      vp(_ptr(rows_out)), vp(_ptr(x_out)),
+                      ctypes.c_int32(COLD_SCORE_VALIDATE if validate else 0), vp(stream))
+        self.scores = scores
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != COLD_OK:
+            raise ColdError(st, "cold_score: " + cold_last_error(self._h))
+        return self.scores
 
 
 def batch_to_device(batch: dict, device="cuda") -> dict:

@@ -176,3 +176,27 @@ def test_concurrent_streams_with_distinct_workspaces():
         del graphs
     finally:
         model.close()
+
+
+def test_prepared_call_equals_score():
+    """A prepared call (binding.ColdModel.prepare: the batch struct,
+    pointers and stream resolved once) enqueued repeatedly, with the
+    request's ids replaced in place between calls, gives bit for bit the
+    scores of score() on the same ids."""
+    cfg, tables, params, batch, model = _setup("serving_bf16", [700, 0, 300, 1000], seed=61)
+    try:
+        a_np, b_np = _requests(cfg, batch, 0, 2), _requests(cfg, batch, 2, 4)
+        b_np = dict(b_np, ad_ids=b_np["ad_ids"][:, :a_np["n_rows"]],
+                    cross_ids=b_np["cross_ids"][:, :a_np["n_rows"]],
+                    req_off=np.array([0, 350, a_np["n_rows"]], np.int32), n_rows=a_np["n_rows"])
+        dev = B.batch_to_device(a_np, DEV)
+        scores = torch.empty(a_np["n_rows"], dtype=torch.float32, device=DEV)
+        call = model.prepare(dev, scores)
+        for src in (a_np, b_np, a_np):
+            _copy_batch_into(dev, src)
+            want = model.score(B.batch_to_device(src, DEV)).clone()
+            call()
+            torch.cuda.synchronize()
+            assert torch.equal(scores.view(torch.int32), want.view(torch.int32))
+    finally:
+        model.close()
