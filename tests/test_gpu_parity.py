@@ -442,6 +442,52 @@ def test_parity_topk_group_counts(fields, k):
     compare_scores(cfg, g["scores"], o["scores"], f"top-k M={cfg.n_groups}")
 
 
+@pytest.mark.parametrize("kw,cand", [(dict(dtype="f16", linear_log=True), [333, 0, 150]),
+                                     (dict(hashed=True, cross="gpu"), [333, 0, 150]),
+                                     (dict(), [2500, 0, 1800, 700]),
+                                     (dict(), [2000] * 16)])
+def test_parity_topk_compact_variants(kw, cand):
+    """The top-k path's compacted first layer (each request's kept groups
+    only, the layer on the matching weight columns, row tiles that never
+    span two requests) in its other forms: fp16 storage with linear_log,
+    hashed ids with GPU-built crosses, 4,999 rows in four requests (160-row
+    tiles, ragged per request) and 32,000 rows in 16 requests (256-row
+    tiles). Masks bit-exact and scores against the checker on a seeded
+    sample of rows (each request's first and last included), for the
+    requests whose checker importance leaves a clear gap at the k-th group."""
+    kw = dict(kw)
+    base = synth.CONFIGS["wide_prune_bf16"]
+    if kw.pop("cross", None) == "gpu":
+        kw["cross_pairs"] = tuple((f % base.n_user, (3 * f + 1) % base.n_ad) for f in range(base.n_cross))
+    cfg = mid("wide_prune_bf16", **kw)
+    log(f"test_parity_topk_compact_variants {kw} R={sum(cand)}")
+    tables, params, batch = problem(cfg, seed=49, cand=cand, model_seed=cfg.seed)
+    run = load(cfg, tables, params)
+    try:
+        g = run.score(batch, want_rows=True, want_s=True, want_mask=True)
+    finally:
+        run.close()
+    off = batch["req_off"]
+    rng = np.random.default_rng(59)
+    ends = np.concatenate([off[:-1], off[1:] - 1])
+    sample = np.unique(np.concatenate([rng.choice(batch["n_rows"], min(600, batch["n_rows"]),
+                                                  replace=False), ends]))
+    sample = sample[(sample >= 0) & (sample < batch["n_rows"])]
+    o = run_oracle(cfg, tables, params, batch, sample=sample, want_rows=True, want_s=True,
+                   want_z=True)
+    assert np.array_equal(g["rows"][:, sample], o["rows"].T.astype(np.int32)), "gather indices differ"
+    assert_se_weights_close(params, g["s"][sample], o)
+    assert np.all(g["mask"].sum(axis=1) == cfg.topk_k)
+    nonempty = [q for q in range(len(off) - 1) if off[q + 1] > off[q]]
+    clear = [q for q in nonempty if mask_gap(o["importance"], cfg.topk_k, [q]) > 1e-4]
+    log(f"{len(clear)} of {len(nonempty)} non-empty requests with a clear top-k gap")
+    assert len(clear) >= (len(nonempty) + 1) // 2
+    assert np.array_equal(g["mask"][clear], o["mask"][clear])
+    req_of = np.searchsorted(off, sample, side="right") - 1
+    keep = np.isin(req_of, clear)
+    compare_scores(cfg, g["scores"][sample][keep], o["scores"][keep], f"top-k compacted {kw}")
+
+
 @pytest.mark.parametrize("widths,n_req,cand", [((768, 384, 320, 256, 128, 64, 2), 12, 1993),
                                                ((768, 1024, 512, 256, 128, 64, 2), 2, 1993),
                                                ((768, 1024, 512, 256, 128, 64, 2), 5, 911),
