@@ -935,29 +935,50 @@ __global__ __launch_bounds__(128 * WN, MINB) void dense_tail_kernel(
   }
 }
 
-// fp32 layer: 64 x 64 output tile, 4 x 4 per thread, K in steps of 16.
+// fp32 layer: 64 x 64 output tile, 4 x 4 per thread, K in chunks of 128
+// staged in LDS; each thread loads its part of the next chunk into
+// registers before it computes on the current one, so a layer of K <= 128
+// costs one memory round trip, not one per 16-deep step. Sums over k in
+// index order.
+constexpr int kF32Chunk = 128;
 __global__ __launch_bounds__(256) void dense_relu_f32_kernel(const float *__restrict__ X,
                                                              const float *__restrict__ W,
                                                              const float *__restrict__ bias,
                                                              float *__restrict__ Y, int64_t R,
                                                              int N, int K, int relu) {
-  __shared__ float sx[16][64 + 1];
-  __shared__ float sw[16][64 + 1];
+  constexpr int KC = kF32Chunk, PER = 64 * KC / 256;   // elements of each operand per thread
+  __shared__ float sx[KC][64 + 1];
+  __shared__ float sw[KC][64 + 1];
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * 64;
   const int n0 = blockIdx.y * 64;
   const int tr = tid >> 4, tn = tid & 15;
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    for (int i = tid; i < 64 * 16; i += 256) {
-      const int row = i >> 4, kk = i & 15;
+  float vx[PER], vw[PER];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * 256;
+      const int row = i / KC, kk = i % KC;
       const int64_t r = r0 + row;
       const int n = n0 + row, k = k0 + kk;
-      sx[kk][row] = (r < R && k < K) ? X[r * K + k] : 0.0f;
-      sw[kk][row] = (n < N && k < K) ? W[(int64_t)n * K + k] : 0.0f;
+      vx[u] = (r < R && k < K) ? X[r * K + k] : 0.0f;
+      vw[u] = (n < N && k < K) ? W[(int64_t)n * K + k] : 0.0f;
+    }
+  };
+  load(0);
+  for (int k0 = 0; k0 < K; k0 += KC) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * 256;
+      const int row = i / KC, kk = i % KC;
+      sx[kk][row] = vx[u];
+      sw[kk][row] = vw[u];
     }
     __syncthreads();
-    for (int kk = 0; kk < 16; ++kk) {
+    if (k0 + KC < K) load(k0 + KC);
+    const int kn = K - k0 < KC ? K - k0 : KC;
+    for (int kk = 0; kk < kn; ++kk) {
       float xv[4], wv[4];
       for (int a = 0; a < 4; ++a) xv[a] = sx[kk][tr * 4 + a];
       for (int b = 0; b < 4; ++b) wv[b] = sw[kk][tn * 4 + b];
@@ -1055,6 +1076,15 @@ template <int ACT>
 static hipError_t launch_dense_f32_act(const float *x, const float *w, const float *b, float *y,
                                        int64_t R, int32_t N, int32_t K, hipStream_t s) {
   const unsigned gx = (unsigned)((R + 63) / 64);
+  // fewer 64-row blocks than CUs: one 16-wide output block per wave and the
+  // output blocks over the grid's second dimension, for more workgroups
+  // (the sum over k runs in the same order whatever a wave's blocks)
+  const int cus = device_cus() > 0 ? device_cus() : 256;
+  if ((int64_t)gx < cus && N > 16) {
+    hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 1>), dim3(gx, (unsigned)((N + 15) / 16)), dim3(256), 0, s,
+                       x, w, b, y, R, N, K);
+    return hipGetLastError();
+  }
   if (N <= 16) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 1>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
   else if (N <= 32) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 2>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
   else if (N <= 48) hipLaunchKernelGGL((dense_f32_mfma_kernel<ACT, 3>), dim3(gx, 1), dim3(256), 0, s, x, w, b, y, R, N, K);
@@ -1227,6 +1257,10 @@ hipError_t launch_dense_relu(int dtype, const void *x, const void *w, const floa
                              int64_t R, int32_t N, int32_t K, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   if (dtype == kF32) {
+    // fp32 models: the fp32 matrix cores when rows are whole 16-byte vectors
+    if (K % 4 == 0)
+      return launch_dense_f32(static_cast<const float *>(x), static_cast<const float *>(w), b,
+                              static_cast<float *>(y), R, N, K, 1, s);
     const dim3 grid((unsigned)((R + 63) / 64), (unsigned)((N + 63) / 64));
     hipLaunchKernelGGL(dense_relu_f32_kernel, grid, dim3(256), 0, s, static_cast<const float *>(x),
                        static_cast<const float *>(w), b, static_cast<float *>(y), R, N, K, 1);
