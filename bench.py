@@ -534,6 +534,10 @@ def _label_call(call):
     out, di = [], 0
     for r in call:
         st = _stage_of(r["Kernel_Name"], di)
+        # the fp32 matrix-core layer is the literal SE layer right after the
+        # raw gather, and a hidden layer of an fp32 model anywhere else
+        if st == "se_dense" and not (out and out[-1][0] == "gather_raw"):
+            st = f"dense{di}"
         if st and st.startswith("dense"):
             di += 1
         out.append([st, r])

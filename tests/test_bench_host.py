@@ -83,16 +83,34 @@ def test_trace_split_handles_demangled_names(tmp_path):
 
 def test_trace_split_of_the_topk_rows_path_and_register_gather(tmp_path):
     """The wide workload's passes (gather with squeeze, row-wise SE, one mask
-    kernel, reweighting) and the register-resident gathers of the other
-    workloads map to their stage names, one call each."""
+    kernel, compacted reweighting) and the register-resident gathers of the
+    other workloads map to their stage names, one call each; the fp32
+    matrix-core layer is the SE layer after the raw gather of the literal
+    Eq. 2 form and a hidden layer of an fp32 model otherwise."""
     wide = ["_ZN4cold16gather_se_kernelIDF16bLi4ELb0ELb0ELi8ELb0EEEvNS_10GatherArgsE",
             "void cold::se_rows_kernel<16>(float const*, float*, long, int, int, "
             "HIP_vector_type<float, 4u> const*, float const*, HIP_vector_type<float, 4u> const*, "
             "float const*, float*)",
             "cold::mask_select_tiles_kernel(float const*, float const*, int const*, long, int, int, "
-            "unsigned char*, unsigned char*)",
-            "_ZN4cold20apply_weights_kernelIDF16bLb0EEEvPT_PKfPKhPKilliiij",
+            "unsigned char*, unsigned char*, int*)",
+            "_ZN4cold20apply_compact_kernelIDF16bLb0EEEvPKT_PS1_PKfPKiS8_lliiiiijlPK15HIP_vector_"
+            "typeIjLj4EElPS9_ilPNS_7RowTileEPi",
             MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    tiny = ["void cold::gather_full_chain_kernel<float, false, false, true>(cold::GatherArgs)",
+            "void cold::dense_f32_mfma_kernel<1, 1>(float const*, float const*, float const*, "
+            "float*, long, int, int)",
+            "void cold::dense_f32_mfma_kernel<1, 1>(float const*, float const*, float const*, "
+            "float*, long, int, int)",
+            "void cold::head_kernel<float>(float const*, float const*, float const*, float*, long, "
+            "int, int)"]
+    literal = ["_ZN4cold16gather_se_kernelIfLi3ELb0ELb0ELi8ELb0EEEvNS_10GatherArgsE",
+               "void cold::dense_f32_mfma_kernel<2, 4>(float const*, float const*, float const*, "
+               "float*, long, int, int)",
+               "_ZN4cold16gather_se_kernelIfLi2ELb0ELb0ELi8ELb0EEEvNS_10GatherArgsE",
+               "void cold::dense_f32_mfma_kernel<1, 1>(float const*, float const*, float const*, "
+               "float*, long, int, int)",
+               "void cold::head_kernel<float>(float const*, float const*, float const*, float*, "
+               "long, int, int)"]
     serving = ["_ZN4cold16user_pool_kernelIDF16bLb0EEEvNS_10GatherArgsE",
                "_ZN4cold18gather_full_kernelIDF16bLb0ELb0ELi12ELb0EEEvNS_10GatherArgsE",
                MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
@@ -100,8 +118,10 @@ def test_trace_split_of_the_topk_rows_path_and_register_gather(tmp_path):
              "_ZN4cold24gather_full_split_kernelIDF16_Lb1ELb1ELb0EEEvNS_10GatherArgsE",
              MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
     for calls, want in [
-            ([wide, wide], ["gather_sq", "se_rows", "group_mask", "apply", "dense0", "dense1",
-                            "dense_tail"]),
+            ([wide, wide], ["gather_sq", "se_rows", "group_mask", "apply_compact", "dense0",
+                            "dense1", "dense_tail"]),
+            ([tiny, tiny], ["gather_se", "dense0", "dense1", "head"]),
+            ([literal], ["gather_raw", "se_dense", "gather_apply", "dense0", "head"]),
             ([serving, serving], ["user_pool", "gather_se", "dense0", "dense1", "dense_tail"]),
             ([large], ["user_pool", "gather_se", "dense0", "dense1", "dense_tail"])]:
         d = tmp_path / want[1] / str(len(calls))
