@@ -216,12 +216,13 @@ int cold_score(cold_model *model, const cold_batch *b, void *workspace, size_t w
  * ends; the other arguments as for cold_score.  The stream (NULL: the null
  * stream) must belong to the current device.  A batch whose
  * cold_workspace_bytes(R, Q) exceeds the array (the serving model: more
- * than five 2,000-ad requests) returns COLD_ERR_WORKSPACE with nothing
+ * than eight 2,000-ad requests; the wide top-k model's 5,000-row request
+ * fits) returns COLD_ERR_WORKSPACE with nothing
  * enqueued.  Every call on one GPU uses that GPU's one array, which keeps
  * the last call's contents: calls that overlap on one GPU (other streams,
  * other threads) race, so the caller serialises them.  Calls no allocating
  * routine; stage profiling does not record these calls. */
-#define COLD_NOALLOC_WORKSPACE_BYTES (64ull * 1024 * 1024)
+#define COLD_NOALLOC_WORKSPACE_BYTES (96ull * 1024 * 1024)
 int cold_score_noalloc(cold_model *model, const cold_batch *b, float *scores, float *importance,
                        uint8_t *group_mask, int32_t *rows_out, void *x_out, int32_t flags,
                        void *stream);

@@ -33,7 +33,7 @@ EXPORTS = ("cold_create_model", "cold_destroy_model", "cold_weight_arena_bytes",
            "cold_workspace_bytes", "cold_load_weights", "cold_score",
            "cold_status_string", "cold_last_error", "cold_profile_enable",
            "cold_profile_read", "cold_select_topn", "cold_score_noalloc")
-COLD_NOALLOC_WORKSPACE_BYTES = 64 * 1024 * 1024
+COLD_NOALLOC_WORKSPACE_BYTES = 96 * 1024 * 1024
 COLD_TOPN_MAX = 1024
 COLD_SE_SQUEEZE, COLD_SE_LITERAL = 0, 1
 

@@ -104,6 +104,35 @@ def test_sizes():
         B.cold_destroy_model(h)
 
 
+def test_noalloc_array_holds_one_wide_request():
+    """The no-allocation entry point's array holds the workspace of the wide
+    top-k model's 5,000-row request (compacted first-layer input and weight
+    columns included) and of eight 2,000-ad requests of the serving model."""
+    d, keep = desc(n_user=50, n_ad=100, n_cross=50, widths=[3200, 1024, 512, 256, 128, 64, 2],
+                   table_rows=[1000] * 200, topk_k=100)
+    h = B.cold_create_model(d)
+    try:
+        assert B.cold_workspace_bytes(h, 5000, 1) <= B.COLD_NOALLOC_WORKSPACE_BYTES
+        # the compacted input and weight columns are part of it
+        d2, keep2 = desc(n_user=50, n_ad=100, n_cross=50, widths=[3200, 1024, 512, 256, 128, 64, 2],
+                         table_rows=[1000] * 200, topk_k=200)
+        h2 = B.cold_create_model(d2)
+        try:
+            grow = B.cold_workspace_bytes(h, 5000, 1) - B.cold_workspace_bytes(h2, 5000, 1)
+            assert grow >= 2 * (5000 * 1600 + 1024 * 1600)
+        finally:
+            B.cold_destroy_model(h2)
+    finally:
+        B.cold_destroy_model(h)
+    d, keep = desc()
+    h = B.cold_create_model(d)
+    try:
+        assert B.cold_workspace_bytes(h, 16000, 8) <= B.COLD_NOALLOC_WORKSPACE_BYTES
+        assert B.cold_workspace_bytes(h, 18000, 9) > B.COLD_NOALLOC_WORKSPACE_BYTES
+    finally:
+        B.cold_destroy_model(h)
+
+
 def test_score_before_load_and_bad_calls():
     d, keep = desc()
     h = B.cold_create_model(d)
