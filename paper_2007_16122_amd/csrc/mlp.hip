@@ -272,7 +272,7 @@ template <int BR, int BN, int S, int WN, int KB = 32> struct BufTile {
 // (i, j), i.e. output features n0 + wn*(BN/WN) + 16 i + 4 (lane/16) + e of row
 // r0 + wr*(BR/2) + 16 j + lane % 16.  smem holds the ring (RING bytes); on
 // return the ring is free once the workgroup has passed a barrier.
-template <typename TS, int BR, int BN, int S, int WN, int KB = 32>
+template <typename TS, int BR, int BN, int S, int WN, int KB = 32, bool HALF = false>
 __device__ __forceinline__ void buf_tile_kloop(
     const TS *__restrict__ X, const TS *__restrict__ W, const float *__restrict__ bias, int64_t R,
     int N, int K, int64_t r0, int n0, unsigned char *smem,
@@ -330,7 +330,12 @@ __device__ __forceinline__ void buf_tile_kloop(
     for (int j = 0; j < RJ; ++j) acc[i][j] = bv;
   }
 
-  const int ksteps = K / KB;
+  // HALF (64-deep stages, K % 64 == 32): the last stage is a half stage;
+  // its second 32 of K lie past the rows' ends and are loaded (the next
+  // row's first elements, or zeros past the operand window) but not used,
+  // so the sum still runs over the same 32-deep K blocks in the same order
+  static_assert(!HALF || KB == 64, "half stages of 64-deep stages");
+  const int ksteps = HALF ? (K + KB - 1) / KB : K / KB;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < ksteps) issue(st, st);
@@ -358,6 +363,8 @@ __device__ __forceinline__ void buf_tile_kloop(
         const unsigned char *base = smem + st * STAGE;
 #pragma unroll
         for (int h = 0; h < KB / 32; ++h) {
+          if constexpr (HALF)
+            if (h > 0 && ks == ksteps - 1) break;   // the same for every wave
           frag fa[NI], fb[RJ];
 #pragma unroll
           for (int i = 0; i < NI; ++i)
@@ -392,7 +399,8 @@ __device__ __forceinline__ void buf_tile_kloop(
 // is entry tr of the device-built table (rows [r0, r0 + n) of request q,
 // whose weights start w_stride elements after the previous request's), and
 // workgroups past the table's count have no tile.
-template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2, int KB = 32, bool GRP = false>
+template <typename TS, int BR, int BN, int S, int WN = 2, int MINW = 2, int KB = 32, bool GRP = false,
+          bool HALF = false>
 __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS *__restrict__ X,
                                                                      const TS *__restrict__ W,
                                                                      const float *__restrict__ bias,
@@ -430,7 +438,7 @@ __global__ __launch_bounds__(128 * WN, MINW) void dense_relu_buf_kernel(const TS
   const int dn = (lane >> 4) * 4, dr = lane & 15;
 
   f32x4 acc[NI][RJ];
-  buf_tile_kloop<TS, BR, BN, S, WN, KB>(X, Wt, bias, R, N, K, r0, n0, smem, acc);
+  buf_tile_kloop<TS, BR, BN, S, WN, KB, HALF>(X, Wt, bias, R, N, K, r0, n0, smem, acc);
 
   // epilogue: round, ReLU, stage the tile in LDS, write rows with 16-byte
   // stores.
@@ -1145,20 +1153,20 @@ struct GroupArgs {
   int64_t w_stride;
 };
 
-template <typename TS, int BR, int BN, int S, int WN, int MINW, int KB = 32>
-static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void *y, int64_t R,
-                              int N, int K, hipStream_t s, const GroupArgs *ga = nullptr) {
+template <typename TS, int BR, int BN, int S, int WN, int MINW, int KB, bool HALF>
+static hipError_t dense_buf_launch(const void *x, const void *w, const float *b, void *y, int64_t R,
+                                   int N, int K, hipStream_t s, const GroupArgs *ga) {
   const int tiles_n = (N + BN - 1) / BN;
   const int64_t tiles_r = ga ? row_tiles_bound(R, ga->Q, BR) : (R + BR - 1) / BR;
   const int64_t total = tiles_r * tiles_n;
   if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
   if (ga) {
-    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB, true>), dim3((unsigned)total),
+    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB, true, HALF>), dim3((unsigned)total),
                        dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
                        static_cast<TS *>(y), R, N, K, tiles_n, (int)total, ga->tiles, ga->n_tiles,
                        ga->w_stride);
   } else {
-    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB>), dim3((unsigned)total),
+    hipLaunchKernelGGL((dense_relu_buf_kernel<TS, BR, BN, S, WN, MINW, KB, false, HALF>), dim3((unsigned)total),
                        dim3(128 * WN), 0, s, static_cast<const TS *>(x), static_cast<const TS *>(w), b,
                        static_cast<TS *>(y), R, N, K, tiles_n, (int)total,
                        static_cast<const RowTile *>(nullptr), static_cast<const int32_t *>(nullptr),
@@ -1167,27 +1175,37 @@ static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void
   return hipGetLastError();
 }
 
+// 64-deep stages take the half-stage variant when K % 64 == 32
+template <typename TS, int BR, int BN, int S, int WN, int MINW, int KB = 32>
+static hipError_t dense_buf_t(const void *x, const void *w, const float *b, void *y, int64_t R,
+                              int N, int K, hipStream_t s, const GroupArgs *ga = nullptr) {
+  if constexpr (KB == 64) {
+    if (K % 64 != 0) return dense_buf_launch<TS, BR, BN, S, WN, MINW, 64, true>(x, w, b, y, R, N, K, s, ga);
+  }
+  return dense_buf_launch<TS, BR, BN, S, WN, MINW, KB, false>(x, w, b, y, R, N, K, s, ga);
+}
+
 // The tile shape of a layer of R rows, N outputs and K inputs (the
 // buffered kernel for K % 32 == 0 and N % 8 == 0, else the plain one).
 //   Large batches: 256 x 256 tiles over 8 waves, in 64-deep stages (one
-// barrier per 64 MFMAs per wave, whole 128-byte rows per load) when K
-// allows (256 x 128 or 256 x 64 over 4 waves for narrower layers); batches
-// of a few thousand ads would leave most CUs idle with those, so 128..192 x
-// 128 tiles while 128-row tiles would still number one per CU, else 64 x 64.
+// barrier per 64 MFMAs per wave, whole 128-byte rows per load; a last half
+// stage when K % 64 == 32), or 256 x 128 and 256 x 64 over 4 waves in
+// 32-deep stages for narrower layers; batches of a few thousand ads would
+// leave most CUs idle with those, so 128..192 x 128 tiles while 128-row
+// tiles would still number one per CU, else 64 x 64.
 //   Every tile shape sums the same 32-deep K blocks in the same order, so the
 // outputs do not depend on the shape.
 enum class DTile {
-  k192x128, k160x128, k128x128_64, k128x128_32, k64x64_3s, k64x64_64, k64x64_32,
-  k256x256_64, k256x256_32, k256x128, k256x64, kPlain128, kPlain64
+  k192x128, k160x128, k128x128, k64x64_3s, k64x64, k256x256, k256x128, k256x64, kPlain128, kPlain64
 };
 
 static DTile dense_tile(int64_t R, int N, int K) {
   if (K % kBK != 0 || N % 8 != 0) return N % 128 == 0 ? DTile::kPlain128 : DTile::kPlain64;
   const int64_t big_tiles = ((R + 255) / 256) * ((N + 127) / 128);
   const int64_t mid_tiles = ((R + 127) / 128) * ((N + 127) / 128);
-  const bool k64 = K % 64 == 0;
+  // 64-deep stages for every K here (K % 32 == 0; a half stage ends K % 64 == 32)
   const int64_t cus = device_cus() > 0 ? device_cus() : 256;
-  if (big_tiles < 256 && mid_tiles >= 256 && k64 && N % 128 == 0) {
+  if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0) {
     // x 128 tiles with the row height that gives the least work to the
     // busiest CU (rounds of one tile per CU), provided the tiles still
     // cover three quarters of the CUs (fewer, smaller layers run faster on
@@ -1202,19 +1220,16 @@ static DTile dense_tile(int64_t R, int N, int K) {
     }
     if (best == 192) return DTile::k192x128;
     if (best == 160) return DTile::k160x128;
-    if (best == 128) return DTile::k128x128_64;
+    return DTile::k128x128;
   }
-  if (big_tiles < 256 && mid_tiles >= 256 && N % 128 == 0)
-    return k64 ? DTile::k128x128_64 : DTile::k128x128_32;
   if (big_tiles < 256) {
     // at most two tiles per CU: a third 64-deep stage in flight (the K steps
     // wait on load latency, not on the CU's throughput); more tiles than
     // that run better with the smaller ring, more workgroups per CU
     const int64_t small_tiles = ((R + 63) / 64) * ((N + 63) / 64);
-    if (k64 && small_tiles <= 2 * cus) return DTile::k64x64_3s;
-    return k64 ? DTile::k64x64_64 : DTile::k64x64_32;
+    return small_tiles <= 2 * cus ? DTile::k64x64_3s : DTile::k64x64;
   }
-  if (N % 256 == 0) return k64 ? DTile::k256x256_64 : DTile::k256x256_32;
+  if (N % 256 == 0) return DTile::k256x256;
   return N % 128 == 0 ? DTile::k256x128 : DTile::k256x64;
 }
 
@@ -1223,8 +1238,8 @@ static int dense_tile_rows(DTile t) {
   switch (t) {
     case DTile::k192x128: return 192;
     case DTile::k160x128: return 160;
-    case DTile::k128x128_64: case DTile::k128x128_32: return 128;
-    case DTile::k64x64_3s: case DTile::k64x64_64: case DTile::k64x64_32: return 64;
+    case DTile::k128x128: return 128;
+    case DTile::k64x64_3s: case DTile::k64x64: return 64;
     default: return 256;
   }
 }
@@ -1235,13 +1250,10 @@ static hipError_t dense_mfma_dt(const void *x, const void *w, const float *b, vo
   switch (dense_tile(R, N, K)) {
     case DTile::k192x128: return dense_buf_t<TS, 192, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
     case DTile::k160x128: return dense_buf_t<TS, 160, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k128x128_64: return dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k128x128_32: return dense_buf_t<TS, 128, 128, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k128x128: return dense_buf_t<TS, 128, 128, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
     case DTile::k64x64_3s: return dense_buf_t<TS, 64, 64, 3, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k64x64_64: return dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k64x64_32: return dense_buf_t<TS, 64, 64, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k256x256_64: return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s, ga);
-    case DTile::k256x256_32: return dense_buf_t<TS, 256, 256, 3, 4, 1>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k64x64: return dense_buf_t<TS, 64, 64, 2, 2, 2, 64>(x, w, b, y, R, N, K, s, ga);
+    case DTile::k256x256: return dense_buf_t<TS, 256, 256, 2, 4, 1, 64>(x, w, b, y, R, N, K, s, ga);
     case DTile::k256x128: return dense_buf_t<TS, 256, 128, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
     case DTile::k256x64: return dense_buf_t<TS, 256, 64, 3, 2, 2>(x, w, b, y, R, N, K, s, ga);
     case DTile::kPlain128:

@@ -500,10 +500,10 @@ def test_parity_layer_tile_shapes(widths, n_req, cand):
     256 x 64 tiles) on a batch large enough for 256-row tiles; batches of
     the serving widths with 3,986, 4,555 and 5,979 rows (128, 160 and 192 x
     128 tiles for the 1,024-wide layer, 64-row tiles of the fused last
-    layers). A 544-wide layer (256 x 64 tiles; 32-deep K steps into the
-    256-wide layer) keeps the tail in its own kernel: two workgroups per CU
-    on 6,000 rows, three on 72,000. Ragged last row tiles; checker on a
-    seeded sample of rows."""
+    layers). A 544-wide layer (256 x 64 tiles; 64-deep K steps ending in a
+    half step into the 256-wide layer) keeps the tail in its own kernel:
+    two workgroups per CU on 6,000 rows, three on 72,000. Ragged last row
+    tiles; checker on a seeded sample of rows."""
     cfg = mid("serving_bf16", widths=widths, n_requests=n_req, cand_per_request=cand)
     log(f"test_parity_layer_tile_shapes widths={widths} R={cfg.n_rows}")
     tables, params, batch = problem(cfg, seed=29, model_seed=cfg.seed)
@@ -602,7 +602,7 @@ def test_request_alone_equals_batch_bitwise(name, n_req):
 
 def test_many_tile_batch_equals_smaller_batch_bitwise():
     """With a layer before the tail that keeps the tail in its own kernel
-    (544 -> 256 in 32-deep K steps), a batch of more than four 64-row tiles
+    (544 -> 256, K % 64 == 32), a batch of more than four 64-row tiles
     per CU and a prefix of it give bit-identical scores for the shared
     rows: the tail kernel's sums do not depend on the number of tiles."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
