@@ -52,12 +52,16 @@ def _copy_batch_into(dst: dict, src_np: dict):
 
 @pytest.mark.parametrize("name,entry", [("serving_bf16", "cold_score"),
                                         ("multivalued_fp16_ll", "cold_score"),
-                                        ("serving_bf16", "cold_score_noalloc")])
+                                        ("wide_prune_bf16", "cold_score"),
+                                        ("serving_bf16", "cold_score_noalloc"),
+                                        ("wide_prune_bf16", "cold_score_noalloc")])
 def test_graph_replay_equals_eager(name, entry):
     """One 2,000-ad request's scoring call captured in a graph: every replay,
     with eager work and synchronisations between replays and the request's
     ids replaced in place between them, gives bit for bit the scores of
-    eager scoring of the same ids, which match the checker."""
+    eager scoring of the same ids, which match the checker (on the top-k
+    model each replay forms its request's mask, kept-group list, weight
+    columns and row-tile table on the device)."""
     cfg, tables, params, batch, model = _setup(name, [2000, 2000, 2000], seed=61)
     try:
         reqs = [request_slice(cfg, batch, q) for q in range(3)]
