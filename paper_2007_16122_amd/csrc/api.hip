@@ -640,7 +640,7 @@ int score_launch(cold_model *m, const cold_batch *b, unsigned char *W, float *sc
     if (l == 0 && compact)
       e = launch_dense_relu_grouped(m->dtype, W + wl.Xc, W + wl.Wc,
                                     reinterpret_cast<const float *>(A + al.b[0]), outp, R, Q,
-                                    b->req_off, m->widths[1], kept_groups(*m) * m->d,
+                                    m->widths[1], kept_groups(*m) * m->d,
                                     reinterpret_cast<RowTile *>(W + wl.rtiles),
                                     reinterpret_cast<int32_t *>(W + wl.n_rtiles), s);
     else

@@ -307,9 +307,9 @@ __device__ void build_row_tiles(const int32_t *__restrict__ req_off, int64_t Q, 
 // rows of the tile launch_dense_relu_grouped uses for R rows, N outputs and K inputs
 int dense_grouped_tile_rows(int64_t R, int32_t N, int32_t K);
 // Y = ReLU(X W_q^T + b) where row r of X [R][K] belongs to request q(r)
-// (req_off [Q+1]) and W_q = W + q * N * K; the row tiles never straddle two
-// requests (the table and count that launch_apply_compact built for the
-// same R, Q, N and K).
+// and W_q = W + q * N * K; the row tiles, which never straddle two
+// requests, come from the table and count that launch_apply_compact built
+// for the same R, Q, N and K.
 // Same tile shapes and sum order as launch_dense_relu; bf16 and fp16 with
 // K % 32 == 0 and N % 8 == 0.
 bool dense_grouped_supported(int dtype, int32_t N, int32_t K);
@@ -324,9 +324,8 @@ hipError_t launch_apply_compact(int dtype, bool ll, const void *Xraw, void *Xc, 
                                 int32_t M, int32_t kp, int32_t d, const void *W, int32_t N,
                                 void *Wc, RowTile *tiles, int32_t *n_tiles, hipStream_t s);
 hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, const float *b,
-                                     void *y, int64_t R, int64_t Q, const int32_t *req_off,
-                                     int32_t N, int32_t K, RowTile *tiles, int32_t *n_tiles,
-                                     hipStream_t s);
+                                     void *y, int64_t R, int64_t Q, int32_t N, int32_t K,
+                                     RowTile *tiles, int32_t *n_tiles, hipStream_t s);
 bool tail_supported(int dtype, int K0, int N1, int N2, int n_out);
 // the fused tail reads its two hidden layers' weights fragment-major
 // (mlp.hip, frag_offset): [N][K] row-major -> that order (N % 16 == 0, K % 32 == 0)

@@ -1146,7 +1146,6 @@ static hipError_t dense_mfma_t(const void *x, const void *w, const float *b, voi
 
 // requests with weights of their own (see dense_relu_buf_kernel's GRP)
 struct GroupArgs {
-  const int32_t *req_off;
   int64_t Q;
   RowTile *tiles;
   int32_t *n_tiles;
@@ -1287,12 +1286,11 @@ bool dense_grouped_supported(int dtype, int32_t N, int32_t K) {
 }
 
 hipError_t launch_dense_relu_grouped(int dtype, const void *x, const void *w, const float *b,
-                                     void *y, int64_t R, int64_t Q, const int32_t *req_off,
-                                     int32_t N, int32_t K, RowTile *tiles, int32_t *n_tiles,
-                                     hipStream_t s) {
+                                     void *y, int64_t R, int64_t Q, int32_t N, int32_t K,
+                                     RowTile *tiles, int32_t *n_tiles, hipStream_t s) {
   if (R <= 0 || Q <= 0) return hipSuccess;
   if (!dense_grouped_supported(dtype, N, K)) return hipErrorInvalidValue;
-  const GroupArgs ga{req_off, Q, tiles, n_tiles, (int64_t)N * K};
+  const GroupArgs ga{Q, tiles, n_tiles, (int64_t)N * K};
   if (dtype == kBF16) return dense_mfma_dt<__bf16>(x, w, b, y, R, N, K, s, &ga);
   return dense_mfma_dt<_Float16>(x, w, b, y, R, N, K, s, &ga);
 }
