@@ -148,6 +148,66 @@ def batching_curve(model, batch, cfg, sizes, iters, torch, binding):
     return out
 
 
+def time_workload(name, steps, warmup, torch, binding, synth, dev):
+    """One other workload, timed the way the main one is: inputs resident,
+    `warmup` untimed calls, then `steps` calls between two events with
+    nothing recorded between the kernels, and a second pass with an event
+    before every kernel stage for the per-stage times and rooflines."""
+    cfg = synth.CONFIGS[name]
+    batch = synth.make_batch(cfg, device=dev)
+    params = synth.make_params(cfg)
+    tables = [synth.table_torch(cfg, g, device=dev) for g in range(cfg.n_groups)]
+    model = binding.ColdModel(cfg, device=dev)
+    try:
+        model.load(tables, binding.params_to_device(params, cfg.dtype, dev))
+        dev_batch = binding.batch_to_device(batch, dev)
+        R = batch["n_rows"]
+        scores = torch.empty(R, dtype=torch.float32, device=dev)
+        model.ensure_workspace(R, len(batch["req_off"]) - 1)
+        for _ in range(warmup):
+            model.score(dev_batch, scores=scores)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(scores).all()), f"non-finite scores ({name})"
+        stream = torch.cuda.current_stream()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(steps):
+            model.score(dev_batch, scores=scores)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / steps
+        binding.cold_profile_enable(model.h, True)
+        for _ in range(steps):
+            model.score(dev_batch, scores=scores)
+        torch.cuda.synchronize()
+        stages, n_calls = binding.cold_profile_read(model.h)
+        binding.cold_profile_enable(model.h, False)
+    finally:
+        model.close()
+    compact = any(st == "apply_compact" for st, _ in stages)
+    rows = []
+    for st, tot in stages:
+        e = roofline_entry(cfg, batch, st, tot / max(n_calls, 1), compact)
+        e.update(name=st, ms=tot / max(n_calls, 1))
+        rows.append(e)
+
+    def frac(bound):
+        part = [e for e in rows if e["bound"] == bound and not (bound == "hbm" and e["name"] == "head")]
+        t = sum(e["ms"] for e in part)
+        if not part or t <= 0:
+            return None
+        peak = part[0]["peak"] if bound == "hbm" else PEAK_MFMA_TFLOPS[cfg.dtype]
+        scale = 1e9 if bound == "hbm" else 1e12
+        return round(sum(e["work_per_launch"] for e in part) / (t * 1e-3) / scale / peak, 4)
+
+    out = {"workload": name, "rows": R, "dtype": cfg.dtype, "steps": steps,
+           "ms_per_step": round(ms, 5), "value": round(R / (ms * 1e-3), 1), "unit": "ads/s",
+           "stages_us": {e["name"]: round(e["ms"] * 1e3, 2) for e in rows},
+           "gather_se_hbm_frac": frac("hbm"), "mlp_mfma_frac": frac("mfma")}
+    log(f"{name}: {ms:.4f} ms/step, {out['value']:.4g} ads/s, stages {out['stages_us']}")
+    return out
+
+
 def latency(model, dev_batch, scores, iters, torch, graph):
     stream = torch.cuda.current_stream()
     times = []
@@ -574,6 +634,78 @@ def _last_call(rows, key_start="Start_Timestamp"):
     return _label_call(ours[starts[-1]:])
 
 
+def summarize_single_request(trace_dir, command):
+    """Per-kernel durations of the single-request scoring calls (the latency
+    loops: one 2,000-ad request of the serving model) from a rocprofv3
+    --kernel-trace CSV directory: median and 10th/90th percentiles per
+    kernel, the gaps between consecutive kernels and the span of a call.
+    A call starts at its pooling or gather kernel; calls of fewer than four
+    kernels or with a kernel of more than 200,000 threads (the whole batch)
+    are left out."""
+    import csv
+    import glob
+    import statistics
+    path = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = sorted((r for r in csv.DictReader(open(path)) if "cold" in r["Kernel_Name"]),
+                  key=lambda r: int(r["Start_Timestamp"]))
+
+    def short(n):
+        for k, v in (("user_pool", "user_pool"), ("gather_full", "gather_se"),
+                     ("gather_se", "gather_se"), ("dense_tail", "dense_tail"),
+                     ("mlp_tail", "tail"), ("dense_relu_buf", "dense")):
+            if k in n:
+                return v
+        return None
+
+    calls, cur = [], []
+    for r in rows:
+        st = short(r["Kernel_Name"])
+        if st is None:
+            continue
+        starts = st == "user_pool" or (st == "gather_se" and not (
+            cur and short(cur[-1]["Kernel_Name"]) == "user_pool"))
+        if starts and cur:
+            calls.append(cur)
+            cur = []
+        cur.append(r)
+    if cur:
+        calls.append(cur)
+    small = [c for c in calls if len(c) >= 4 and all(int(x["Grid_Size_X"]) <= 200000 for x in c)]
+    if not small:
+        return "no single-request calls in the trace\n"
+    names = []
+    for i, r in enumerate(small[0]):
+        st = short(r["Kernel_Name"])
+        if st == "dense":
+            st = "dense%d" % sum(1 for x in small[0][:i] if short(x["Kernel_Name"]) == "dense")
+        names.append(st)
+
+    def us(a, b):
+        return (int(a) - int(b)) / 1e3
+
+    def pct(v, f):
+        v = sorted(v)
+        return v[min(len(v) - 1, int(f * len(v)))]
+
+    out = ["# rocprofv3 kernel trace of single-request scoring calls (one 2,000-ad request "
+           "of the serving model, bf16)",
+           f"# command: {command}",
+           "# calls: the eager and HIP-graph latency loops; a call = " + ", ".join(names)
+           + " on 2,000 rows",
+           f"# {len(small)} single-request calls",
+           f"{'stage':12s} {'median_us':>9s} {'p10_us':>7s} {'p90_us':>7s}  grid  kernel"]
+    for i, nm in enumerate(names):
+        v = [us(c[i]["End_Timestamp"], c[i]["Start_Timestamp"]) for c in small if len(c) > i]
+        out.append(f"{nm:12s} {statistics.median(v):9.2f} {pct(v, .1):7.2f} {pct(v, .9):7.2f}  "
+                   f"{small[0][i]['Grid_Size_X']}  {small[0][i]['Kernel_Name'][:100]}")
+    gaps = [statistics.median([us(c[i]["Start_Timestamp"], c[i - 1]["End_Timestamp"])
+                               for c in small if len(c) > i]) for i in range(1, len(names))]
+    out.append("gaps between consecutive kernels, median us: " + ", ".join(f"{g:.2f}" for g in gaps))
+    out.append("first kernel start to last kernel end, median us: %.2f" % statistics.median(
+        [us(c[-1]["End_Timestamp"], c[0]["Start_Timestamp"]) for c in small]))
+    return "\n".join(out) + "\n"
+
+
 def summarize_trace(trace_dir, command):
     """Per-stage kernel durations (mean over the profiled calls) from a
     rocprofv3 --kernel-trace CSV directory."""
@@ -756,6 +888,10 @@ def main():
                     help="skip every measurement after the timed steps: the 2,000-ad latency, "
                          "the serving curves and the top-n selection (kernel-trace profiles of "
                          "the step only)")
+    ap.add_argument("--other-workloads",
+                    default="tiny_fp32,multivalued_fp16_ll,large_fp16_ll,wide_prune_bf16",
+                    help="comma-separated workloads also timed in the same run (step time, "
+                         "stage times, rooflines) and listed under other_workloads; '' for none")
     ap.add_argument("--serving-processes", default="",
                     help="only measure concurrent serving from this many processes (comma list), "
                          "each replaying a 2,000-ad request back to back, and print one JSON line")
@@ -768,6 +904,8 @@ def main():
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--summarize-single-request", metavar="DIR",
+                    help="summarise a kernel trace of the latency loops (single requests) and exit")
     ap.add_argument("--summarize-parity", metavar="DIR",
                     help="write profiles/parity_<workload>.txt from a GPU run's parity.jsonl "
                          "(tests with COLD_PARITY_LOG) and bench_<workload>.json files, and exit")
@@ -790,6 +928,9 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.profile_command), end="")
+        return
+    if args.summarize_single_request:
+        print(summarize_single_request(args.summarize_single_request, args.profile_command), end="")
         return
     if args.summarize_mfma:
         print(summarize_mfma(args.summarize_mfma, args.profile_command, args.workload, args.simds,
@@ -979,6 +1120,11 @@ def main():
         log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
         del src, dst
 
+    others = None
+    names = [w for w in args.other_workloads.split(",") if w and w != cfg.name]
+    if names and not args.no_latency:
+        others = [time_workload(w, args.steps, args.warmup, torch, binding, synth, dev) for w in names]
+
     cpu = parity = cpu1 = None
     if not args.no_cpu_baseline:
         cpu, parity, cpu1 = cpu_baseline(cfg, batch, params, args.cpu_seconds,
@@ -1022,6 +1168,7 @@ def main():
         "groups_sweep": sweep,
         "serving_streams": serving,
         "serving_batching": batching,
+        "other_workloads": others,
         "usable_requests_per_s": None if not batching else {
             f"p99<={lim}ms": max([e["requests_per_s"] for e in batching if e["p99_ms"] <= lim],
                                  default=None) for lim in (0.1, 0.5, 1.0)},

@@ -131,3 +131,36 @@ def test_trace_split_of_the_topk_rows_path_and_register_gather(tmp_path):
         assert [st for st, _ in bench._last_call(rows)] == want
         text = bench.summarize_trace(str(d), "cmd")
         assert f"# {len(calls)} calls profiled" in text
+
+
+def test_single_request_summary_keeps_the_small_calls(tmp_path):
+    """The latency-loop trace summary splits the trace into calls at the
+    gather kernel, keeps the calls whose kernels are all small (a 2,000-ad
+    request), and labels the dense layers in call order."""
+    one = ["void cold::gather_full_chain_kernel<__bf16, false, false, true>(cold::GatherArgs)",
+           MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    batch = ["_ZN4cold16user_pool_kernelIDF16bLb0EEEvNS_10GatherArgsE",
+             "_ZN4cold18gather_full_kernelIDF16bLb0ELb0ELi12ELb0EEEvNS_10GatherArgsE",
+             MANGLED["dense"], MANGLED["dense"], MANGLED["fused"]]
+    d = tmp_path / "lat"
+    d.mkdir()
+    path = os.path.join(d, "bench_kernel_trace.csv")
+    _write_trace(path, [batch, one, one, one])
+    rows = list(csv.DictReader(open(path)))
+    big = rows[1]["Kernel_Name"], rows[2]["Kernel_Name"]
+    with open(path, "w", newline="") as fh:   # the whole-batch call has a large grid
+        w = csv.DictWriter(fh, list(rows[0].keys()))
+        w.writeheader()
+        for i, r in enumerate(rows):
+            if 1 <= i <= 5:
+                r["Grid_Size_X"] = 512000
+            w.writerow(r)
+    assert big[0].startswith("_ZN4cold16user_pool")
+    text = bench.summarize_single_request(str(d), "cmd")
+    assert "# 3 single-request calls" in text
+    assert "a call = gather_se, dense0, dense1, dense_tail on 2,000 rows" in text
+    lines = {l.split()[0]: l.split() for l in text.splitlines() if l and not l.startswith(("#", "stage", "gaps", "first"))}
+    assert list(lines) == ["gather_se", "dense0", "dense1", "dense_tail"]
+    assert float(lines["dense1"][1]) == 0.5                       # median duration in us
+    assert "gaps between consecutive kernels, median us: 0.50, 0.50, 0.50" in text
+    assert "first kernel start to last kernel end, median us: 3.50" in text
