@@ -71,7 +71,7 @@ def sparse_host_tables(cfg, batch, sample, seed=None, scheme=None, whole_request
     return tabs
 
 
-class GpuRun:
+class GpuScorer:
     """A model loaded on the GPU for one configuration."""
 
     def __init__(self, cfg, tables_dev, params, device="cuda"):

@@ -9,7 +9,7 @@ import pytest
 
 from paper_2007_16122_amd import binding, synth
 from tests.common import assert_se_weights_close, problem
-from tests.gpu_common import (GpuRun, compare_scores, device_table_from_numpy, half_ulp, log,
+from tests.gpu_common import (GpuScorer, compare_scores, device_table_from_numpy, half_ulp, log,
                               record, request_slice, run_oracle, sparse_host_tables,
                               with_empty_sequences)
 
@@ -35,7 +35,7 @@ MID_CANDS = {"tiny_fp32": [300, 0, 1, 211], "serving_bf16": [257, 0, 1, 700],
 
 
 def load(cfg, tables, params):
-    return GpuRun(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
+    return GpuScorer(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
 
 
 def mask_gap(importance, k, nonempty):
@@ -372,7 +372,7 @@ def test_parity_full_size_sampled(name):
     batch = synth.make_batch(cfg, device=DEV)
     params = synth.make_params(cfg)
     tables_dev = [synth.table_torch(cfg, g, device=DEV) for g in range(cfg.n_groups)]
-    run = GpuRun(cfg, tables_dev, params, DEV)
+    run = GpuScorer(cfg, tables_dev, params, DEV)
     try:
         g = run.score(batch, want_rows=True, want_s=cfg.emit_importance, want_mask=cfg.topk_k > 0)
     finally:

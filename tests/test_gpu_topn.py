@@ -9,7 +9,7 @@ import pytest
 import oracle
 from paper_2007_16122_amd import binding, synth
 from tests.common import problem
-from tests.gpu_common import GpuRun, device_table_from_numpy, log, run_oracle
+from tests.gpu_common import GpuScorer, device_table_from_numpy, log, run_oracle
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -86,7 +86,7 @@ def test_recall_of_gpu_scores_against_checker_scores():
     base = synth.CONFIGS["serving_bf16"]
     cfg = synth.config("serving_bf16", vocab=20_000)
     tables, params, batch = problem(cfg, seed=31, cand=[2000] * 4, model_seed=cfg.seed)
-    run = GpuRun(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
+    run = GpuScorer(cfg, [device_table_from_numpy(t, cfg.dtype, DEV) for t in tables], params, DEV)
     try:
         g = run.score(batch)
     finally:
