@@ -148,6 +148,79 @@ def batching_curve(model, batch, cfg, sizes, iters, torch, binding):
     return out
 
 
+def gather_reference(cfg, batch, tables, iters, torch, dev):
+    """Context for the gather's ceiling, not part of the scoring path: the
+    table rows one scoring call reads (every group of every row, users' rows
+    per request), gathered into the same [rows, groups, dim] layout with no
+    SE block and no reweighting, from the tables laid end to end (each
+    table's rows keep their positions), by
+      - the plainest gather kernel (libcold_probe.so, include/cold_probe.h:
+        int64 indices, two threads per row each copying 16 bytes, coalesced
+        index reads and stores), which times the scattered row reads on
+        their own, and
+      - the vendor's generic gather, torch.index_select.
+    Models with direct ids, 32-byte rows and no sequence or GPU-built cross
+    groups only."""
+    import ctypes
+    from paper_2007_16122_amd import build as hip_build
+    if cfg.hashed or cfg.n_seq or cfg.cross_pairs or cfg.emb_dim * (4 if cfg.dtype == "f32" else 2) != 32:
+        return None
+    R, V = batch["n_rows"], cfg.vocab
+    off = torch.from_numpy(batch["req_off"].astype(np.int64)).to(dev)
+    q_of_row = torch.repeat_interleave(torch.arange(len(off) - 1, device=dev), off[1:] - off[:-1])
+
+    def col(ids, g):
+        return torch.from_numpy(np.ascontiguousarray(ids).astype(np.int64)).to(dev) + g * V
+
+    cols = [col(batch["user_ids"][f], f)[q_of_row] for f in range(cfg.n_user)]
+    cols += [col(batch["ad_ids"][f], cfg.n_user + f) for f in range(cfg.n_ad)]
+    cols += [col(batch["cross_ids"][f], cfg.n_user + cfg.n_ad + f) for f in range(cfg.n_cross)]
+    idx = torch.stack(cols, dim=1).reshape(-1).contiguous()
+    big = torch.cat(tables, 0)
+    want = torch.index_select(big, 0, idx)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e3
+
+    out = torch.empty_like(want)
+    vendor_us = timed(lambda: torch.index_select(big, 0, idx, out=out))
+    probe_us = None
+    if os.path.exists(hip_build.PROBE_LIB):
+        plib = ctypes.CDLL(hip_build.PROBE_LIB)
+        plib.cold_probe_row_gather.restype = ctypes.c_int
+        plib.cold_probe_row_gather.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        args = (big.data_ptr(), big.shape[0], idx.data_ptr(), out.data_ptr(), idx.numel(),
+                stream.cuda_stream)
+        out.zero_()
+
+        def run():
+            rc = plib.cold_probe_row_gather(*args)
+            if rc != 0:
+                raise RuntimeError(f"cold_probe_row_gather returned {rc}")
+
+        probe_us = timed(run)
+        if not torch.equal(out, want):
+            raise RuntimeError("the row-gather probe does not reproduce torch.index_select")
+    row_bytes = cfg.emb_dim * big.element_size()
+    del big, out, idx, want
+    return {"what": "the same table rows gathered into the same [rows, groups, dim] layout "
+                    "with no SE and no reweighting; context only",
+            "rows_gathered": R * cfg.n_groups,
+            "rows_and_output_bytes": 2 * R * cfg.n_groups * row_bytes,
+            "probe_us": None if probe_us is None else round(probe_us, 2),
+            "vendor_index_select_us": round(vendor_us, 2)}
+
+
 def time_workload(name, steps, warmup, torch, binding, synth, dev):
     """One other workload, timed the way the main one is: inputs resident,
     `warmup` untimed calls, then `steps` calls between two events with
@@ -1120,6 +1193,17 @@ def main():
         log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
         del src, dst
 
+    gref = None
+    if not args.no_latency:
+        gref = gather_reference(cfg, batch, tables, 20, torch, dev)
+        if gref:
+            gs = next((e for e in stage_rows if e["name"] == "gather_se"), None)
+            if gs:
+                gref["gather_se_us"] = round(gs["ms"] * 1e3, 2)
+            log(f"plain gather of the same rows: {gref['probe_us']} us (probe), "
+                f"{gref['vendor_index_select_us']} us (torch.index_select); "
+                f"gather_se {gref.get('gather_se_us')} us")
+
     others = None
     names = [w for w in args.other_workloads.split(",") if w and w != cfg.name]
     if names and not args.no_latency:
@@ -1169,6 +1253,7 @@ def main():
         "serving_streams": serving,
         "serving_batching": batching,
         "other_workloads": others,
+        "gather_reference": gref,
         "usable_requests_per_s": None if not batching else {
             f"p99<={lim}ms": max([e["requests_per_s"] for e in batching if e["p99_ms"] <= lim],
                                  default=None) for lim in (0.1, 0.5, 1.0)},

@@ -1,4 +1,5 @@
-"""Build libcold.so (HIP, gfx950) in-tree with hipcc."""
+"""Build libcold.so (HIP, gfx950) in-tree with hipcc, and beside it
+libcold_probe.so, the row-gather measurement aid (include/cold_probe.h)."""
 from __future__ import annotations
 
 import glob
@@ -10,6 +11,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libcold.so")
+PROBE_SRC = os.path.join(PKG, "probe", "row_gather.hip")
+PROBE_LIB = os.path.join(PKG, "libcold_probe.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -62,7 +65,22 @@ def build(verbose: bool = False) -> str:
         if res.returncode != 0:
             raise RuntimeError(f"hipcc link failed ({res.returncode}):\n{_filtered(res)}")
     os.replace(tmp, LIB)
+    build_probe(verbose)
     return LIB
+
+
+def build_probe(verbose: bool = False) -> str:
+    """Compile the row-gather measurement aid into ``libcold_probe.so``."""
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), PROBE_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {PROBE_SRC} ({res.returncode}):\n{_filtered(res)}")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":

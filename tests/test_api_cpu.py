@@ -193,3 +193,28 @@ def test_literal_se_arena_holds_the_full_layer():
     # that the squeeze form keeps
     grow = 4 * (48 * 768 + 48) - 4 * (2 * 12 * 48 + 12 + 2 * 48 * 12 + 48) - 2 * 4096
     assert sizes[B.COLD_SE_LITERAL] - sizes[B.COLD_SE_SQUEEZE] >= grow - 4 * 256
+
+
+def test_probe_library_exports_its_declared_symbol():
+    """libcold_probe.so (the row-gather measurement aid beside the scoring
+    library) exports what include/cold_probe.h declares, and rejects bad
+    arguments before anything is enqueued."""
+    from paper_2007_16122_amd import build as hip_build
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "cold_probe.h")).read(),
+                  flags=re.S)
+    names = sorted(set(re.findall(r"\b(cold_[a-z_]+)\s*\(", text)))
+    assert names == ["cold_probe_row_gather"]
+    out = subprocess.run(["nm", "-D", "--defined-only", hip_build.PROBE_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    assert set(names) <= set(re.findall(r"\bT (cold_[a-z_]+)\b", out))
+    L = ctypes.CDLL(hip_build.PROBE_LIB)
+    f = L.cold_probe_row_gather
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_void_p]
+    p = ctypes.c_void_p(16)          # never dereferenced: each call is rejected on the host
+    assert f(None, 10, p, p, 4, None) == -1
+    assert f(p, 0, p, p, 4, None) == -1
+    assert f(p, 10, p, p, -1, None) == -1
+    assert f(p, 10, None, p, 4, None) == -1
+    assert f(p, 10, p, p, 0, None) == 0   # nothing to gather: nothing enqueued
