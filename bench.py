@@ -830,6 +830,42 @@ def summarize_pmc(fetch_dir, write_dir, probe_mb, command, workload):
             "stages": stages, "sources": _source_hashes()}
 
 
+def summarize_probe(fetch_dir, write_dir, probe_mb, command):
+    """HBM bytes per dispatch of the row-gather probe (the gather's ceiling
+    measurement) from FETCH_SIZE and WRITE_SIZE runs, scaled so that the
+    plain copy of probe_mb MiB (the largest copy in the run) reads (writes)
+    exactly probe_mb MiB; beside it the fused gather's bytes from the
+    serving workload's traffic file."""
+    import csv
+    import glob
+    import statistics
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        copy_kib = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
+        factor = probe_mb * 1024.0 / copy_kib
+        vals = [float(r["Counter_Value"]) * factor * 1024.0 for r in rows
+                if "row_gather_probe_kernel" in r["Kernel_Name"]]
+        out[counter] = (statistics.median(vals), len(vals), factor)
+    fused = load_traffic("serving_bf16")
+    fg = fused["stages"].get("gather_se") if fused else None
+    f, w = out["FETCH_SIZE"][0], out["WRITE_SIZE"][0]
+    lines = ["# rocprofv3 HBM traffic of the row-gather probe (libcold_probe.so) on the rows of one",
+             "# scoring call of the serving workload (3,072,000 rows of 32 bytes gathered into the",
+             "# [rows, groups, dim] layout; int64 indices), beside the fused gather+SE of the same call",
+             f"# command: {command}",
+             f"# FETCH_SIZE scaled by {out['FETCH_SIZE'][2]:.3f}, WRITE_SIZE by "
+             f"{out['WRITE_SIZE'][2]:.3f} (the {probe_mb} MiB copy reads and writes {probe_mb} MiB);"
+             f" median over {out['FETCH_SIZE'][1]} dispatches",
+             f"{'kernel':28s} {'fetch_MB':>9s} {'write_MB':>9s} {'total_MB':>9s}",
+             f"{'row_gather_probe':28s} {f / 1e6:9.1f} {w / 1e6:9.1f} {(f + w) / 1e6:9.1f}"]
+    if fg:
+        lines.append(f"{'gather_se (fused, profiles)':28s} {fg['fetch_bytes'] / 1e6:9.1f} "
+                     f"{fg['write_bytes'] / 1e6:9.1f} {(fg['fetch_bytes'] + fg['write_bytes']) / 1e6:9.1f}")
+    return "\n".join(lines) + "\n"
+
+
 def summarize_mfma(pmc_dir, command, workload, simds, xcds):
     """Matrix-core utilisation per stage from one rocprofv3 run with
     SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: the first summed over all
@@ -977,6 +1013,8 @@ def main():
                     help="print a per-stage summary of a rocprofv3 kernel-trace run and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_<workload>.json from FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--summarize-probe", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise FETCH_SIZE/WRITE_SIZE runs of the row-gather probe and exit")
     ap.add_argument("--summarize-single-request", metavar="DIR",
                     help="summarise a kernel trace of the latency loops (single requests) and exit")
     ap.add_argument("--summarize-parity", metavar="DIR",
@@ -1001,6 +1039,10 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.profile_command), end="")
+        return
+    if args.summarize_probe:
+        print(summarize_probe(args.summarize_probe[0], args.summarize_probe[1],
+                              args.copy_probe_mb or 1024, args.profile_command), end="")
         return
     if args.summarize_single_request:
         print(summarize_single_request(args.summarize_single_request, args.profile_command), end="")

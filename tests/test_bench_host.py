@@ -164,3 +164,31 @@ def test_single_request_summary_keeps_the_small_calls(tmp_path):
     assert float(lines["dense1"][1]) == 0.5                       # median duration in us
     assert "gaps between consecutive kernels, median us: 0.50, 0.50, 0.50" in text
     assert "first kernel start to last kernel end, median us: 3.50" in text
+
+
+def test_probe_traffic_summary_scales_by_the_largest_copy(tmp_path):
+    """The probe's counter summary scales each counter so that the largest
+    copy (the 1 GiB probe copy) moves exactly its size, and takes the median
+    over the probe's dispatches."""
+    dirs = []
+    for counter, copy_kib, probe_kib in (("FETCH_SIZE", 524288.0, [1000.0, 1000.0, 5000.0]),
+                                         ("WRITE_SIZE", 1048576.0, [2000.0, 2000.0, 2000.0])):
+        d = tmp_path / counter
+        d.mkdir()
+        with open(os.path.join(d, "bench_counter_collection.csv"), "w", newline="") as fh:
+            w = csv.DictWriter(fh, ["Kernel_Name", "Counter_Name", "Counter_Value"])
+            w.writeheader()
+            w.writerow({"Kernel_Name": "__amd_rocclr_copyBuffer", "Counter_Name": counter,
+                        "Counter_Value": 12.0})
+            w.writerow({"Kernel_Name": "__amd_rocclr_copyBuffer", "Counter_Name": counter,
+                        "Counter_Value": copy_kib})
+            for v in probe_kib:
+                w.writerow({"Kernel_Name": "(anonymous namespace)::row_gather_probe_kernel(...)",
+                            "Counter_Name": counter, "Counter_Value": v})
+        dirs.append(str(d))
+    text = bench.summarize_probe(dirs[0], dirs[1], 1024, "cmd")
+    assert "FETCH_SIZE scaled by 2.000, WRITE_SIZE by 1.000" in text
+    assert "median over 3 dispatches" in text
+    row = [l.split() for l in text.splitlines() if l.startswith("row_gather_probe")][0]
+    assert float(row[1]) == round(2000.0 * 1024 / 1e6, 1)   # fetch MB: 1000 KiB x 2
+    assert float(row[2]) == round(2000.0 * 1024 / 1e6, 1)   # write MB: 2000 KiB x 1
